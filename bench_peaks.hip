@@ -1,0 +1,90 @@
+// Microbenchmarks of the MI355X ceilings the convolution is measured against:
+// fp32 matrix-core throughput (v_mfma_f32_16x16x4_f32), fp32 vector FMA
+// throughput, HBM copy bandwidth and the cost of an empty launch.  Built into
+// bench_peaks.so next to bench.py; used only by `bench.py --peaks`.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+// Every wave keeps 16 independent 16x16 accumulators busy for `iters` rounds.
+// clk[2*blockIdx.x] / clk[2*blockIdx.x+1]: shader-clock and 100 MHz wall-clock
+// ticks over the loop, read by thread 0.
+__global__ __launch_bounds__(256) void peak_mfma_f32(float *out, uint64_t *clk, int iters)
+{
+    floatx4 acc[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) acc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
+    const float a = 1e-3f * (float)(threadIdx.x & 7);
+    const float b = 1.0f + 1e-3f * (float)(threadIdx.x >> 6);
+    const uint64_t c0 = clock64();
+    const uint64_t w0 = wall_clock64();
+    for (int i = 0; i < iters; ++i) {
+#pragma unroll
+        for (int j = 0; j < 16; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc[j], 0, 0, 0);
+    }
+    const uint64_t c1 = clock64();
+    const uint64_t w1 = wall_clock64();
+    float s = 0.f;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) s += acc[j][0] + acc[j][1] + acc[j][2] + acc[j][3];
+    out[(size_t)blockIdx.x * 256 + threadIdx.x] = s;
+    if (threadIdx.x == 0) {
+        clk[2 * blockIdx.x] = c1 - c0;
+        clk[2 * blockIdx.x + 1] = w1 - w0;
+    }
+}
+
+// 16 independent fp32 FMA chains per lane.
+__global__ __launch_bounds__(256) void peak_valu_fma(float *out, int iters)
+{
+    float x[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) x[j] = 1e-3f * (float)(threadIdx.x + j);
+    for (int i = 0; i < iters; ++i) {
+#pragma unroll
+        for (int j = 0; j < 16; ++j) x[j] = fmaf(x[j], 0.9999f, 1e-4f);
+    }
+    float s = 0.f;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) s += x[j];
+    out[(size_t)blockIdx.x * 256 + threadIdx.x] = s;
+}
+
+__global__ __launch_bounds__(256) void copy_f4(const float4 *__restrict__ src, float4 *__restrict__ dst, size_t n)
+{
+    size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+    const size_t step = (size_t)gridDim.x * 256;
+    for (; i < n; i += step) dst[i] = src[i];
+}
+
+__global__ void empty_kernel() {}
+
+extern "C" {
+
+int peak_mfma_launch(float *out, uint64_t *clk, int iters, int grid, hipStream_t s)
+{
+    hipLaunchKernelGGL(peak_mfma_f32, dim3(grid), dim3(256), 0, s, out, clk, iters);
+    return (int)hipGetLastError();
+}
+
+int peak_valu_launch(float *out, int iters, int grid, hipStream_t s)
+{
+    hipLaunchKernelGGL(peak_valu_fma, dim3(grid), dim3(256), 0, s, out, iters);
+    return (int)hipGetLastError();
+}
+
+// n16: number of 16-byte elements; src and dst 16-byte aligned, not overlapping.
+int copy_launch(const void *src, void *dst, size_t n16, int grid, hipStream_t s)
+{
+    hipLaunchKernelGGL(copy_f4, dim3(grid), dim3(256), 0, s, (const float4 *)src, (float4 *)dst, n16);
+    return (int)hipGetLastError();
+}
+
+int empty_launch(hipStream_t s)
+{
+    hipLaunchKernelGGL(empty_kernel, dim3(1), dim3(64), 0, s);
+    return (int)hipGetLastError();
+}
+
+}  // extern "C"

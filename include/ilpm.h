@@ -1,0 +1,178 @@
+/*
+ * ilpm.h -- batch-1 2-D convolution forward pass on AMD MI355X (gfx950).
+ *
+ * The operation (ILP-M, Section 4 and Algorithm 2 of "ILP-M Conv: Optimize
+ * Convolution Algorithm for Single-Image Convolution Neural Network Inference
+ * on Mobile GPUs"): every output pixel of every output channel accumulates,
+ * over all input channels and all K x K filter taps (r, s), the filter weight
+ * times the input pixel at (y + r, x + s) -- a cross-correlation, no filter
+ * flip.  The paper's algorithm is stride 1 with an implicit halo; this library
+ * adds the standard stride s, symmetric zero padding p and an optional
+ * per-output-channel bias:
+ *
+ *   H_out = floor((H + 2p - K) / s) + 1,  W_out = floor((W + 2p - K) / s) + 1
+ *   out[co][oh][ow] = bias[co]
+ *       + sum_{ci<C_in, kh<K, kw<K} w[co][ci][kh][kw] * x[ci][oh*s - p + kh][ow*s - p + kw]
+ *   (x read as 0 outside [0,H) x [0,W)).
+ *
+ * Arithmetic is fp32 in, fp32 accumulate (fp32 FMA or fp32 MFMA), fp32 out.
+ * The summation order is not the definition's; results agree with the exact
+ * sum to within 1e-4 * (1 + S / (C_in*K*K)), S = sum of |products|.
+ *
+ * Conventions for every entry point:
+ *   - Tensor pointers are DEVICE pointers to contiguous fp32 arrays, 4-byte
+ *     aligned, on the current HIP device.  The caller owns (allocates and
+ *     frees) them; the library keeps no tensor pointer after a call returns.
+ *   - Work is only enqueued on `stream` (NULL = the default stream); no call
+ *     synchronises the host.  A device-side fault shows up at the caller's
+ *     next synchronisation.
+ *   - Arguments are checked before anything is launched; on an error the
+ *     call returns a negative status and writes nothing.
+ *   - K in this library is the filter size; output channels are C_out.  (The
+ *     paper's Algorithm 2 uses K for the output channels.)
+ */
+#ifndef ILPM_H
+#define ILPM_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+enum {
+    ILPM_OK = 0,
+    ILPM_ERR_INVALID_ARG = -1, /* null pointer, dimension <= 0, stride <= 0, pad < 0,
+                                  no output pixel, out overlapping an input, bad plan */
+    ILPM_ERR_UNSUPPORTED = -2, /* a tensor above 2^31-1 elements */
+    ILPM_ERR_WORKSPACE = -3,   /* registered workspace smaller than the plan needs */
+    ILPM_ERR_HIP = -4,         /* a HIP runtime call or kernel launch failed */
+    ILPM_ERR_ARCH = -5         /* the current device is not gfx950 */
+};
+
+/* Kernel families. */
+enum {
+    ILPM_PATH_DIRECT = 0, /* VALU direct convolution: lanes on output pixels, a
+                             block of output channels per thread, taps outermost */
+    ILPM_PATH_IGEMM = 1   /* fp32-MFMA implicit GEMM: M = C_out, N = output pixels,
+                             K = C_in*K*K, input halo tiles staged in LDS */
+};
+
+/* How one call is executed (see ilpm_conv2d_plan). */
+typedef struct ilpm_plan {
+    int path;              /* ILPM_PATH_* */
+    int variant;           /* compiled kernel variant within the path */
+    int tile_h, tile_w;    /* output pixels per workgroup */
+    int co_tile;           /* output channels per workgroup */
+    int ci_chunk;          /* input channels staged in LDS per stage */
+    int splits;            /* input-channel splits across workgroups (1 = none) */
+    int grid;              /* workgroups launched */
+    int block;             /* threads per workgroup */
+    int lds_bytes;         /* LDS per workgroup */
+    int h_out, w_out;      /* output size */
+    size_t workspace_bytes;/* device workspace the plan needs (0 if none) */
+} ilpm_plan;
+
+/*
+ * ilpm_conv2d_fwd -- out = conv2d(in, w) + bias, batch 1.
+ *   in   [1, C_in, H, W]            NCHW, read only
+ *   w    [C_out, C_in, K, K]        OIHW, read only
+ *   bias [C_out] or NULL (no bias)  read only
+ *   out  [1, C_out, H_out, W_out]   NCHW, fully written; must not overlap the inputs
+ *   stride >= 1, pad >= 0, all sizes >= 1, H_out >= 1 and W_out >= 1.
+ * Picks the kernel with ilpm_conv2d_plan.  Plans with splits > 1 use the
+ * device workspace (registered with ilpm_set_workspace, else allocated by the
+ * library on first need); calls that overlap in time on one device and both
+ * use split plans must be ordered on one stream.
+ * Returns ILPM_OK or a negative status.
+ */
+int ilpm_conv2d_fwd(const float *in, const float *w, const float *bias,
+                    int C_in, int H, int W, int C_out, int K, int stride, int pad,
+                    float *out, hipStream_t stream);
+
+/*
+ * ilpm_conv2d_workspace_size -- bytes of device workspace the default plan
+ * for this shape needs (0 when it needs none).  Pure host; no device access.
+ */
+int ilpm_conv2d_workspace_size(int C_in, int H, int W, int C_out, int K, int stride, int pad,
+                               size_t *bytes);
+
+/*
+ * ilpm_set_workspace -- register caller-owned device memory (ptr, bytes) as
+ * the workspace of the current device, replacing any earlier one; ptr = NULL
+ * unregisters it (the library then allocates its own on need).  The memory is
+ * cleared on `stream`, must stay allocated while calls may use it, and must be
+ * 256-byte aligned.
+ */
+int ilpm_set_workspace(void *ptr, size_t bytes, hipStream_t stream);
+
+/* Text for a status code (static storage). */
+const char *ilpm_status_str(int status);
+
+/* The hipError_t value behind the calling thread's most recent ILPM_ERR_HIP
+ * (0 if there was none). */
+int ilpm_last_hip_error(void);
+
+/*
+ * ilpm_conv2d_validate -- the argument checks of ilpm_conv2d_fwd, on the host
+ * only (pointers are compared, never dereferenced).  Returns ILPM_OK,
+ * ILPM_ERR_INVALID_ARG or ILPM_ERR_UNSUPPORTED.
+ */
+int ilpm_conv2d_validate(const void *in, const void *w, const void *bias,
+                         int C_in, int H, int W, int C_out, int K, int stride, int pad,
+                         const void *out);
+
+/*
+ * ilpm_conv2d_plan -- the plan ilpm_conv2d_fwd uses for this shape (path,
+ * tile, split count, grid, workspace).  Pure host.  The environment variables
+ * ILPM_FORCE_PATH=direct|igemm and ILPM_SPLIT=n override the choice.
+ */
+int ilpm_conv2d_plan(int C_in, int H, int W, int C_out, int K, int stride, int pad,
+                     ilpm_plan *plan);
+
+/*
+ * ilpm_conv2d_plan_variant -- a plan that runs compiled variant `variant` of
+ * `path` with `splits` input-channel splits (0 = choose).  Pure host.  Returns
+ * ILPM_ERR_INVALID_ARG when the variant does not exist or does not support the
+ * filter size and stride.
+ */
+int ilpm_conv2d_plan_variant(int C_in, int H, int W, int C_out, int K, int stride, int pad,
+                             int path, int variant, int splits, ilpm_plan *plan);
+
+/* Number of compiled variants of `path` (0 for an unknown path). */
+int ilpm_num_variants(int path);
+
+/*
+ * ilpm_variant_info -- filter size, stride (0 = any), output tile and output
+ * channels per workgroup of one compiled variant.  Pure host.
+ */
+int ilpm_variant_info(int path, int variant, int *K, int *stride, int *tile_h, int *tile_w,
+                      int *co_tile);
+
+/*
+ * ilpm_conv2d_fwd_plan -- ilpm_conv2d_fwd with an explicit plan (from
+ * ilpm_conv2d_plan or ilpm_conv2d_plan_variant for the same shape).
+ */
+int ilpm_conv2d_fwd_plan(const float *in, const float *w, const float *bias,
+                         int C_in, int H, int W, int C_out, int K, int stride, int pad,
+                         float *out, const ilpm_plan *plan, hipStream_t stream);
+
+/* ---- helpers for layer stacks (not part of the convolution) ---- */
+
+/* x[i] = max(x[i], 0) for i < n, in place.  x: device fp32, n >= 0. */
+int ilpm_relu_inplace(float *x, int64_t n, hipStream_t stream);
+
+/*
+ * ilpm_maxpool2x2 -- out[c][i][j] = max of in[c][2i..2i+1][2j..2j+1];
+ * in [C, H, W] -> out [C, H/2, W/2] (floor).  Requires H, W >= 2; no overlap.
+ */
+int ilpm_maxpool2x2(const float *in, int C, int H, int W, float *out, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ILPM_H */

@@ -1,0 +1,83 @@
+"""Build libilpm.so (the HIP kernels and the C ABI) for gfx950 with hipcc.
+
+    python -m paper_1909_02765_amd.build            # build in-tree
+    python -m paper_1909_02765_amd.build --isa DIR  # also keep the gfx950 assembly in DIR
+"""
+from __future__ import annotations
+
+import argparse
+import glob
+import os
+import shutil
+import subprocess
+import sys
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG)
+CSRC = os.path.join(PKG, "csrc")
+INCLUDE = os.path.join(ROOT, "include")
+LIBRARY = os.path.join(PKG, "libilpm.so")
+
+ARCH = "gfx950"
+# Packed fp32 VALU instructions stay disabled: the compiler forms them on its
+# own from scalar float code, and they are not needed here (the dense path
+# uses the fp32 matrix cores).
+FLAGS = ["-O3", "-std=c++17", f"--offload-arch={ARCH}", "-fPIC", "-shared",
+         "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+         "-Wall", "-Wno-unused-function", "-Wno-unused-command-line-argument"]
+
+
+def sources():
+    return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
+
+
+def hipcc() -> str:
+    p = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
+    return p
+
+
+def build(output: str = LIBRARY, isa_dir: str | None = None, verbose: bool = False) -> str:
+    cmd = [hipcc()] + FLAGS + ["-I", INCLUDE, "-I", CSRC] + sources()
+    tmp = output + ".tmp"
+    cmd += ["-o", tmp]
+    if isa_dir:
+        os.makedirs(isa_dir, exist_ok=True)
+        cmd += ["-save-temps=obj"]
+        cmd[-1:-1] = []
+    if verbose:
+        print(" ".join(cmd), file=sys.stderr)
+    cwd = isa_dir if isa_dir else None
+    if isa_dir:
+        # -save-temps=obj writes next to the output object; build inside isa_dir.
+        cmd[cmd.index("-o") + 1] = os.path.join(isa_dir, "libilpm.so")
+        subprocess.run(cmd, check=True, cwd=cwd)
+        shutil.copyfile(os.path.join(isa_dir, "libilpm.so"), tmp)
+    else:
+        subprocess.run(cmd, check=True)
+    os.replace(tmp, output)
+    return output
+
+
+PEAKS_SOURCE = os.path.join(ROOT, "bench_peaks.hip")
+PEAKS_LIBRARY = os.path.join(ROOT, "bench_peaks.so")
+
+
+def build_peaks(output: str = PEAKS_LIBRARY) -> str:
+    """The peak microbenchmarks used by bench.py --peaks."""
+    tmp = output + ".tmp"
+    subprocess.run([hipcc()] + FLAGS + [PEAKS_SOURCE, "-o", tmp], check=True)
+    os.replace(tmp, output)
+    return output
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--isa", default=None, help="keep intermediate files (gfx950 assembly) here")
+    ap.add_argument("-v", action="store_true")
+    args = ap.parse_args()
+    print(build(isa_dir=args.isa, verbose=args.v))
+    print(build_peaks())
+
+
+if __name__ == "__main__":
+    main()

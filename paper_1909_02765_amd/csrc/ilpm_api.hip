@@ -1,0 +1,377 @@
+// C-ABI layer: argument checks, plan choice, workspace, device check and
+// launch.  Declarations and contracts are in include/ilpm.h.
+#include <algorithm>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <mutex>
+
+#include "internal.h"
+
+namespace ilpm {
+namespace {
+
+constexpr int kMaxDevices = 64;
+constexpr int64_t kMaxElems = 0x7fffffffLL;
+
+std::mutex g_mu;
+int g_arch[kMaxDevices];  // 0 unknown, 1 gfx950, -1 other
+thread_local int g_last_hip = 0;  // hipError_t behind the last ILPM_ERR_HIP of this thread
+
+int hip_fail(hipError_t e)
+{
+    g_last_hip = (int)e;
+    return ILPM_ERR_HIP;
+}
+
+struct Workspace {
+    void *user = nullptr;
+    size_t user_bytes = 0;
+    void *own = nullptr;
+    size_t own_bytes = 0;
+};
+Workspace g_ws[kMaxDevices];
+
+bool overlaps(const void *a, size_t an, const void *b, size_t bn)
+{
+    if (!a || !b || an == 0 || bn == 0) return false;
+    const uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
+    return a0 < b0 + bn && b0 < a0 + an;
+}
+
+// Output size along one axis, -1 when no window fits.
+int64_t out_extent(int n, int k, int stride, int pad)
+{
+    const int64_t span = (int64_t)n + 2 * (int64_t)pad - k;
+    if (span < 0) return -1;
+    return span / stride + 1;
+}
+
+int check_dims(int c_in, int h, int w, int c_out, int k, int stride, int pad, ConvShape *s)
+{
+    if (c_in <= 0 || h <= 0 || w <= 0 || c_out <= 0 || k <= 0 || stride <= 0 || pad < 0)
+        return ILPM_ERR_INVALID_ARG;
+    const int64_t ho = out_extent(h, k, stride, pad);
+    const int64_t wo = out_extent(w, k, stride, pad);
+    if (ho < 1 || wo < 1) return ILPM_ERR_INVALID_ARG;
+    if ((int64_t)c_in * h * w > kMaxElems) return ILPM_ERR_UNSUPPORTED;
+    if ((int64_t)c_out * c_in * k * k > kMaxElems) return ILPM_ERR_UNSUPPORTED;
+    if ((int64_t)c_out * ho * wo > kMaxElems) return ILPM_ERR_UNSUPPORTED;
+    if (ho > kMaxElems || wo > kMaxElems) return ILPM_ERR_UNSUPPORTED;
+    if (s) {
+        s->c_in = c_in; s->h = h; s->w = w; s->c_out = c_out; s->k = k;
+        s->stride = stride; s->pad = pad; s->h_out = (int)ho; s->w_out = (int)wo;
+    }
+    return ILPM_OK;
+}
+
+int validate(const void *in, const void *w, const void *bias, const ConvShape &s, const void *out)
+{
+    if (!in || !w || !out) return ILPM_ERR_INVALID_ARG;
+    const size_t in_b = sizeof(float) * (size_t)s.c_in * s.h * s.w;
+    const size_t w_b = sizeof(float) * (size_t)s.c_out * s.c_in * s.k * s.k;
+    const size_t b_b = sizeof(float) * (size_t)s.c_out;
+    const size_t o_b = sizeof(float) * (size_t)s.c_out * s.h_out * s.w_out;
+    if (((uintptr_t)in | (uintptr_t)w | (uintptr_t)out | (uintptr_t)bias) & 3u) return ILPM_ERR_INVALID_ARG;
+    if (overlaps(out, o_b, in, in_b) || overlaps(out, o_b, w, w_b) || overlaps(out, o_b, bias, b_b))
+        return ILPM_ERR_INVALID_ARG;
+    return ILPM_OK;
+}
+
+// The default plan: the cheapest matrix-core variant for this filter size and
+// stride by the cost model, else the LDS direct kernel, else the plain one.
+int choose_plan(const ConvShape &s, ilpm_plan *p)
+{
+    const char *force = std::getenv("ILPM_FORCE_PATH");
+    const char *split_env = std::getenv("ILPM_SPLIT");
+    const int forced_splits = split_env ? std::atoi(split_env) : 0;
+    const bool want_direct = force && std::strcmp(force, "direct") == 0;
+    if (!want_direct) {
+        bool found = false;
+        double best = 0;
+        ilpm_plan bp = {};
+        for (int v = 0; v < igemm_num_variants(); ++v) {
+            ilpm_plan q;
+            if (!igemm_make_plan(s, v, forced_splits > 0 ? forced_splits : 0, &q)) continue;
+            const double c = igemm_plan_cost(s, q);
+            if (!found || c < best) {
+                found = true;
+                best = c;
+                bp = q;
+            }
+        }
+        if (found) {
+            *p = bp;
+            return ILPM_OK;
+        }
+    }
+    if (direct_make_plan(s, 0, p)) return ILPM_OK;
+    if (direct_make_plan(s, 1, p)) return ILPM_OK;
+    return ILPM_ERR_UNSUPPORTED;
+}
+
+bool same_plan_shape(const ilpm_plan &a, const ilpm_plan &b)
+{
+    return a.path == b.path && a.variant == b.variant && a.tile_h == b.tile_h && a.tile_w == b.tile_w &&
+           a.co_tile == b.co_tile && a.ci_chunk == b.ci_chunk && a.splits == b.splits && a.grid == b.grid &&
+           a.block == b.block && a.lds_bytes == b.lds_bytes && a.h_out == b.h_out && a.w_out == b.w_out &&
+           a.workspace_bytes == b.workspace_bytes;
+}
+
+// Rebuild the plan the caller passed for this shape and insist it matches, so
+// a plan made for another shape is refused rather than run.
+int check_plan(const ConvShape &s, const ilpm_plan &p)
+{
+    ilpm_plan q;
+    bool ok = false;
+    if (p.path == ILPM_PATH_IGEMM) ok = igemm_make_plan(s, p.variant, p.splits, &q);
+    else if (p.path == ILPM_PATH_DIRECT) ok = direct_make_plan(s, p.variant, &q);
+    if (!ok || !same_plan_shape(p, q)) return ILPM_ERR_INVALID_ARG;
+    return ILPM_OK;
+}
+
+int device_check(int *dev_out)
+{
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e);
+    if (dev < 0 || dev >= kMaxDevices) return hip_fail(hipErrorInvalidDevice);
+    std::lock_guard<std::mutex> lk(g_mu);
+    if (g_arch[dev] == 0) {
+        hipDeviceProp_t prop;
+        e = hipGetDeviceProperties(&prop, dev);
+        if (e != hipSuccess) return hip_fail(e);
+        g_arch[dev] = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0 ? 1 : -1;
+    }
+    *dev_out = dev;
+    return g_arch[dev] == 1 ? ILPM_OK : ILPM_ERR_ARCH;
+}
+
+int get_workspace(int dev, size_t need, hipStream_t stream, void **ws)
+{
+    *ws = nullptr;
+    if (need == 0) return ILPM_OK;
+    std::lock_guard<std::mutex> lk(g_mu);
+    Workspace &w = g_ws[dev];
+    if (w.user) {
+        if (w.user_bytes < need) return ILPM_ERR_WORKSPACE;
+        *ws = w.user;
+        return ILPM_OK;
+    }
+    if (w.own_bytes < need) {
+        hipError_t e;
+        if (w.own) {
+            // Earlier calls may still use the old buffer.
+            if ((e = hipDeviceSynchronize()) != hipSuccess) return hip_fail(e);
+            if ((e = hipFree(w.own)) != hipSuccess) return hip_fail(e);
+            w.own = nullptr;
+            w.own_bytes = 0;
+        }
+        const size_t bytes = ((need + (1u << 20) - 1) >> 20) << 20;
+        void *p = nullptr;
+        if ((e = hipMalloc(&p, bytes)) != hipSuccess) return hip_fail(e);
+        (void)hipGetLastError();
+        if ((e = launch_fill_zero(p, bytes, stream)) != hipSuccess) {
+            (void)hipFree(p);
+            return hip_fail(e);
+        }
+        w.own = p;
+        w.own_bytes = bytes;
+    }
+    *ws = w.own;
+    return ILPM_OK;
+}
+
+void log_plan(const ConvShape &s, const ilpm_plan &p)
+{
+    static const int on = [] {
+        const char *e = std::getenv("ILPM_LOG");
+        return e && *e && *e != '0';
+    }();
+    if (!on) return;
+    std::fprintf(stderr,
+                 "ilpm: C_in=%d H=%d W=%d C_out=%d K=%d s=%d p=%d -> %s v%d tile %dx%d co%d cc%d splits %d "
+                 "grid %d block %d lds %d ws %zu\n",
+                 s.c_in, s.h, s.w, s.c_out, s.k, s.stride, s.pad, p.path == ILPM_PATH_IGEMM ? "igemm" : "direct",
+                 p.variant, p.tile_h, p.tile_w, p.co_tile, p.ci_chunk, p.splits, p.grid, p.block, p.lds_bytes,
+                 p.workspace_bytes);
+}
+
+int run(const float *in, const float *w, const float *bias, const ConvShape &s, float *out, const ilpm_plan &p,
+        hipStream_t stream)
+{
+    int dev = 0;
+    int rc = device_check(&dev);
+    if (rc != ILPM_OK) return rc;
+    void *ws = nullptr;
+    rc = get_workspace(dev, p.workspace_bytes, stream, &ws);
+    if (rc != ILPM_OK) return rc;
+    log_plan(s, p);
+    // Launch errors are read back with hipGetLastError; drop any error an
+    // earlier, unrelated runtime call of this thread left behind.
+    (void)hipGetLastError();
+    hipError_t e;
+    if (p.path == ILPM_PATH_IGEMM) e = igemm_launch(p, s, in, w, bias, out, ws, stream);
+    else e = direct_launch(p, s, in, w, bias, out, stream);
+    return e == hipSuccess ? ILPM_OK : hip_fail(e);
+}
+
+}  // namespace
+}  // namespace ilpm
+
+using namespace ilpm;
+
+extern "C" {
+
+const char *ilpm_status_str(int status)
+{
+    switch (status) {
+    case ILPM_OK: return "ok";
+    case ILPM_ERR_INVALID_ARG: return "invalid argument";
+    case ILPM_ERR_UNSUPPORTED: return "unsupported size";
+    case ILPM_ERR_WORKSPACE: return "workspace too small";
+    case ILPM_ERR_HIP: return "HIP runtime error";
+    case ILPM_ERR_ARCH: return "device is not gfx950";
+    default: return "unknown status";
+    }
+}
+
+int ilpm_conv2d_validate(const void *in, const void *w, const void *bias, int C_in, int H, int W, int C_out,
+                         int K, int stride, int pad, const void *out)
+{
+    ConvShape s;
+    int rc = check_dims(C_in, H, W, C_out, K, stride, pad, &s);
+    if (rc != ILPM_OK) return rc;
+    return validate(in, w, bias, s, out);
+}
+
+int ilpm_conv2d_plan(int C_in, int H, int W, int C_out, int K, int stride, int pad, ilpm_plan *plan)
+{
+    if (!plan) return ILPM_ERR_INVALID_ARG;
+    ConvShape s;
+    int rc = check_dims(C_in, H, W, C_out, K, stride, pad, &s);
+    if (rc != ILPM_OK) return rc;
+    return choose_plan(s, plan);
+}
+
+int ilpm_conv2d_plan_variant(int C_in, int H, int W, int C_out, int K, int stride, int pad, int path,
+                             int variant, int splits, ilpm_plan *plan)
+{
+    if (!plan) return ILPM_ERR_INVALID_ARG;
+    ConvShape s;
+    int rc = check_dims(C_in, H, W, C_out, K, stride, pad, &s);
+    if (rc != ILPM_OK) return rc;
+    bool ok = false;
+    if (path == ILPM_PATH_IGEMM) ok = igemm_make_plan(s, variant, splits, plan);
+    else if (path == ILPM_PATH_DIRECT) ok = splits <= 1 && direct_make_plan(s, variant, plan);
+    return ok ? ILPM_OK : ILPM_ERR_INVALID_ARG;
+}
+
+int ilpm_num_variants(int path)
+{
+    if (path == ILPM_PATH_IGEMM) return igemm_num_variants();
+    if (path == ILPM_PATH_DIRECT) return direct_num_variants();
+    return 0;
+}
+
+int ilpm_variant_info(int path, int variant, int *K, int *stride, int *tile_h, int *tile_w, int *co_tile)
+{
+    int k, st, th, tw, ct;
+    bool ok = false;
+    if (path == ILPM_PATH_IGEMM) ok = igemm_variant_info(variant, &k, &st, &th, &tw, &ct);
+    else if (path == ILPM_PATH_DIRECT) ok = direct_variant_info(variant, &k, &st, &th, &tw, &ct);
+    if (!ok) return ILPM_ERR_INVALID_ARG;
+    if (K) *K = k;
+    if (stride) *stride = st;
+    if (tile_h) *tile_h = th;
+    if (tile_w) *tile_w = tw;
+    if (co_tile) *co_tile = ct;
+    return ILPM_OK;
+}
+
+int ilpm_conv2d_workspace_size(int C_in, int H, int W, int C_out, int K, int stride, int pad, size_t *bytes)
+{
+    if (!bytes) return ILPM_ERR_INVALID_ARG;
+    ilpm_plan p;
+    int rc = ilpm_conv2d_plan(C_in, H, W, C_out, K, stride, pad, &p);
+    if (rc != ILPM_OK) return rc;
+    *bytes = p.workspace_bytes;
+    return ILPM_OK;
+}
+
+int ilpm_last_hip_error(void) { return g_last_hip; }
+
+int ilpm_set_workspace(void *ptr, size_t bytes, hipStream_t stream)
+{
+    if (ptr && ((uintptr_t)ptr & 255u)) return ILPM_ERR_INVALID_ARG;
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e);
+    if (dev < 0 || dev >= kMaxDevices) return hip_fail(hipErrorInvalidDevice);
+    if (ptr && bytes > 0) {
+        (void)hipGetLastError();
+        if ((e = launch_fill_zero(ptr, bytes, stream)) != hipSuccess) return hip_fail(e);
+    }
+    std::lock_guard<std::mutex> lk(g_mu);
+    g_ws[dev].user = ptr;
+    g_ws[dev].user_bytes = ptr ? bytes : 0;
+    return ILPM_OK;
+}
+
+int ilpm_conv2d_fwd(const float *in, const float *w, const float *bias, int C_in, int H, int W, int C_out, int K,
+                    int stride, int pad, float *out, hipStream_t stream)
+{
+    ConvShape s;
+    int rc = check_dims(C_in, H, W, C_out, K, stride, pad, &s);
+    if (rc != ILPM_OK) return rc;
+    rc = validate(in, w, bias, s, out);
+    if (rc != ILPM_OK) return rc;
+    ilpm_plan p;
+    rc = choose_plan(s, &p);
+    if (rc != ILPM_OK) return rc;
+    return run(in, w, bias, s, out, p, stream);
+}
+
+int ilpm_conv2d_fwd_plan(const float *in, const float *w, const float *bias, int C_in, int H, int W, int C_out,
+                         int K, int stride, int pad, float *out, const ilpm_plan *plan, hipStream_t stream)
+{
+    if (!plan) return ILPM_ERR_INVALID_ARG;
+    ConvShape s;
+    int rc = check_dims(C_in, H, W, C_out, K, stride, pad, &s);
+    if (rc != ILPM_OK) return rc;
+    rc = validate(in, w, bias, s, out);
+    if (rc != ILPM_OK) return rc;
+    rc = check_plan(s, *plan);
+    if (rc != ILPM_OK) return rc;
+    return run(in, w, bias, s, out, *plan, stream);
+}
+
+int ilpm_relu_inplace(float *x, int64_t n, hipStream_t stream)
+{
+    if (n < 0 || (!x && n > 0) || ((uintptr_t)x & 3u)) return ILPM_ERR_INVALID_ARG;
+    if (n == 0) return ILPM_OK;
+    int dev = 0;
+    int rc = device_check(&dev);
+    if (rc != ILPM_OK) return rc;
+    (void)hipGetLastError();
+    const hipError_t e = launch_relu(x, n, stream);
+    return e == hipSuccess ? ILPM_OK : hip_fail(e);
+}
+
+int ilpm_maxpool2x2(const float *in, int C, int H, int W, float *out, hipStream_t stream)
+{
+    if (!in || !out || C <= 0 || H < 2 || W < 2) return ILPM_ERR_INVALID_ARG;
+    if ((int64_t)C * H * W > kMaxElems) return ILPM_ERR_UNSUPPORTED;
+    if (((uintptr_t)in | (uintptr_t)out) & 3u) return ILPM_ERR_INVALID_ARG;
+    const size_t in_b = sizeof(float) * (size_t)C * H * W;
+    const size_t o_b = sizeof(float) * (size_t)C * (H / 2) * (W / 2);
+    if (overlaps(in, in_b, out, o_b)) return ILPM_ERR_INVALID_ARG;
+    int dev = 0;
+    int rc = device_check(&dev);
+    if (rc != ILPM_OK) return rc;
+    (void)hipGetLastError();
+    const hipError_t e = launch_maxpool2x2(in, C, H, W, out, stream);
+    return e == hipSuccess ? ILPM_OK : hip_fail(e);
+}
+
+}  // extern "C"

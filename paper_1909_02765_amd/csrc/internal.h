@@ -1,0 +1,48 @@
+// Internal interfaces between the C-ABI layer (ilpm_api.hip) and the kernel
+// families (conv_direct.hip, conv_igemm.hip, stack_ops.hip).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "ilpm.h"
+
+namespace ilpm {
+
+// One convolution call's geometry; h_out/w_out follow the output-size formula
+// in ilpm.h.
+struct ConvShape {
+    int c_in, h, w, c_out, k, stride, pad, h_out, w_out;
+};
+
+// Split-K bookkeeping lives at the start of the workspace: one arrival
+// counter per output tile, always returned to zero by the workgroup that
+// reduces the tile.  Partial sums follow, 256-byte aligned.
+constexpr int kMaxTileCounters = 65536;
+constexpr size_t kCounterBytes = sizeof(unsigned) * kMaxTileCounters;
+
+// ---- direct (VALU) family ----
+int direct_num_variants();
+bool direct_variant_info(int v, int *k, int *stride, int *tile_h, int *tile_w, int *co_tile);
+bool direct_make_plan(const ConvShape &s, int variant, ilpm_plan *p);
+hipError_t direct_launch(const ilpm_plan &p, const ConvShape &s, const float *x, const float *w,
+                         const float *bias, float *out, hipStream_t stream);
+
+// ---- implicit-GEMM (fp32 MFMA) family ----
+int igemm_num_variants();
+bool igemm_variant_info(int v, int *k, int *stride, int *tile_h, int *tile_w, int *co_tile);
+// splits = 0 lets the family choose.
+bool igemm_make_plan(const ConvShape &s, int variant, int splits, ilpm_plan *p);
+// Modelled cost of a plan in SIMD cycles of the slowest compute unit, used to
+// rank variants; lower is better.
+double igemm_plan_cost(const ConvShape &s, const ilpm_plan &p);
+hipError_t igemm_launch(const ilpm_plan &p, const ConvShape &s, const float *x, const float *w,
+                        const float *bias, float *out, void *workspace, hipStream_t stream);
+
+// ---- helpers ----
+hipError_t launch_fill_zero(void *p, size_t bytes, hipStream_t stream);
+hipError_t launch_relu(float *x, int64_t n, hipStream_t stream);
+hipError_t launch_maxpool2x2(const float *in, int c, int h, int w, float *out, hipStream_t stream);
+
+inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+}  // namespace ilpm

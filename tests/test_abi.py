@@ -1,0 +1,143 @@
+"""The C ABI on the host: the library loads, exports every declared symbol, and
+its pure-host entry points (validation, planning, workspace sizing, status
+text) behave as include/ilpm.h states.  No kernel is launched."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_1909_02765_amd as ilpm
+import workloads
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ilpm.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ilpm_\w+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_functions()
+    assert len(names) >= 12
+    for n in names:
+        assert hasattr(ilpm.lib, n), f"{n} declared in ilpm.h but not exported"
+
+
+def test_status_strings():
+    assert ilpm.status_str(0) == "ok"
+    seen = set()
+    for code in (-1, -2, -3, -4, -5):
+        s = ilpm.status_str(code)
+        assert s and s != "unknown status"
+        seen.add(s)
+    assert len(seen) == 5
+    assert ilpm.status_str(7) == "unknown status"
+
+
+def _validate(inp=0x1000, w=0x100000, b=None, c_in=3, h=8, wd=8, c_out=4, k=3, s=1, p=1, out=0x200000):
+    return ilpm.lib.ilpm_conv2d_validate(inp, w, b, c_in, h, wd, c_out, k, s, p, out)
+
+
+def test_validate_ok():
+    assert _validate() == ilpm.OK
+    assert _validate(b=0x300000) == ilpm.OK
+
+
+@pytest.mark.parametrize("kw", [
+    dict(inp=None), dict(w=None), dict(out=None),
+    dict(c_in=0), dict(h=0), dict(wd=-1), dict(c_out=0), dict(k=0), dict(s=0), dict(s=-2), dict(p=-1),
+    dict(h=2, k=5, p=1),          # H_out < 1
+    dict(wd=1, k=3, p=0),         # W_out < 1
+    dict(out=0x1000 + 16),        # out overlaps the input
+    dict(out=0x100000 + 4),       # out overlaps the weights
+    dict(b=0x200000 + 8),         # out overlaps the bias
+    dict(inp=0x1002),             # misaligned
+])
+def test_validate_invalid(kw):
+    assert _validate(**kw) == ilpm.ERR_INVALID_ARG
+
+
+def test_validate_unsupported_size():
+    # 2^31 input elements
+    assert _validate(c_in=2, h=32768, wd=32768, out=0x7000000000000) == ilpm.ERR_UNSUPPORTED
+
+
+def test_fwd_rejects_before_any_launch():
+    # Returns from the argument check without touching a device.
+    rc = ilpm.lib.ilpm_conv2d_fwd(None, 0x1000, None, 3, 8, 8, 4, 3, 1, 1, 0x100000, None)
+    assert rc == ilpm.ERR_INVALID_ARG
+    rc = ilpm.lib.ilpm_conv2d_fwd(0x1000, 0x100000, None, 3, 2, 2, 4, 5, 1, 0, 0x200000, None)
+    assert rc == ilpm.ERR_INVALID_ARG
+    rc = ilpm.lib.ilpm_maxpool2x2(0x1000, 3, 1, 8, 0x2000, None)
+    assert rc == ilpm.ERR_INVALID_ARG
+    rc = ilpm.lib.ilpm_relu_inplace(None, 10, None)
+    assert rc == ilpm.ERR_INVALID_ARG
+
+
+def test_set_workspace_rejects_misaligned():
+    assert ilpm.lib.ilpm_set_workspace(ctypes.c_void_p(0x1000 + 16), 4096, None) == ilpm.ERR_INVALID_ARG
+
+
+def test_variants_table():
+    assert ilpm.num_variants(ilpm.PATH_DIRECT) == 2
+    n = ilpm.num_variants(ilpm.PATH_IGEMM)
+    assert n >= 4
+    assert ilpm.num_variants(7) == 0
+    ks = set()
+    for v in range(n):
+        info = ilpm.variant_info(ilpm.PATH_IGEMM, v)
+        assert info["co_tile"] % 16 == 0 and info["tile_h"] >= 1 and info["tile_w"] >= 1
+        ks.add((info["k"], info["stride"]))
+    assert {(3, 1), (3, 2), (1, 1), (5, 1)} <= ks
+    with pytest.raises(ilpm.IlpmError):
+        ilpm.variant_info(ilpm.PATH_IGEMM, n)
+
+
+@pytest.mark.parametrize("case", workloads.SINGLE_LAYER_CASES, ids=lambda c: c.name)
+def test_plan_for_every_workload(case):
+    d = case.dims()
+    p = ilpm.plan(d["c_in"], d["h"], d["w"], d["c_out"], d["k"], d["stride"], d["pad"])
+    assert p.h_out == ilpm.out_size(d["h"], d["k"], d["stride"], d["pad"])
+    assert p.w_out == ilpm.out_size(d["w"], d["k"], d["stride"], d["pad"])
+    assert p.grid >= 1 and p.block in (64, 128, 256, 512)
+    assert p.lds_bytes <= 65536
+    if p.splits > 1:
+        assert p.workspace_bytes > 0
+    assert ilpm.workspace_size(d["c_in"], d["h"], d["w"], d["c_out"], d["k"], d["stride"], d["pad"]) \
+        == p.workspace_bytes
+
+
+def test_plan_variant_rules():
+    # A 3x3/stride-1 variant refuses a 5x5 filter; direct variants take any.
+    v33 = next(v for v in range(ilpm.num_variants(ilpm.PATH_IGEMM))
+               if ilpm.variant_info(ilpm.PATH_IGEMM, v)["k"] == 3
+               and ilpm.variant_info(ilpm.PATH_IGEMM, v)["stride"] == 1)
+    with pytest.raises(ilpm.IlpmError):
+        ilpm.plan_variant(8, 7, 7, 16, 5, 1, 2, ilpm.PATH_IGEMM, v33)
+    p = ilpm.plan_variant(8, 7, 7, 16, 7, 3, 2, ilpm.PATH_DIRECT, 0)
+    assert p.path == ilpm.PATH_DIRECT and p.h_out == 2
+    p = ilpm.plan_variant(512, 14, 14, 512, 3, 1, 1, ilpm.PATH_IGEMM, v33, 4)
+    assert p.splits == 4 and p.workspace_bytes > 0
+    # more splits than input-channel stages is refused
+    with pytest.raises(ilpm.IlpmError):
+        ilpm.plan_variant(8, 14, 14, 64, 3, 1, 1, ilpm.PATH_IGEMM, v33, 2)
+
+
+def test_plan_env_override(monkeypatch):
+    monkeypatch.setenv("ILPM_FORCE_PATH", "direct")
+    p = ilpm.plan(64, 56, 56, 64, 3, 1, 1)
+    assert p.path == ilpm.PATH_DIRECT
+    monkeypatch.delenv("ILPM_FORCE_PATH")
+    p = ilpm.plan(64, 56, 56, 64, 3, 1, 1)
+    assert p.path == ilpm.PATH_IGEMM
+
+
+def test_fwd_plan_rejects_foreign_plan():
+    p = ilpm.plan(64, 56, 56, 64, 3, 1, 1)
+    rc = ilpm.lib.ilpm_conv2d_fwd_plan(0x1000, 0x10000000, None, 64, 28, 28, 64, 3, 1, 1, 0x20000000,
+                                       ctypes.byref(p), None)
+    assert rc == ilpm.ERR_INVALID_ARG

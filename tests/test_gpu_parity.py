@@ -1,0 +1,198 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle, element
+by element, within 1e-4 * (1 + S / (C_in*K*K)); bit for bit where every
+partial sum is exactly representable (small-integer tensors)."""
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+from gpu_common import (assert_matches, note, random_case, run_conv, small_int_case, torch_cuda)
+
+pytestmark = pytest.mark.gpu
+
+CASES = workloads.SINGLE_LAYER_CASES
+_ORACLE = {}
+
+
+@pytest.fixture(scope="module")
+def ilpm():
+    torch_cuda()
+    import paper_1909_02765_amd as m
+    oracle.set_threads(16)
+    return m
+
+
+def case_data(case):
+    if case.name not in _ORACLE:
+        x, w, b = case.inputs()
+        ref, sab = oracle.conv2d_f64(x, w, b, case.stride, case.pad)
+        _ORACLE[case.name] = (x, w, b, ref, sab)
+    return _ORACLE[case.name]
+
+
+def plans_for(ilpm, c_in, h, w, c_out, k, s, p):
+    """Every compiled variant that accepts this shape, with one and several splits."""
+    plans = []
+    for v in range(ilpm.num_variants(ilpm.PATH_DIRECT)):
+        try:
+            plans.append(ilpm.plan_variant(c_in, h, w, c_out, k, s, p, ilpm.PATH_DIRECT, v))
+        except ilpm.IlpmError:
+            pass
+    for v in range(ilpm.num_variants(ilpm.PATH_IGEMM)):
+        info = ilpm.variant_info(ilpm.PATH_IGEMM, v)
+        if info["k"] != k or info["stride"] != s:
+            continue
+        seen = set()
+        for splits in (1, 0, 3):
+            try:
+                q = ilpm.plan_variant(c_in, h, w, c_out, k, s, p, ilpm.PATH_IGEMM, v, splits)
+            except ilpm.IlpmError:
+                continue
+            if q.splits not in seen:
+                seen.add(q.splits)
+                plans.append(q)
+    return plans
+
+
+def describe(plan):
+    return (f"path={plan.path} v={plan.variant} tile={plan.tile_h}x{plan.tile_w} co={plan.co_tile} "
+            f"splits={plan.splits} grid={plan.grid}")
+
+
+@pytest.mark.parametrize("case", CASES, ids=lambda c: c.name)
+def test_default_plan_full_output(ilpm, case):
+    x, w, b, ref, sab = case_data(case)
+    plan = ilpm.plan(case.c_in, case.h, case.w, case.c_out, case.k, case.stride, case.pad)
+    note(f"[default] {case.name} {describe(plan)}")
+    got = run_conv(x, w, b, case.stride, case.pad)
+    assert_matches(got, ref, sab, case.c_in, case.k, case.name)
+
+
+@pytest.mark.parametrize("case", CASES, ids=lambda c: c.name)
+def test_every_variant_full_output(ilpm, case):
+    x, w, b, ref, sab = case_data(case)
+    plans = plans_for(ilpm, case.c_in, case.h, case.w, case.c_out, case.k, case.stride, case.pad)
+    assert plans
+    for plan in plans:
+        if plan.path == ilpm.PATH_DIRECT and plan.variant == 1 and case.c_in * case.c_out * case.h * case.w > 50e6:
+            continue  # the plain fallback kernel is covered on the smaller layers
+        note(f"[variant] {case.name} {describe(plan)}")
+        got = run_conv(x, w, b, case.stride, case.pad, plan=plan)
+        assert_matches(got, ref, sab, case.c_in, case.k, f"{case.name} {describe(plan)}")
+
+
+@pytest.mark.parametrize("case", CASES, ids=lambda c: c.name)
+def test_small_integers_bit_exact(ilpm, case):
+    """Integer tensors in [-2, 2]: every partial sum is an integer below 2^24, so
+    any summation order gives the oracle's value exactly."""
+    x, w, b = small_int_case(7000 + case.x_seed, case.c_in, case.h, case.w, case.c_out, case.k)
+    ref, _ = oracle.conv2d_f64(x, w, b, case.stride, case.pad)
+    assert np.abs(ref).max() < 2 ** 24
+    for plan in [None] + plans_for(ilpm, case.c_in, case.h, case.w, case.c_out, case.k, case.stride, case.pad):
+        if plan is not None and plan.path == ilpm.PATH_DIRECT and plan.variant == 1 and \
+                case.c_in * case.c_out * case.h * case.w > 50e6:
+            continue
+        note(f"[exact] {case.name} {describe(plan) if plan is not None else 'default'}")
+        got = run_conv(x, w, b, case.stride, case.pad, plan=plan)
+        np.testing.assert_array_equal(got.astype(np.float64), ref)
+
+
+def test_fuzz_small_shapes(ilpm):
+    """Random small shapes: every variant that accepts each shape."""
+    shapes = workloads.fuzz_shapes(2024, 40)
+    for i, s in enumerate(shapes):
+        x, w, b = random_case(100 + 3 * i, s["c_in"], s["h"], s["w"], s["c_out"], s["k"], bias=(i % 2 == 0))
+        ref, sab = oracle.conv2d_f64(x, w, b, s["stride"], s["pad"])
+        for plan in [None] + plans_for(ilpm, s["c_in"], s["h"], s["w"], s["c_out"], s["k"], s["stride"], s["pad"]):
+            note(f"[fuzz {i}] {s} {describe(plan) if plan is not None else 'default'}")
+            got = run_conv(x, w, b, s["stride"], s["pad"], plan=plan)
+            assert_matches(got, ref, sab, s["c_in"], s["k"], f"fuzz {i} {s}")
+
+
+def test_fuzz_matrix_core_ragged(ilpm):
+    """Shapes that leave partial output tiles, partial channel stages and
+    partial output-channel tiles for every matrix-core variant."""
+    rng = np.random.default_rng(31)
+    n = ilpm.num_variants(ilpm.PATH_IGEMM)
+    for v in range(n):
+        info = ilpm.variant_info(ilpm.PATH_IGEMM, v)
+        k, s = info["k"], info["stride"]
+        for j in range(4):
+            c_in = int(rng.integers(1, 41))
+            c_out = int(rng.integers(1, 150))
+            h = int(rng.integers(1, 40))
+            w = int(rng.integers(1, 40))
+            p = int(rng.integers(0, k))
+            if h + 2 * p < k or w + 2 * p < k:
+                p = k
+            x, wt, b = random_case(5000 + 10 * v + j, c_in, h, w, c_out, k, bias=(j % 2 == 1))
+            ref, sab = oracle.conv2d_f64(x, wt, b, s, p)
+            for splits in (1, 0, 2):
+                try:
+                    plan = ilpm.plan_variant(c_in, h, w, c_out, k, s, p, ilpm.PATH_IGEMM, v, splits)
+                except ilpm.IlpmError:
+                    continue
+                note(f"[ragged] v={v} c_in={c_in} h={h} w={w} c_out={c_out} k={k} s={s} p={p} {describe(plan)}")
+                got = run_conv(x, wt, b, s, p, plan=plan)
+                assert_matches(got, ref, sab, c_in, k, f"ragged v={v} {describe(plan)}")
+
+
+def test_split_reduction_repeats_bitwise(ilpm):
+    """A split plan run several times gives identical bits (fixed reduction
+    order, arrival counters returned to zero)."""
+    case = workloads.RESNET_CONV4
+    x, w, b, ref, sab = case_data(case)
+    p = ilpm.plan(case.c_in, case.h, case.w, case.c_out, case.k, case.stride, case.pad)
+    plan = p if p.splits > 1 else ilpm.plan_variant(case.c_in, case.h, case.w, case.c_out, case.k, case.stride,
+                                                    case.pad, ilpm.PATH_IGEMM, p.variant, 8)
+    assert plan.splits > 1
+    note(f"[repeat] {describe(plan)}")
+    outs = [run_conv(x, w, b, case.stride, case.pad, plan=plan) for _ in range(3)]
+    for o in outs[1:]:
+        np.testing.assert_array_equal(o, outs[0])
+    assert_matches(outs[0], ref, sab, case.c_in, case.k, "repeat")
+
+
+def test_registered_workspace(ilpm):
+    torch = torch_cuda()
+    case = workloads.RESNET_CONV4
+    x, w, b, ref, sab = case_data(case)
+    v = ilpm.plan(case.c_in, case.h, case.w, case.c_out, case.k, case.stride, case.pad).variant
+    plan = ilpm.plan_variant(case.c_in, case.h, case.w, case.c_out, case.k, case.stride, case.pad,
+                             ilpm.PATH_IGEMM, v, 4)
+    small = torch.empty(1024, dtype=torch.float32, device="cuda")
+    big = torch.empty((plan.workspace_bytes + 3) // 4 + 64, dtype=torch.float32, device="cuda")
+    try:
+        ilpm.set_workspace(small)
+        with pytest.raises(ilpm.IlpmError) as e:
+            run_conv(x, w, b, case.stride, case.pad, plan=plan)
+        assert e.value.status == ilpm.ERR_WORKSPACE
+        ilpm.set_workspace(big)
+        note("[workspace] registered")
+        got = run_conv(x, w, b, case.stride, case.pad, plan=plan)
+        assert_matches(got, ref, sab, case.c_in, case.k, "registered workspace")
+    finally:
+        ilpm.set_workspace(None)
+        torch.cuda.synchronize()
+
+
+def test_non_default_stream(ilpm):
+    torch = torch_cuda()
+    case = workloads.RESNET_STRIDED
+    x, w, b, ref, sab = case_data(case)
+    s = torch.cuda.Stream()
+    note("[stream] side stream")
+    with torch.cuda.stream(s):
+        got = run_conv(x, w, b, case.stride, case.pad, stream=s)
+    assert_matches(got, ref, sab, case.c_in, case.k, "side stream")
+
+
+def test_bad_arguments_raise(ilpm):
+    torch = torch_cuda()
+    x = torch.zeros((1, 4, 8, 8), device="cuda")
+    w = torch.zeros((4, 4, 3, 3), device="cuda")
+    # an output aliasing the input is refused before anything is launched
+    rc = ilpm.lib.ilpm_conv2d_fwd(x.data_ptr(), w.data_ptr(), None, 4, 8, 8, 4, 3, 1, 1, x.data_ptr(), None)
+    assert rc == ilpm.ERR_INVALID_ARG
+    with pytest.raises(TypeError):
+        ilpm.conv2d(x.double(), w, None)

@@ -204,6 +204,13 @@ def fuzz_shapes(seed: int, n: int):
     return shapes
 
 
+def to_device(torch, a):
+    """A contiguous float32 CUDA copy of a host array (None stays None)."""
+    if a is None:
+        return None
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
+
+
 def case_by_name(name: str) -> Optional[ConvCase]:
     for c in SINGLE_LAYER_CASES:
         if c.name == name:
