@@ -181,6 +181,8 @@ def main():
     ap.add_argument("--all", action="store_true", help="also time every workload and the VGG-16 stack")
     ap.add_argument("--report", default=None, help="JSON file for the --all table")
     ap.add_argument("--peaks", action="store_true", help="also measure the MI355X ceilings")
+    ap.add_argument("--copy-calib", type=int, default=0, metavar="MIB",
+                    help="also run a plain copy of MIB MiB (counter calibration under rocprofv3)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -232,6 +234,19 @@ def main():
     if not args.no_cpu_baseline:
         y = r["out"].cpu().numpy()
         line["cpu_baseline"] = cpu_baseline(case, r["x"], r["w"], r["b"], y)
+
+    if args.copy_calib:
+        import ctypes
+        plib = ctypes.CDLL(os.path.join(ROOT, "bench_peaks.so"))
+        n = args.copy_calib << 18  # floats
+        src = torch.ones(n, device="cuda")
+        dst = torch.empty(n, device="cuda")
+        st = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+        for _ in range(3):
+            plib.copy_launch(ctypes.c_void_p(src.data_ptr()), ctypes.c_void_p(dst.data_ptr()),
+                             ctypes.c_size_t(n // 4), 4096, st)
+        torch.cuda.synchronize()
+        line["copy_calib_bytes_each_way"] = 4 * n
 
     if args.peaks:
         line["measured_peaks"] = measure_peaks(torch)

@@ -83,10 +83,11 @@ typedef struct ilpm_plan {
  *   bias [C_out] or NULL (no bias)  read only
  *   out  [1, C_out, H_out, W_out]   NCHW, fully written; must not overlap the inputs
  *   stride >= 1, pad >= 0, all sizes >= 1, H_out >= 1 and W_out >= 1.
- * Picks the kernel with ilpm_conv2d_plan.  Plans with splits > 1 use the
- * device workspace (registered with ilpm_set_workspace, else allocated by the
- * library on first need); calls that overlap in time on one device and both
- * use split plans must be ordered on one stream.
+ * Picks the kernel with ilpm_conv2d_plan.  Plans with splits > 1 write
+ * per-split partial outputs to the device workspace (registered with
+ * ilpm_set_workspace, else allocated by the library on first need) and sum
+ * them in a second kernel on the same stream; calls that overlap in time on
+ * one device and both use split plans must be ordered on one stream.
  * Returns ILPM_OK or a negative status.
  */
 int ilpm_conv2d_fwd(const float *in, const float *w, const float *bias,
@@ -103,9 +104,10 @@ int ilpm_conv2d_workspace_size(int C_in, int H, int W, int C_out, int K, int str
 /*
  * ilpm_set_workspace -- register caller-owned device memory (ptr, bytes) as
  * the workspace of the current device, replacing any earlier one; ptr = NULL
- * unregisters it (the library then allocates its own on need).  The memory is
- * cleared on `stream`, must stay allocated while calls may use it, and must be
- * 256-byte aligned.
+ * unregisters it (the library then allocates its own on need).  Its contents
+ * on entry do not matter (every byte a call reads, the same call wrote first).
+ * It must stay allocated while calls may use it and be 256-byte aligned;
+ * `stream` is unused (kept for ABI stability).
  */
 int ilpm_set_workspace(void *ptr, size_t bytes, hipStream_t stream);
 

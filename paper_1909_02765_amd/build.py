@@ -22,8 +22,12 @@ ARCH = "gfx950"
 # Packed fp32 VALU instructions stay disabled: the compiler forms them on its
 # own from scalar float code, and they are not needed here (the dense path
 # uses the fp32 matrix cores).
+# MFMA accumulators in ordinary VGPRs (the register file is unified on gfx950):
+# measured faster than the AGPR form on these kernels, which made the
+# compiler shuttle accumulators between the two register classes.
 FLAGS = ["-O3", "-std=c++17", f"--offload-arch={ARCH}", "-fPIC", "-shared",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+         "-mllvm", "-amdgpu-mfma-vgpr-form=1",
          "-Wall", "-Wno-unused-function", "-Wno-unused-command-line-argument"]
 
 

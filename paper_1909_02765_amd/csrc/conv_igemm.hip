@@ -5,36 +5,44 @@
 //   B [C_in*K*K x pixels] = input patches, never materialised: every B element
 //                           is read from a zero-padded input halo tile in LDS,
 //   D [C_out x pixels]    = the NCHW output.
-// This keeps the two properties the ILP-M paper argues for (Section 4): each
-// input and weight element is fetched from global memory once per workgroup,
-// staged collaboratively with one barrier per stage, and between barriers a
-// wavefront runs a long barrier-free stream of independent multiply-adds (here
-// matrix-core instructions, each 1024 MACs, with every operand reused by a
-// whole row or column of accumulator blocks).
+//
+// How the ILP-M ideas (Section 4, Algorithm 2) land on CDNA4:
+//  * Lanes own output channels for the weight operand.  In a 16x16x4 MFMA the
+//    lane (g, l) supplies A[l][g], i.e. the weight of output channel l for
+//    channel g of the step -- so each lane loads the filter values of "its"
+//    output channel straight from global memory into registers, the paper's
+//    filter_reg, with no shared-memory copy of the weights.  In OIHW the K*K
+//    taps of one (output, input) channel pair are contiguous, so a lane
+//    fetches them with 16-byte loads.  They are loaded one stage ahead.
+//  * The input tile is staged once in LDS for the whole workgroup, by DMA
+//    (buffer loads that write LDS directly), and read by every wavefront:
+//    lanes own output pixels for the B operand.
+//  * Between two barriers a wavefront runs a long barrier-free stream of
+//    independent matrix instructions (1024 multiply-adds each), every operand
+//    reused by a row or a column of accumulator blocks.
 //
 // Contraction order.  Within a stage of CC input channels the contraction
 // index runs tap-major, channel-minor: MFMA step (t, c4) covers tap t and the
-// four channels 4*c4 .. 4*c4+3, one channel per 16-lane group.  Any order of
-// the sum is the same convolution; this one makes every LDS address a
-// per-lane base plus a compile-time offset.
+// channel group c4 (4 channels, one per 16-lane group).  Any order of the
+// sum is the same convolution; this one makes every LDS address a per-lane
+// base plus a compile-time offset.
 //
-// Work split.  A workgroup owns TH x TW output pixels and COT = NWC*16*MA
-// output channels.  Wave (wc, wp) owns 16*MA channels and NB blocks of 16
-// pixels, so it keeps MA*NB 16x16 accumulator blocks.  Optional split of the
-// input channels across `splits` workgroups (grid y): each writes its partial
-// tile to the workspace and the last one to arrive (per-tile counter) sums the
-// partials in split order, adds the bias and stores the tile, so the result
-// does not depend on arrival order.
+// Work split inside a workgroup: NWC x NWP x NWK wavefronts.  Wave (wc, wp, wk)
+// owns 16*MA output channels (slab wc), NB blocks of 16 pixels (group wp) and
+// the channel groups wk, wk + NWK, ... of every stage; the NWK partial
+// accumulators of a tile are summed through LDS at the end.
 //
-// LDS per stage (double buffered, one barrier per stage):
-//   weights [COT][RS]   RS >= CC*K*K, row = one output channel's CC*K*K
-//                       weights in OIHW order (a straight copy of global);
-//                       RS = 2 mod 4 so the 16 rows one MFMA operand reads
-//                       fall in distinct banks.
-//   halo    [CC][PL]    plane = (TH-1)*S+K rows of (TW-1)*S+K pixels, planes
-//                       padded to PL = 16 mod 32 words (stride 1) or odd
-//                       (stride 2) so the four lane groups of a read spread
-//                       over the banks.
+// Work split across workgroups: output tiles (TH x TW pixels x COT channels)
+// and, optionally, `splits` contiguous ranges of input-channel stages (grid
+// y).  With splits > 1 each workgroup writes its partial output, in the
+// output's own layout, to slice `split` of the workspace, and a second kernel
+// sums the slices in split order and adds the bias, so the result does not
+// depend on the order in which workgroups run.
+//
+// LDS: two stage buffers of the halo [CC][HR][HCP] -- (TH-1)*S+K rows of
+// (TW-1)*S+K pixels, rows padded to HCP words so that consecutive channel
+// planes start on different bank halves (plane = 16 mod 32 words for odd
+// strides, an odd word count for even strides).
 #include <cmath>
 
 #include "internal.h"
@@ -43,157 +51,275 @@ namespace ilpm {
 namespace {
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void *lds_ptr_t;
 
-constexpr int row_pad(int n)
+// Halo row length in LDS: the smallest r >= hc that puts successive channel
+// planes (hr * r words) on different bank halves.
+constexpr int halo_row(int hr, int hc, int s)
 {
-    int r = n;
-    while (r % 4 != 2) ++r;
-    return r;
-}
-
-constexpr int plane_pad(int n, int s)
-{
-    int r = n;
-    if (s % 2 == 1) {
-        while (r % 32 != 16) ++r;
-    } else {
-        while (r % 2 != 1) ++r;
+    for (int r = hc; r < hc + 64; ++r) {
+        if (s % 2 == 1 && (hr * r) % 32 == 16) return r;
+        if (s % 2 == 0 && (hr * r) % 2 == 1) return r;
     }
-    return r;
+    return hc;
 }
 
-template <int KS_, int S_, int TH_, int TW_, int NWC_, int NWP_, int MA_, int CC_>
+constexpr int round64(int n) { return (n + 63) / 64 * 64; }
+constexpr int cmax(int a, int b) { return a > b ? a : b; }
+
+template <int KS_, int S_, int TH_, int TW_, int NWC_, int NWP_, int NWK_, int MA_, int CC_>
 struct Cfg {
     static constexpr int KS = KS_, S = S_, TH = TH_, TW = TW_;
-    static constexpr int NWC = NWC_, NWP = NWP_, MA = MA_, CC = CC_;
-    static constexpr int NT = 64 * NWC * NWP;
+    static constexpr int NWC = NWC_, NWP = NWP_, NWK = NWK_, MA = MA_, CC = CC_;
+    static constexpr int NW = NWC * NWP * NWK;  // wavefronts per workgroup
+    static constexpr int NT = 64 * NW;
     static constexpr int NPIX = TH * TW;
     static constexpr int NB = (NPIX + 16 * NWP - 1) / (16 * NWP);
-    static constexpr int NPIXP = NWP * NB * 16;
     static constexpr int KK = KS * KS;
     static constexpr int HR = (TH - 1) * S + KS;
     static constexpr int HC = (TW - 1) * S + KS;
-    static constexpr int PL = plane_pad(HR * HC, S);
-    static constexpr int WROW = CC * KK;
-    static constexpr int RS = row_pad(WROW);
+    static constexpr int HCP = halo_row(HR, HC, S);
+    static constexpr int PL = HR * HCP;
     static constexpr int COT = NWC * 16 * MA;
-    static constexpr int WSZ = COT * RS;
-    static constexpr int XSZ = CC * PL;
-    static constexpr int BUF = ((WSZ + XSZ + 3) / 4) * 4;
-    static constexpr int XE = CC * HR * HC;
-    static constexpr int XPT = (XE + NT - 1) / NT;
-    static constexpr int WE = COT * WROW;
-    static constexpr int WPT = (WE + NT - 1) / NT;
-    static constexpr int LDS_BYTES = 2 * BUF * 4;
-    static_assert(CC % 4 == 0, "a stage holds whole groups of 4 channels");
-    static_assert(LDS_BYTES <= 65536, "LDS budget");
+    static constexpr int G4 = CC / 4 / NWK;  // channel groups per wave per stage
+    // One stage buffer: the halo, a whole number of 64-word rows (one DMA
+    // instruction each).
+    static constexpr int XSZ = round64(CC * PL);
+    static constexpr int NIX = XSZ / 64;
+    static constexpr int XPT = (NIX + NW - 1) / NW;  // DMA instructions per wave
+    // LDS for the cross-wave sum of the NWK partial accumulators.
+    static constexpr int RED = (NWK - 1) * NWC * NWP * MA * NB * 4 * 64;
+    static constexpr int BUF0 = cmax(XSZ, RED);
+    static constexpr int LDS_BYTES = (BUF0 + XSZ) * 4;
+    static_assert(CC % (4 * NWK) == 0, "a stage holds whole groups of 4 channels per wave");
+    static_assert(LDS_BYTES <= 160 * 1024, "LDS budget of one compute unit");
+    static_assert(NT <= 1024, "workgroup size");
 };
 
 struct IgArgs {
     int c_in, h, w, c_out, pad, h_out, w_out;
     int tiles_w, co_tiles, nchunks, chunks_per_split, splits;
-    size_t part_offset;  // floats from the workspace start to the partial sums
 };
 
-template <class C>
-__device__ __forceinline__ void load_stage(const float *__restrict__ x, const float *__restrict__ w,
-                                           const IgArgs &a, int ci0, int ih0, int iw0, int co0,
-                                           float (&xr)[C::XPT], float (&wr)[C::WPT])
+// Buffer descriptors give branch-free loads: a lane whose element lies in the
+// zero padding (or past the tensor) carries an offset beyond the descriptor's
+// range and reads 0.  Offsets are bytes and fit in 31 bits (checked when the
+// plan is made).
+constexpr int kOutOfRange = 0x7fffffff;
+constexpr int kBufferWord3 = 0x00020000;  // 32-bit elements, raw (stride 0) buffer
+
+// A descriptor for [base, base + bytes).  Both are wave-uniform; saying so
+// explicitly keeps the descriptor in scalar registers (otherwise the compiler
+// may build it in vector registers and wrap every load in a loop over the
+// distinct values).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const float *base, unsigned bytes)
 {
-    const int tid = threadIdx.x;
+    const uint64_t b = reinterpret_cast<uint64_t>(base);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)b);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(b >> 32));
+    float *p = reinterpret_cast<float *>(((uint64_t)hi << 32) | lo);
+    return __builtin_amdgcn_make_buffer_rsrc(p, (short)0, (int)__builtin_amdgcn_readfirstlane(bytes), kBufferWord3);
+}
+
+// The KK contiguous floats at byte offset `off`, in 16-byte pieces.  (An
+// out-of-range `off` stays out of range for every piece: the sums are taken
+// unsigned and stay below 2^32.)
+template <int KK>
+__device__ __forceinline__ void load_taps(__amdgpu_buffer_rsrc_t r, int off, float (&dst)[KK])
+{
+    const unsigned base = (unsigned)off;
 #pragma unroll
-    for (int j = 0; j < C::XPT; ++j) {
-        const int e = tid + j * C::NT;
-        float v = 0.f;
-        if (e < C::XE) {
-            const int c = e / (C::HR * C::HC);
-            const int rem = e - c * (C::HR * C::HC);
-            const int r = rem / C::HC;
-            const int col = rem - r * C::HC;
-            const int ci = ci0 + c, ih = ih0 + r, iw = iw0 + col;
-            if (ci < a.c_in && ih >= 0 && ih < a.h && iw >= 0 && iw < a.w)
-                v = x[((size_t)ci * a.h + ih) * a.w + iw];
-        }
-        xr[j] = v;
+    for (int i = 0; i + 4 <= KK; i += 4) {
+        const floatx4 v =
+            __builtin_bit_cast(floatx4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)(base + 4u * i), 0, 0));
+        dst[i] = v[0];
+        dst[i + 1] = v[1];
+        dst[i + 2] = v[2];
+        dst[i + 3] = v[3];
     }
 #pragma unroll
-    for (int j = 0; j < C::WPT; ++j) {
-        const int e = tid + j * C::NT;
-        float v = 0.f;
-        if (e < C::WE) {
-            const int row = e / C::WROW;
-            const int q = e - row * C::WROW;
-            const int co = co0 + row;
-            const int ci = ci0 + q / C::KK;
-            if (co < a.c_out && ci < a.c_in)
-                v = w[((size_t)co * a.c_in + ci0) * C::KK + q];
+    for (int i = KK / 4 * 4; i < KK; ++i)
+        dst[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, (int)(base + 4u * i), 0, 0));
+}
+
+// Weight registers of one stage for one lane: [m-block][channel group][tap].
+template <class C>
+struct AStage {
+    float v[C::MA][C::G4][C::KK];
+};
+
+// Load the weights of the stage starting at input channel ci0: lane (g, l)
+// of m-block m takes output channel co_m and, for channel group c4, input
+// channel ci0 + ci_lane + 4*NWK*c4 (ci_lane = 4*wk + g).
+template <class C>
+__device__ __forceinline__ void load_a(AStage<C> &A, __amdgpu_buffer_rsrc_t rw, const IgArgs &a,
+                                       const int (&a_off)[C::MA], int ci_lane, int ci0)
+{
+#pragma unroll
+    for (int c4 = 0; c4 < C::G4; ++c4) {
+        const int ci = ci0 + ci_lane + 4 * C::NWK * c4;
+        const bool ok = ci < a.c_in;
+#pragma unroll
+        for (int m = 0; m < C::MA; ++m) {
+            const int off = (ok && a_off[m] != kOutOfRange) ? a_off[m] + ci * C::KK * 4 : kOutOfRange;
+            load_taps<C::KK>(rw, off, A.v[m][c4]);
         }
-        wr[j] = v;
     }
 }
 
+// Per-lane offsets of the halo DMA, the same for every stage: DMA instruction
+// i of a stage fills LDS words [64*i, 64*i + 64) of the stage buffer, lane l
+// word 64*i + l; wave w issues instructions w, w + NW, w + 2*NW, ...
 template <class C>
-__device__ __forceinline__ void store_stage(float *buf, const float (&xr)[C::XPT], const float (&wr)[C::WPT])
+__device__ __forceinline__ void halo_offsets(int (&xo)[C::XPT], const IgArgs &a, int wave, int lane, int ih0,
+                                             int iw0)
 {
-    const int tid = threadIdx.x;
-    float *wl = buf;
-    float *xl = buf + C::WSZ;
 #pragma unroll
     for (int j = 0; j < C::XPT; ++j) {
-        const int e = tid + j * C::NT;
-        if (e < C::XE) {
-            const int c = e / (C::HR * C::HC);
-            const int rem = e - c * (C::HR * C::HC);
-            xl[c * C::PL + rem] = xr[j];
-        }
+        const int e = (j * C::NW + wave) * 64 + lane;
+        const int c = e / C::PL;
+        const int rem = e - c * C::PL;
+        const int r = rem / C::HCP;
+        const int col = rem - r * C::HCP;
+        const int ih = ih0 + r, iw = iw0 + col;
+        const bool ok = c < C::CC && col < C::HC && ih >= 0 && ih < a.h && iw >= 0 && iw < a.w;
+        xo[j] = ok ? ((c * a.h + ih) * a.w + iw) * 4 : kOutOfRange;
     }
+}
+
+// Issue the halo DMA of the stage starting at input channel ci0 into `buf`.
+// Channels at or past C_in lie past the descriptor's end and read 0.
+template <class C>
+__device__ __forceinline__ void dma_halo(float *buf, const float *__restrict__ x, const IgArgs &a, int ci0, int wave,
+                                         const int (&xo)[C::XPT])
+{
+    const unsigned plane = (unsigned)a.h * (unsigned)a.w;
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc(x + (size_t)ci0 * plane, (unsigned)(a.c_in - ci0) * plane * 4u);
+    constexpr int kFull = C::NIX / C::NW;  // rounds in which every wave issues one
 #pragma unroll
-    for (int j = 0; j < C::WPT; ++j) {
-        const int e = tid + j * C::NT;
-        if (e < C::WE) {
-            const int row = e / C::WROW;
-            const int q = e - row * C::WROW;
-            wl[row * C::RS + q] = wr[j];
+    for (int j = 0; j < kFull; ++j)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_ptr_t)(buf + (j * C::NW + wave) * 64), 4, xo[j], 0, 0, 0);
+    if constexpr (kFull < C::XPT) {
+        if (kFull * C::NW + wave < C::NIX)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_ptr_t)(buf + (kFull * C::NW + wave) * 64), 4,
+                                                     xo[kFull], 0, 0, 0);
+    }
+}
+
+// Every load in flight (this wave's DMA and weight registers) has landed, and
+// then every wave's.  The wait is the builtin (vmcnt = 0, expcnt and lgkmcnt
+// left at their maxima) rather than inline assembly so that the compiler
+// knows the loads are complete and adds no waits of its own later.
+__device__ __forceinline__ void stage_ready()
+{
+    __builtin_amdgcn_s_waitcnt(0x0F70);
+    __syncthreads();
+}
+
+// B fragments (input patches) of step st for one wave.
+template <class C>
+__device__ __forceinline__ void read_b(const float *xl, const int (&b_base)[C::NB], int st, float (&bv)[C::NB])
+{
+    const int t = st / C::G4, c4 = st % C::G4;
+    const int kh = t / C::KS, kw = t % C::KS;
+#pragma unroll
+    for (int n = 0; n < C::NB; ++n) bv[n] = xl[b_base[n] + 4 * C::NWK * c4 * C::PL + kh * C::HCP + kw];
+}
+
+// One stage of MFMA work for one wave: every tap, this wave's channel groups,
+// all MA x NB accumulator blocks.  The B fragments are software pipelined by
+// one step: the LDS reads of step s+1 are issued before the matrix
+// instructions of step s, and scheduling barriers keep the compiler from
+// sinking them -- a wave issues in order, so reads placed behind a run of
+// MFMAs would only start once the whole run had issued, leaving the matrix
+// pipe to wait on them.
+template <class C>
+__device__ __forceinline__ void compute_stage(const float *xl, const AStage<C> &A, const int (&b_base)[C::NB],
+                                              floatx4 (&acc)[C::MA][C::NB])
+{
+    constexpr int kSteps = C::KK * C::G4;
+    float bv[2][C::NB];
+    read_b<C>(xl, b_base, 0, bv[0]);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int st = 0; st < kSteps; ++st) {
+        const int cur = st & 1;
+        const int t = st / C::G4, c4 = st % C::G4;
+        if (st + 1 < kSteps) read_b<C>(xl, b_base, st + 1, bv[cur ^ 1]);
+#pragma unroll
+        for (int m = 0; m < C::MA; ++m)
+#pragma unroll
+            for (int n = 0; n < C::NB; ++n)
+                acc[m][n] = __builtin_amdgcn_mfma_f32_16x16x4f32(A.v[m][c4][t], bv[cur][n], acc[m][n], 0, 0, 0);
+        // Within the step: one matrix instruction, then one read of the next
+        // step, so the reads issue while the matrix pipe is busy.
+#pragma unroll
+        for (int i = 0; i < C::MA * C::NB; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
         }
+        __builtin_amdgcn_sched_barrier(0);
     }
 }
 
 template <class C>
 __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x, const float *__restrict__ w,
                                                     const float *__restrict__ bias, float *__restrict__ out,
-                                                    float *__restrict__ ws, IgArgs a)
+                                                    float *__restrict__ part, IgArgs a)
 {
-    __shared__ __attribute__((aligned(16))) float lds[2 * C::BUF];
-    __shared__ unsigned s_last;
+    // Two stage buffers in separate LDS objects, so the compiler can tell a
+    // read of one from the DMA filling the other.
+    __shared__ __attribute__((aligned(16))) float lds0[C::BUF0];
+    __shared__ __attribute__((aligned(16))) float lds1[C::XSZ];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wc = wave % C::NWC;
-    const int wp = wave / C::NWC;
+    const int wp = (wave / C::NWC) % C::NWP;
+    const int wk = wave / (C::NWC * C::NWP);
     const int g = lane >> 4;
     const int l16 = lane & 15;
 
-    const int tile = blockIdx.x;
+    // Workgroup -> (split, tile).  Workgroups are dealt round-robin to the 8
+    // XCDs (workgroup i to XCD i mod 8), each with its own L2; giving every
+    // XCD a contiguous run of tiles keeps neighbouring tiles -- which share
+    // halo rows and output cache lines -- in one L2.
+    const int nwg = (int)gridDim.x;
+    const int xcd = (int)blockIdx.x % 8, slot = (int)blockIdx.x / 8;
+    const int per = nwg / 8, extra = nwg % 8;
+    const int lin = xcd * per + min(xcd, extra) + slot;
+    const int ntiles = nwg / a.splits;
+    const int split = lin / ntiles;
+    const int tile = lin - split * ntiles;
     const int co_t = tile % a.co_tiles;
     const int sp = tile / a.co_tiles;
     const int tw_i = sp % a.tiles_w;
     const int th_i = sp / a.tiles_w;
-    const int split = blockIdx.y;
     const int co0 = co_t * C::COT;
     const int oh0 = th_i * C::TH, ow0 = tw_i * C::TW;
     const int ih0 = oh0 * C::S - a.pad, iw0 = ow0 * C::S - a.pad;
     const int c_begin = split * a.chunks_per_split;
     const int c_end = min(c_begin + a.chunks_per_split, a.nchunks);
 
-    // Per-lane LDS bases of the two MFMA operands.
-    const int a_base = (wc * 16 * C::MA + l16) * C::RS + g * C::KK;
+    // Weight operand: lane (g, l16) of m-block m loads output channel
+    // co0 + wc*16*MA + 16*m + l16.
+    const __amdgpu_buffer_rsrc_t rw = make_rsrc(w, (unsigned)a.c_out * a.c_in * C::KK * 4u);
+    const int ci_lane = 4 * wk + g;
+    int a_off[C::MA];
+#pragma unroll
+    for (int m = 0; m < C::MA; ++m) {
+        const int co = co0 + wc * 16 * C::MA + 16 * m + l16;
+        a_off[m] = co < a.c_out ? co * a.c_in * C::KK * 4 : kOutOfRange;
+    }
+
+    // Input operand: LDS base of each pixel block for this lane.
     int b_base[C::NB];
 #pragma unroll
     for (int nb = 0; nb < C::NB; ++nb) {
         int p = (wp * C::NB + nb) * 16 + l16;
         if (p >= C::NPIX) p = 0;  // padding lanes read a valid word; never stored
-        b_base[nb] = g * C::PL + (p / C::TW) * C::S * C::HC + (p % C::TW) * C::S;
+        b_base[nb] = ci_lane * C::PL + (p / C::TW) * C::S * C::HCP + (p % C::TW) * C::S;
     }
 
     floatx4 acc[C::MA][C::NB];
@@ -202,99 +328,109 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
 #pragma unroll
         for (int n = 0; n < C::NB; ++n) acc[m][n] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-    float xr[C::XPT], wr[C::WPT];
-    if (c_begin < c_end) {
-        load_stage<C>(x, w, a, c_begin * C::CC, ih0, iw0, co0, xr, wr);
-        store_stage<C>(lds, xr, wr);
-    }
-    __syncthreads();
+    int xo[C::XPT];
+    halo_offsets<C>(xo, a, wave, lane, ih0, iw0);
+    AStage<C> a0, a1;
+    dma_halo<C>(lds0, x, a, c_begin * C::CC, wave, xo);
+    load_a<C>(a0, rw, a, a_off, ci_lane, c_begin * C::CC);
+    stage_ready();
 
-    for (int ch = c_begin; ch < c_end; ++ch) {
-        const int it = ch - c_begin;
-        const bool more = ch + 1 < c_end;
-        if (more) load_stage<C>(x, w, a, (ch + 1) * C::CC, ih0, iw0, co0, xr, wr);
-
-        const float *wl = lds + (it & 1) * C::BUF;
-        const float *xl = wl + C::WSZ;
-#pragma unroll
-        for (int t = 0; t < C::KK; ++t) {
-            const int kh = t / C::KS, kw = t % C::KS;
-#pragma unroll
-            for (int c4 = 0; c4 < C::CC / 4; ++c4) {
-                float av[C::MA], bv[C::NB];
-#pragma unroll
-                for (int m = 0; m < C::MA; ++m) av[m] = wl[a_base + m * 16 * C::RS + c4 * 4 * C::KK + t];
-#pragma unroll
-                for (int n = 0; n < C::NB; ++n) bv[n] = xl[b_base[n] + c4 * 4 * C::PL + kh * C::HC + kw];
-#pragma unroll
-                for (int m = 0; m < C::MA; ++m)
-#pragma unroll
-                    for (int n = 0; n < C::NB; ++n)
-                        acc[m][n] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[m], bv[n], acc[m][n], 0, 0, 0);
-            }
+    for (int ch = c_begin; ch < c_end; ch += 2) {
+        if (ch + 1 < c_end) {
+            dma_halo<C>(lds1, x, a, (ch + 1) * C::CC, wave, xo);
+            load_a<C>(a1, rw, a, a_off, ci_lane, (ch + 1) * C::CC);
         }
-        if (more) store_stage<C>(lds + ((it + 1) & 1) * C::BUF, xr, wr);
+        compute_stage<C>(lds0, a0, b_base, acc);
+        stage_ready();
+        if (ch + 1 >= c_end) break;
+        if (ch + 2 < c_end) {
+            dma_halo<C>(lds0, x, a, (ch + 2) * C::CC, wave, xo);
+            load_a<C>(a0, rw, a, a_off, ci_lane, (ch + 2) * C::CC);
+        }
+        compute_stage<C>(lds1, a1, b_base, acc);
+        stage_ready();
+    }
+
+    // Sum the NWK channel-group partials: waves wk > 0 park theirs in LDS
+    // (the stage buffers are free after the last barrier), waves wk = 0 add.
+    if constexpr (C::NWK > 1) {
+        constexpr int per_wave = C::MA * C::NB * 4 * 64;
+        const int wcp = wave % (C::NWC * C::NWP);
+        if (wk > 0) {
+            float *park = lds0 + ((wk - 1) * C::NWC * C::NWP + wcp) * per_wave + lane;
+#pragma unroll
+            for (int m = 0; m < C::MA; ++m)
+#pragma unroll
+                for (int n = 0; n < C::NB; ++n)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) park[((m * C::NB + n) * 4 + r) * 64] = acc[m][n][r];
+        }
         __syncthreads();
+        if (wk > 0) return;
+#pragma unroll
+        for (int k = 1; k < C::NWK; ++k) {
+            const float *src = lds0 + ((k - 1) * C::NWC * C::NWP + wcp) * per_wave + lane;
+#pragma unroll
+            for (int m = 0; m < C::MA; ++m)
+#pragma unroll
+                for (int n = 0; n < C::NB; ++n)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) acc[m][n][r] += src[((m * C::NB + n) * 4 + r) * 64];
+        }
     }
 
     // Accumulator block (m, n), register r holds output channel
     // co0 + wc*16*MA + m*16 + 4*g + r at tile pixel (wp*NB + n)*16 + l16.
-    if (a.splits == 1) {
+    // Split workgroups write slice `split` of the partial sums, in the
+    // output's layout, without the bias.  Stores go through a buffer
+    // descriptor: a lane outside the output (pixel or channel) gets an offset
+    // of at least 2^30 bytes, past the descriptor's range (< 2^30, checked
+    // when the plan is made), and its store is dropped.
+    const unsigned plane_b = (unsigned)a.h_out * a.w_out * 4u;
+    const unsigned out_b = (unsigned)a.c_out * plane_b;
+    const __amdgpu_buffer_rsrc_t ro = make_rsrc(a.splits == 1 ? out : part + (size_t)split * (out_b / 4), out_b);
+    constexpr unsigned kFar = 1u << 30;
+    unsigned pix_off[C::NB];
 #pragma unroll
-        for (int m = 0; m < C::MA; ++m) {
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int co = co0 + wc * 16 * C::MA + m * 16 + 4 * g + r;
-                const float b = (bias && co < a.c_out) ? bias[co] : 0.f;
-#pragma unroll
-                for (int n = 0; n < C::NB; ++n) {
-                    const int p = (wp * C::NB + n) * 16 + l16;
-                    const int oh = oh0 + p / C::TW, ow = ow0 + p % C::TW;
-                    if (p < C::NPIX && co < a.c_out && oh < a.h_out && ow < a.w_out)
-                        out[((size_t)co * a.h_out + oh) * a.w_out + ow] = acc[m][n][r] + b;
-                }
-            }
-        }
-        return;
+    for (int n = 0; n < C::NB; ++n) {
+        const int p = (wp * C::NB + n) * 16 + l16;
+        const int oh = oh0 + p / C::TW, ow = ow0 + p % C::TW;
+        pix_off[n] = (p < C::NPIX && oh < a.h_out && ow < a.w_out) ? (unsigned)(oh * a.w_out + ow) * 4u : kFar;
     }
-
-    // Split input channels: publish this partial tile, count arrivals.
-    unsigned *counters = reinterpret_cast<unsigned *>(ws);
-    float *part = ws + a.part_offset + (size_t)tile * a.splits * (C::COT * C::NPIXP);
-    float *mine = part + (size_t)split * (C::COT * C::NPIXP);
 #pragma unroll
-    for (int m = 0; m < C::MA; ++m)
+    for (int m = 0; m < C::MA; ++m) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-            const int col = wc * 16 * C::MA + m * 16 + 4 * g + r;
+            const int co = co0 + wc * 16 * C::MA + m * 16 + 4 * g + r;
+            const bool co_ok = co < a.c_out;
+            const float b = (a.splits == 1 && bias && co_ok) ? bias[co] : 0.f;
+            const unsigned chan_off = co_ok ? (unsigned)co * plane_b : kFar;
 #pragma unroll
             for (int n = 0; n < C::NB; ++n)
-                mine[col * C::NPIXP + (wp * C::NB + n) * 16 + l16] = acc[m][n][r];
-        }
-    __threadfence();
-    __syncthreads();
-    if (tid == 0) s_last = (atomicAdd(&counters[tile], 1u) == (unsigned)(a.splits - 1)) ? 1u : 0u;
-    __syncthreads();
-    if (!s_last) return;
-    __threadfence();
-    for (int e = tid; e < C::COT * C::NPIX; e += C::NT) {
-        const int col = e / C::NPIX;
-        const int p = e - col * C::NPIX;
-        const int co = co0 + col;
-        const int oh = oh0 + p / C::TW, ow = ow0 + p % C::TW;
-        if (co < a.c_out && oh < a.h_out && ow < a.w_out) {
-            float s = 0.f;
-            for (int k = 0; k < a.splits; ++k) s += part[(size_t)k * (C::COT * C::NPIXP) + col * C::NPIXP + p];
-            out[((size_t)co * a.h_out + oh) * a.w_out + ow] = s + (bias ? bias[co] : 0.f);
+                __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, acc[m][n][r] + b), ro,
+                                                      (int)(chan_off + pix_off[n]), 0, 0);
         }
     }
-    if (tid == 0) counters[tile] = 0u;  // ready for the next call
+}
+
+// out[i] = part[0][i] + part[1][i] + ... + part[splits-1][i] + bias[channel(i)],
+// summed in that order.
+__global__ __launch_bounds__(256) void sum_splits(const float *__restrict__ part, const float *__restrict__ bias,
+                                                  float *__restrict__ out, int splits, int plane, int64_t total)
+{
+    int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int64_t step = (int64_t)gridDim.x * 256;
+    for (; i < total; i += step) {
+        float s = part[i];
+        for (int k = 1; k < splits; ++k) s += part[(size_t)k * total + i];
+        out[i] = s + (bias ? bias[i / plane] : 0.f);
+    }
 }
 
 struct Variant {
     const char *name;
-    int ks, s, th, tw, nwc, nwp, ma, cc;
-    int nt, npixp, cot, lds;
+    int ks, s, th, tw, nwc, nwp, nwk, ma, cc;
+    int nt, cot, lds;
     void (*launch)(dim3 grid, hipStream_t st, const float *, const float *, const float *, float *, float *,
                    const IgArgs &);
 };
@@ -309,35 +445,30 @@ void launch_cfg(dim3 grid, hipStream_t st, const float *x, const float *w, const
 template <class C>
 constexpr Variant make_variant(const char *name)
 {
-    return Variant{name, C::KS, C::S, C::TH, C::TW, C::NWC, C::NWP, C::MA, C::CC,
-                   C::NT, C::NPIXP, C::COT, C::LDS_BYTES, &launch_cfg<C>};
+    return Variant{name, C::KS, C::S, C::TH, C::TW, C::NWC, C::NWP, C::NWK, C::MA, C::CC,
+                   C::NT, C::COT, C::LDS_BYTES, &launch_cfg<C>};
 }
 
-//                       KS S  TH  TW NWC NWP MA CC
-using K3S1_T14_C64 = Cfg<3, 1, 14, 14, 4, 1, 1, 8>;
-using K3S1_T7_C64 = Cfg<3, 1, 7, 7, 4, 1, 1, 8>;
-using K3S1_T14_C128 = Cfg<3, 1, 14, 14, 4, 1, 2, 4>;
-using K3S1_T8x32_C64 = Cfg<3, 1, 8, 32, 2, 2, 2, 4>;
-using K3S2_T7_C64 = Cfg<3, 2, 7, 7, 4, 1, 1, 8>;
-using K1S1_T7_C64 = Cfg<1, 1, 7, 7, 4, 1, 1, 16>;
-using K1S1_T14_C64 = Cfg<1, 1, 14, 14, 4, 1, 1, 16>;
-using K5S1_T7_C64 = Cfg<5, 1, 7, 7, 4, 1, 1, 4>;
-
+//                                  KS S  TH  TW NWC NWP NWK MA CC
 const Variant kVariants[] = {
-    make_variant<K3S1_T14_C64>("k3s1_t14x14_co64"),
-    make_variant<K3S1_T7_C64>("k3s1_t7x7_co64"),
-    make_variant<K3S1_T14_C128>("k3s1_t14x14_co128"),
-    make_variant<K3S1_T8x32_C64>("k3s1_t8x32_co64"),
-    make_variant<K3S2_T7_C64>("k3s2_t7x7_co64"),
-    make_variant<K1S1_T7_C64>("k1s1_t7x7_co64"),
-    make_variant<K1S1_T14_C64>("k1s1_t14x14_co64"),
-    make_variant<K5S1_T7_C64>("k5s1_t7x7_co64"),
+    make_variant<Cfg<3, 1, 14, 14, 2, 1, 2, 2, 8>>("k3s1_t14x14_co64_k2"),
+    make_variant<Cfg<3, 1, 14, 14, 2, 1, 2, 2, 16>>("k3s1_t14x14_co64_k2_cc16"),
+    make_variant<Cfg<3, 1, 14, 14, 4, 1, 1, 1, 8>>("k3s1_t14x14_co64"),
+    make_variant<Cfg<3, 1, 14, 14, 4, 1, 1, 2, 8>>("k3s1_t14x14_co128"),
+    make_variant<Cfg<3, 1, 7, 7, 4, 1, 1, 1, 8>>("k3s1_t7x7_co64"),
+    make_variant<Cfg<3, 1, 7, 7, 4, 1, 4, 1, 16>>("k3s1_t7x7_co64_k4"),
+    make_variant<Cfg<3, 1, 8, 32, 2, 2, 1, 2, 8>>("k3s1_t8x32_co64"),
+    make_variant<Cfg<3, 2, 7, 7, 4, 1, 1, 1, 8>>("k3s2_t7x7_co64"),
+    make_variant<Cfg<3, 2, 7, 7, 4, 1, 4, 1, 16>>("k3s2_t7x7_co64_k4"),
+    make_variant<Cfg<1, 1, 7, 7, 4, 1, 1, 1, 16>>("k1s1_t7x7_co64"),
+    make_variant<Cfg<1, 1, 7, 7, 4, 1, 4, 1, 32>>("k1s1_t7x7_co64_k4"),
+    make_variant<Cfg<1, 1, 14, 14, 4, 1, 1, 1, 16>>("k1s1_t14x14_co64"),
+    make_variant<Cfg<5, 1, 7, 7, 4, 1, 1, 1, 4>>("k5s1_t7x7_co64"),
+    make_variant<Cfg<5, 1, 7, 7, 4, 1, 2, 1, 8>>("k5s1_t7x7_co64_k2"),
 };
 constexpr int kNumVariants = sizeof(kVariants) / sizeof(kVariants[0]);
 
 constexpr int kCUs = 256;
-
-size_t part_offset_floats() { return kCounterBytes / sizeof(float); }
 
 }  // namespace
 
@@ -360,12 +491,15 @@ bool igemm_make_plan(const ConvShape &s, int variant, int splits, ilpm_plan *p)
     if (variant < 0 || variant >= kNumVariants) return false;
     const Variant &d = kVariants[variant];
     if (d.ks != s.k || d.s != s.stride) return false;
+    // Load offsets are 31-bit byte offsets.
+    if ((int64_t)s.c_in * s.h * s.w * 4 >= (1LL << 31)) return false;
+    if ((int64_t)s.c_out * s.c_in * s.k * s.k * 4 >= (1LL << 31)) return false;
+    if ((int64_t)s.c_out * s.h_out * s.w_out * 4 >= (1LL << 30)) return false;
     const long tiles = (long)ceil_div(s.h_out, d.th) * ceil_div(s.w_out, d.tw) * ceil_div(s.c_out, d.cot);
     if (tiles > 0x7fffffffL) return false;
     const int nchunks = ceil_div(s.c_in, d.cc);
     if (splits <= 0) {
-        // Enough workgroups to give every compute unit one, without splitting a
-        // stage.
+        // Enough workgroups to give every compute unit one.
         splits = 1;
         if (tiles < kCUs) splits = (int)((kCUs + tiles - 1) / tiles);
         if (splits > nchunks) splits = nchunks;
@@ -373,8 +507,8 @@ bool igemm_make_plan(const ConvShape &s, int variant, int splits, ilpm_plan *p)
     if (splits > nchunks) return false;
     const int cps = ceil_div(nchunks, splits);
     splits = ceil_div(nchunks, cps);  // no empty split
-    if (splits > 1 && tiles > kMaxTileCounters) return false;
     if (splits > 65535) return false;
+    const size_t out_elems = (size_t)s.c_out * s.h_out * s.w_out;
     ilpm_plan q = {};
     q.path = ILPM_PATH_IGEMM;
     q.variant = variant;
@@ -388,9 +522,7 @@ bool igemm_make_plan(const ConvShape &s, int variant, int splits, ilpm_plan *p)
     q.lds_bytes = d.lds;
     q.h_out = s.h_out;
     q.w_out = s.w_out;
-    q.workspace_bytes = splits > 1
-                            ? kCounterBytes + sizeof(float) * (size_t)tiles * splits * d.cot * d.npixp
-                            : 0;
+    q.workspace_bytes = splits > 1 ? sizeof(float) * out_elems * splits : 0;
     *p = q;
     return true;
 }
@@ -400,20 +532,24 @@ double igemm_plan_cost(const ConvShape &s, const ilpm_plan &p)
     const Variant &d = kVariants[p.variant];
     const int nchunks = ceil_div(s.c_in, d.cc);
     const int cps = ceil_div(nchunks, p.splits);
-    const int nb = d.npixp / (16 * d.nwp);
-    // MFMA cycles of one wave for one stage: taps * channel groups * blocks * 32.
-    const double stage = (double)d.ks * d.ks * (d.cc / 4) * d.ma * nb * 32.0;
-    const double stage_overhead = 600.0;  // barrier, LDS stores, issue gaps
-    double wg = cps * (stage + stage_overhead) + 3000.0;  // + first load and epilogue
+    const int nb = ceil_div(d.th * d.tw, 16 * d.nwp);
+    // MFMA cycles of one SIMD for one stage: a workgroup's waves share the
+    // compute unit's four SIMDs.
+    const int waves = d.nwc * d.nwp * d.nwk;
+    const double stage_wave = (double)d.ks * d.ks * (d.cc / 4 / d.nwk) * d.ma * nb * 32.0;
+    const double stage_simd = stage_wave * waves / 4.0;
+    const double stage_overhead = 700.0;
+    double wg = cps * (stage_simd + stage_overhead) + 6000.0;
+    if (d.nwk > 1) wg += 1500.0;
+    const double rounds = std::ceil((double)p.grid / kCUs);
+    double cycles = rounds * wg;
     if (p.splits > 1) {
-        // Partial tile out, and the reducer reads every partial back
-        // (~13 bytes per cycle per compute unit of HBM bandwidth).
-        const double bytes = 4.0 * d.cot * d.npixp;
-        wg += bytes / 13.0 + bytes * p.splits / 13.0 / 2.0;
+        // Partial sums out and back in (~10 bytes per cycle per compute unit),
+        // plus the second launch.
+        const double bytes = 4.0 * s.c_out * s.h_out * s.w_out * (2.0 * p.splits + 1.0);
+        cycles += bytes / (10.0 * kCUs) + 4000.0;
     }
-    const long wgs = (long)p.grid;
-    const double rounds = std::ceil((double)wgs / kCUs);
-    return rounds * wg;
+    return cycles;
 }
 
 hipError_t igemm_launch(const ilpm_plan &p, const ConvShape &s, const float *x, const float *w,
@@ -433,9 +569,16 @@ hipError_t igemm_launch(const ilpm_plan &p, const ConvShape &s, const float *x, 
     a.nchunks = ceil_div(s.c_in, d.cc);
     a.chunks_per_split = ceil_div(a.nchunks, p.splits);
     a.splits = p.splits;
-    a.part_offset = part_offset_floats();
     const int tiles = p.grid / p.splits;
-    d.launch(dim3(tiles, p.splits), stream, x, w, bias, out, static_cast<float *>(workspace), a);
+    float *part = static_cast<float *>(workspace);
+    d.launch(dim3(tiles * p.splits), stream, x, w, bias, out, part, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || p.splits == 1) return e;
+    const int64_t total = (int64_t)s.c_out * s.h_out * s.w_out;
+    int64_t blocks = (total + 255) / 256;
+    if (blocks > 4096) blocks = 4096;
+    hipLaunchKernelGGL(sum_splits, dim3((unsigned)blocks), dim3(256), 0, stream, part, bias, out, p.splits,
+                       s.h_out * s.w_out, total);
     return hipGetLastError();
 }
 

@@ -147,7 +147,7 @@ int device_check(int *dev_out)
     return g_arch[dev] == 1 ? ILPM_OK : ILPM_ERR_ARCH;
 }
 
-int get_workspace(int dev, size_t need, hipStream_t stream, void **ws)
+int get_workspace(int dev, size_t need, void **ws)
 {
     *ws = nullptr;
     if (need == 0) return ILPM_OK;
@@ -170,11 +170,6 @@ int get_workspace(int dev, size_t need, hipStream_t stream, void **ws)
         const size_t bytes = ((need + (1u << 20) - 1) >> 20) << 20;
         void *p = nullptr;
         if ((e = hipMalloc(&p, bytes)) != hipSuccess) return hip_fail(e);
-        (void)hipGetLastError();
-        if ((e = launch_fill_zero(p, bytes, stream)) != hipSuccess) {
-            (void)hipFree(p);
-            return hip_fail(e);
-        }
         w.own = p;
         w.own_bytes = bytes;
     }
@@ -204,7 +199,7 @@ int run(const float *in, const float *w, const float *bias, const ConvShape &s, 
     int rc = device_check(&dev);
     if (rc != ILPM_OK) return rc;
     void *ws = nullptr;
-    rc = get_workspace(dev, p.workspace_bytes, stream, &ws);
+    rc = get_workspace(dev, p.workspace_bytes, &ws);
     if (rc != ILPM_OK) return rc;
     log_plan(s, p);
     // Launch errors are read back with hipGetLastError; drop any error an
@@ -303,15 +298,12 @@ int ilpm_last_hip_error(void) { return g_last_hip; }
 
 int ilpm_set_workspace(void *ptr, size_t bytes, hipStream_t stream)
 {
+    (void)stream;
     if (ptr && ((uintptr_t)ptr & 255u)) return ILPM_ERR_INVALID_ARG;
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return hip_fail(e);
     if (dev < 0 || dev >= kMaxDevices) return hip_fail(hipErrorInvalidDevice);
-    if (ptr && bytes > 0) {
-        (void)hipGetLastError();
-        if ((e = launch_fill_zero(ptr, bytes, stream)) != hipSuccess) return hip_fail(e);
-    }
     std::lock_guard<std::mutex> lk(g_mu);
     g_ws[dev].user = ptr;
     g_ws[dev].user_bytes = ptr ? bytes : 0;

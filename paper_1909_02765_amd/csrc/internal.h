@@ -14,12 +14,6 @@ struct ConvShape {
     int c_in, h, w, c_out, k, stride, pad, h_out, w_out;
 };
 
-// Split-K bookkeeping lives at the start of the workspace: one arrival
-// counter per output tile, always returned to zero by the workgroup that
-// reduces the tile.  Partial sums follow, 256-byte aligned.
-constexpr int kMaxTileCounters = 65536;
-constexpr size_t kCounterBytes = sizeof(unsigned) * kMaxTileCounters;
-
 // ---- direct (VALU) family ----
 int direct_num_variants();
 bool direct_variant_info(int v, int *k, int *stride, int *tile_h, int *tile_w, int *co_tile);
@@ -39,7 +33,6 @@ hipError_t igemm_launch(const ilpm_plan &p, const ConvShape &s, const float *x, 
                         const float *bias, float *out, void *workspace, hipStream_t stream);
 
 // ---- helpers ----
-hipError_t launch_fill_zero(void *p, size_t bytes, hipStream_t stream);
 hipError_t launch_relu(float *x, int64_t n, hipStream_t stream);
 hipError_t launch_maxpool2x2(const float *in, int c, int h, int w, float *out, hipStream_t stream);
 

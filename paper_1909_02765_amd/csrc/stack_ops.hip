@@ -1,17 +1,9 @@
 // Elementwise helpers used between the convolutions of a layer stack (ReLU,
-// 2x2 max-pool) and a plain fill used to clear the workspace.  They are not
-// part of the convolution.
+// 2x2 max-pool).  They are not part of the convolution.
 #include "internal.h"
 
 namespace ilpm {
 namespace {
-
-__global__ __launch_bounds__(256) void fill_zero_kernel(uint32_t *p, size_t n)
-{
-    size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
-    const size_t step = (size_t)gridDim.x * 256;
-    for (; i < n; i += step) p[i] = 0u;
-}
 
 __global__ __launch_bounds__(256) void relu_kernel(float *x, int64_t n)
 {
@@ -52,15 +44,6 @@ int grid_for(int64_t n)
 }
 
 }  // namespace
-
-hipError_t launch_fill_zero(void *p, size_t bytes, hipStream_t stream)
-{
-    const size_t n = bytes / 4;
-    if (n == 0) return hipSuccess;
-    hipLaunchKernelGGL(fill_zero_kernel, dim3(grid_for((int64_t)n)), dim3(256), 0, stream,
-                       static_cast<uint32_t *>(p), n);
-    return hipGetLastError();
-}
 
 hipError_t launch_relu(float *x, int64_t n, hipStream_t stream)
 {

@@ -103,8 +103,8 @@ def test_plan_for_every_workload(case):
     p = ilpm.plan(d["c_in"], d["h"], d["w"], d["c_out"], d["k"], d["stride"], d["pad"])
     assert p.h_out == ilpm.out_size(d["h"], d["k"], d["stride"], d["pad"])
     assert p.w_out == ilpm.out_size(d["w"], d["k"], d["stride"], d["pad"])
-    assert p.grid >= 1 and p.block in (64, 128, 256, 512)
-    assert p.lds_bytes <= 65536
+    assert p.grid >= 1 and p.block in (64, 128, 256, 512, 768, 1024)
+    assert p.lds_bytes <= 160 * 1024
     if p.splits > 1:
         assert p.workspace_bytes > 0
     assert ilpm.workspace_size(d["c_in"], d["h"], d["w"], d["c_out"], d["k"], d["stride"], d["pad"]) \
