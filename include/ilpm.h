@@ -129,7 +129,9 @@ int ilpm_conv2d_validate(const void *in, const void *w, const void *bias,
 
 /*
  * ilpm_conv2d_plan -- the plan ilpm_conv2d_fwd uses for this shape (path,
- * tile, split count, grid, workspace).  Pure host.  The environment variables
+ * tile, split count, grid, workspace): the fastest plan measured on MI355X
+ * for this exact shape when the compiled-in tuning table lists it, else the
+ * best by a cost model.  Pure host.  The environment variables
  * ILPM_FORCE_PATH=direct|igemm and ILPM_SPLIT=n override the choice.
  */
 int ilpm_conv2d_plan(int C_in, int H, int W, int C_out, int K, int stride, int pad,
@@ -146,6 +148,9 @@ int ilpm_conv2d_plan_variant(int C_in, int H, int W, int C_out, int K, int strid
 
 /* Number of compiled variants of `path` (0 for an unknown path). */
 int ilpm_num_variants(int path);
+
+/* Name of a compiled variant (static storage), NULL if it does not exist. */
+const char *ilpm_variant_name(int path, int variant);
 
 /*
  * ilpm_variant_info -- filter size, stride (0 = any), output tile and output

@@ -50,7 +50,7 @@ class ilpm_plan(ctypes.Structure):
 
 
 if not os.path.exists(LIBRARY):
-    raise ImportError(f"{LIBRARY} is not built: run `python -m paper_1909_02765_amd.build` "
+    raise ImportError(f"{LIBRARY} is not built: run `python paper_1909_02765_amd/build.py` "
                       "(or __graft_entry__.build()) first")
 
 # PyTorch ships its own HIP runtime.  Load it first so that the library's
@@ -91,6 +91,7 @@ _SIGS = {
     "ilpm_conv2d_plan": ([_i] * 7 + [_plan_p], _i),
     "ilpm_conv2d_plan_variant": ([_i] * 10 + [_plan_p], _i),
     "ilpm_num_variants": ([_i], _i),
+    "ilpm_variant_name": ([_i, _i], ctypes.c_char_p),
     "ilpm_variant_info": ([_i, _i] + [ctypes.POINTER(_i)] * 5, _i),
     "ilpm_relu_inplace": ([_vp, ctypes.c_int64, _vp], _i),
     "ilpm_maxpool2x2": ([_vp, _i, _i, _i, _vp, _vp], _i),
@@ -149,6 +150,13 @@ def plan_variant(c_in, h, w, c_out, k, stride, pad, path, variant, splits=0) -> 
 
 def num_variants(path: int) -> int:
     return lib.ilpm_num_variants(path)
+
+
+def variant_name(path: int, variant: int) -> str:
+    n = lib.ilpm_variant_name(path, variant)
+    if n is None:
+        raise IlpmError(ERR_INVALID_ARG, "ilpm_variant_name")
+    return n.decode()
 
 
 def variant_info(path: int, variant: int):

@@ -1,7 +1,9 @@
 """Build libilpm.so (the HIP kernels and the C ABI) for gfx950 with hipcc.
 
-    python -m paper_1909_02765_amd.build            # build in-tree
-    python -m paper_1909_02765_amd.build --isa DIR  # also keep the gfx950 assembly in DIR
+    python paper_1909_02765_amd/build.py            # build in-tree
+    python paper_1909_02765_amd/build.py --isa DIR  # also keep the gfx950 assembly in DIR
+
+(Run it as a script: importing the package loads the library it builds.)
 """
 from __future__ import annotations
 

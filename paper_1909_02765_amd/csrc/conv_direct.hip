@@ -170,6 +170,13 @@ int lds_chunk(const ConvShape &s)
 
 int direct_num_variants() { return 2; }
 
+const char *direct_variant_name(int v)
+{
+    if (v == 0) return "direct_lds_t8x32_co16";
+    if (v == 1) return "direct_global";
+    return nullptr;
+}
+
 bool direct_variant_info(int v, int *k, int *stride, int *tile_h, int *tile_w, int *co_tile)
 {
     if (v < 0 || v >= 2) return false;

@@ -454,6 +454,9 @@ const Variant kVariants[] = {
     make_variant<Cfg<3, 1, 14, 14, 2, 1, 2, 2, 8>>("k3s1_t14x14_co64_k2"),
     make_variant<Cfg<3, 1, 14, 14, 2, 1, 2, 2, 16>>("k3s1_t14x14_co64_k2_cc16"),
     make_variant<Cfg<3, 1, 14, 14, 4, 1, 1, 1, 8>>("k3s1_t14x14_co64"),
+    make_variant<Cfg<3, 1, 14, 14, 4, 1, 2, 1, 8>>("k3s1_t14x14_co64_w8"),
+    make_variant<Cfg<3, 1, 14, 14, 4, 1, 2, 1, 16>>("k3s1_t14x14_co64_w8_cc16"),
+    make_variant<Cfg<3, 1, 14, 14, 4, 1, 1, 1, 16>>("k3s1_t14x14_co64_cc16"),
     make_variant<Cfg<3, 1, 14, 14, 4, 1, 1, 2, 8>>("k3s1_t14x14_co128"),
     make_variant<Cfg<3, 1, 7, 7, 4, 1, 1, 1, 8>>("k3s1_t7x7_co64"),
     make_variant<Cfg<3, 1, 7, 7, 4, 1, 4, 1, 16>>("k3s1_t7x7_co64_k4"),
@@ -473,6 +476,8 @@ constexpr int kCUs = 256;
 }  // namespace
 
 int igemm_num_variants() { return kNumVariants; }
+
+const char *igemm_variant_name(int v) { return (v >= 0 && v < kNumVariants) ? kVariants[v].name : nullptr; }
 
 bool igemm_variant_info(int v, int *k, int *stride, int *tile_h, int *tile_w, int *co_tile)
 {

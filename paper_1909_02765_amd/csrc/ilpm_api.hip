@@ -78,15 +78,19 @@ int validate(const void *in, const void *w, const void *bias, const ConvShape &s
     return ILPM_OK;
 }
 
-// The default plan: the cheapest matrix-core variant for this filter size and
-// stride by the cost model, else the LDS direct kernel, else the plain one.
+// The default plan: the measured best for this exact shape when the tuning
+// table has it, else the cheapest matrix-core variant for this filter size
+// and stride by the cost model, else the LDS direct kernel, else the plain
+// one.
 int choose_plan(const ConvShape &s, ilpm_plan *p)
 {
     const char *force = std::getenv("ILPM_FORCE_PATH");
     const char *split_env = std::getenv("ILPM_SPLIT");
     const int forced_splits = split_env ? std::atoi(split_env) : 0;
     const bool want_direct = force && std::strcmp(force, "direct") == 0;
-    if (!want_direct) {
+    const bool want_igemm = force && std::strcmp(force, "igemm") == 0;
+    if (!force && forced_splits <= 0 && tuned_plan(s, p)) return ILPM_OK;
+    if (want_igemm || !want_direct) {
         bool found = false;
         double best = 0;
         ilpm_plan bp = {};
@@ -260,6 +264,13 @@ int ilpm_conv2d_plan_variant(int C_in, int H, int W, int C_out, int K, int strid
     if (path == ILPM_PATH_IGEMM) ok = igemm_make_plan(s, variant, splits, plan);
     else if (path == ILPM_PATH_DIRECT) ok = splits <= 1 && direct_make_plan(s, variant, plan);
     return ok ? ILPM_OK : ILPM_ERR_INVALID_ARG;
+}
+
+const char *ilpm_variant_name(int path, int variant)
+{
+    if (path == ILPM_PATH_IGEMM) return igemm_variant_name(variant);
+    if (path == ILPM_PATH_DIRECT) return direct_variant_name(variant);
+    return nullptr;
 }
 
 int ilpm_num_variants(int path)

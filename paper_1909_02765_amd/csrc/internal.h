@@ -17,6 +17,7 @@ struct ConvShape {
 // ---- direct (VALU) family ----
 int direct_num_variants();
 bool direct_variant_info(int v, int *k, int *stride, int *tile_h, int *tile_w, int *co_tile);
+const char *direct_variant_name(int v);
 bool direct_make_plan(const ConvShape &s, int variant, ilpm_plan *p);
 hipError_t direct_launch(const ilpm_plan &p, const ConvShape &s, const float *x, const float *w,
                          const float *bias, float *out, hipStream_t stream);
@@ -24,6 +25,7 @@ hipError_t direct_launch(const ilpm_plan &p, const ConvShape &s, const float *x,
 // ---- implicit-GEMM (fp32 MFMA) family ----
 int igemm_num_variants();
 bool igemm_variant_info(int v, int *k, int *stride, int *tile_h, int *tile_w, int *co_tile);
+const char *igemm_variant_name(int v);
 // splits = 0 lets the family choose.
 bool igemm_make_plan(const ConvShape &s, int variant, int splits, ilpm_plan *p);
 // Modelled cost of a plan in SIMD cycles of the slowest compute unit, used to
@@ -31,6 +33,10 @@ bool igemm_make_plan(const ConvShape &s, int variant, int splits, ilpm_plan *p);
 double igemm_plan_cost(const ConvShape &s, const ilpm_plan &p);
 hipError_t igemm_launch(const ilpm_plan &p, const ConvShape &s, const float *x, const float *w,
                         const float *bias, float *out, void *workspace, hipStream_t stream);
+
+// ---- measured plan table (tuned_plans.inc) ----
+// The plan the offline sweep found fastest for this exact shape, if any.
+bool tuned_plan(const ConvShape &s, ilpm_plan *p);
 
 // ---- helpers ----
 hipError_t launch_relu(float *x, int64_t n, hipStream_t stream);

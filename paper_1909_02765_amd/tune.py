@@ -1,0 +1,133 @@
+"""Offline plan sweep (the auto-tuning step): time every compiled kernel
+variant and split count on the shapes of interest on one MI355X, keep the
+fastest per shape, and write the table the library compiles in.
+
+    python -m paper_1909_02765_amd.tune --out tuned.json          # on the GPU
+    python -m paper_1909_02765_amd.tune --emit tuned.json         # rewrite csrc/tuned_plans.inc
+
+The table maps an exact shape (C_in, H, W, C_out, K, stride, pad) to a variant
+name and a split count; shapes not in it fall back to the cost model.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import os
+import sys
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG)
+INC = os.path.join(PKG, "csrc", "tuned_plans.inc")
+
+SPLITS = (1, 2, 3, 4, 6, 8, 12, 16, 24, 32, 48, 64)
+
+
+def default_shapes():
+    sys.path.insert(0, ROOT)
+    import workloads
+    shapes = [tuple(c.dims()[k] for k in ("c_in", "h", "w", "c_out", "k", "stride", "pad"))
+              for c in workloads.SINGLE_LAYER_CASES]
+    for _, ci, co, hw, _, _ in workloads.vgg16_layers():
+        shapes.append((ci, hw, hw, co, 3, 1, 1))
+    # The 3x3 layers of ResNet (Table 2 of the paper): conv2.x .. conv5.x.
+    shapes += [(64, 56, 56, 64, 3, 1, 1), (128, 28, 28, 128, 3, 1, 1),
+               (256, 14, 14, 256, 3, 1, 1), (512, 7, 7, 512, 3, 1, 1)]
+    out = []
+    for s in shapes:
+        if s not in out:
+            out.append(s)
+    return out
+
+
+def candidate_plans(ilpm, shape):
+    c_in, h, w, c_out, k, s, p = shape
+    plans, seen = [], set()
+    for path in (ilpm.PATH_DIRECT, ilpm.PATH_IGEMM):
+        for v in range(ilpm.num_variants(path)):
+            for sp in (SPLITS if path == ilpm.PATH_IGEMM else (1,)):
+                try:
+                    pl = ilpm.plan_variant(c_in, h, w, c_out, k, s, p, path, v, sp)
+                except ilpm.IlpmError:
+                    continue
+                key = (pl.path, pl.variant, pl.splits)
+                if key not in seen:
+                    seen.add(key)
+                    plans.append(pl)
+    return plans
+
+
+def time_plan(torch, ilpm, bufs, shape, plan, reps):
+    c_in, h, w, c_out, k, s, p = shape
+    x, wt, out = bufs
+    args = (ctypes.c_void_p(x.data_ptr()), ctypes.c_void_p(wt.data_ptr()), None, c_in, h, w, c_out, k, s, p,
+            ctypes.c_void_p(out.data_ptr()), ctypes.byref(plan),
+            ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+    f = ilpm.lib.ilpm_conv2d_fwd_plan
+    for _ in range(3):
+        rc = f(*args)
+        if rc != 0:
+            raise ilpm.IlpmError(rc, "ilpm_conv2d_fwd_plan")
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        f(*args)
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) * 1000.0 / reps
+
+
+def sweep(shapes, reps=100):
+    import torch
+    import paper_1909_02765_amd as ilpm
+    torch.cuda.set_device(0)
+    result = {}
+    for shape in shapes:
+        c_in, h, w, c_out, k, s, p = shape
+        ho, wo = ilpm.out_size(h, k, s, p), ilpm.out_size(w, k, s, p)
+        x = torch.rand((1, c_in, h, w), device="cuda")
+        wt = torch.randn((c_out, c_in, k, k), device="cuda") * 0.05
+        out = torch.empty((1, c_out, ho, wo), device="cuda")
+        rows = []
+        for plan in candidate_plans(ilpm, shape):
+            if plan.path == ilpm.PATH_DIRECT and plan.variant == 1 and c_in * c_out * ho * wo * k * k > 3e8:
+                continue  # the plain fallback is far too slow to matter here
+            us = time_plan(torch, ilpm, (x, wt, out), shape, plan, reps)
+            rows.append({"variant": ilpm.variant_name(plan.path, plan.variant), "path": plan.path,
+                         "splits": plan.splits, "us": round(us, 3)})
+        rows.sort(key=lambda r: r["us"])
+        key = ",".join(str(v) for v in shape)
+        result[key] = {"best": rows[0], "top": rows[:8]}
+        print(key, rows[0], flush=True)
+    return result
+
+
+def emit(table, path=INC):
+    lines = ["// {C_in, H, W, C_out, K, stride, pad, \"variant\", splits}",
+             "// Fastest measured plan per shape on one MI355X (written by tune.py --emit)."]
+    for key, v in sorted(table.items(), key=lambda kv: [int(t) for t in kv[0].split(",")]):
+        b = v["best"]
+        lines.append("{%s, \"%s\", %d},  // %.2f us" % (key.replace(",", ", "), b["variant"], b["splits"], b["us"]))
+    with open(path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--out", default=None, help="write the sweep as JSON")
+    ap.add_argument("--emit", default=None, help="JSON from a sweep -> csrc/tuned_plans.inc")
+    ap.add_argument("--reps", type=int, default=100)
+    args = ap.parse_args()
+    if args.emit:
+        with open(args.emit) as f:
+            emit(json.load(f))
+        return
+    table = sweep(default_shapes(), args.reps)
+    if args.out:
+        with open(args.out, "w") as f:
+            json.dump(table, f, indent=1)
+
+
+if __name__ == "__main__":
+    main()

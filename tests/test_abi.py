@@ -141,3 +141,26 @@ def test_fwd_plan_rejects_foreign_plan():
     rc = ilpm.lib.ilpm_conv2d_fwd_plan(0x1000, 0x10000000, None, 64, 28, 28, 64, 3, 1, 1, 0x20000000,
                                        ctypes.byref(p), None)
     assert rc == ilpm.ERR_INVALID_ARG
+
+
+def test_tuned_table_entries_resolve():
+    """Every entry of the compiled-in tuning table names a variant that exists
+    and accepts its shape, and the default plan for that shape is that entry."""
+    import re
+    inc = os.path.join(ROOT, "paper_1909_02765_amd", "csrc", "tuned_plans.inc")
+    rows = re.findall(r'\{(\d+), (\d+), (\d+), (\d+), (\d+), (\d+), (\d+), "([^"]*)", (\d+)\}', open(inc).read())
+    names = {(path, ilpm.variant_name(path, v)): v for path in (0, 1) for v in range(ilpm.num_variants(path))}
+    n = 0
+    for r in rows:
+        c_in, h, w, c_out, k, s, p = map(int, r[:7])
+        if c_in == 0:
+            continue
+        name, splits = r[7], int(r[8])
+        path = 1 if (1, name) in names else 0
+        assert (path, name) in names, f"unknown variant {name}"
+        plan = ilpm.plan(c_in, h, w, c_out, k, s, p)
+        assert plan.path == path and ilpm.variant_name(plan.path, plan.variant) == name
+        if path == 1:
+            assert plan.splits == splits
+        n += 1
+    assert n >= 10
