@@ -262,6 +262,145 @@ __device__ __forceinline__ void compute_stage(const float *xl, const AStage<C> &
     }
 }
 
+// Where and how one wave stores its accumulators.
+template <class C>
+struct Epilogue {
+    __amdgpu_buffer_rsrc_t ro;
+    unsigned pix_off[C::NB];   // byte offset of each pixel block's lane pixel
+    unsigned chan_off[C::MA][4];
+    float b[C::MA][4];
+
+    __device__ __forceinline__ void init(const IgArgs &a, float *out, float *part, const float *bias, int split,
+                                         int co_lane, int wp, int l16, int oh0, int ow0)
+    {
+        constexpr unsigned kFar = 1u << 30;
+        const unsigned plane_b = (unsigned)a.h_out * a.w_out * 4u;
+        const unsigned out_b = (unsigned)a.c_out * plane_b;
+        ro = make_rsrc(a.splits == 1 ? out : part + (size_t)split * (out_b / 4), out_b);
+#pragma unroll
+        for (int n = 0; n < C::NB; ++n) {
+            const int p = (wp * C::NB + n) * 16 + l16;
+            const int oh = oh0 + p / C::TW, ow = ow0 + p % C::TW;
+            pix_off[n] = (p < C::NPIX && oh < a.h_out && ow < a.w_out) ? (unsigned)(oh * a.w_out + ow) * 4u : kFar;
+        }
+#pragma unroll
+        for (int m = 0; m < C::MA; ++m)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int co = co_lane + 16 * m + r;
+                const bool ok = co < a.c_out;
+                b[m][r] = (a.splits == 1 && bias && ok) ? bias[co] : 0.f;
+                chan_off[m][r] = ok ? (unsigned)co * plane_b : kFar;
+            }
+    }
+
+    __device__ __forceinline__ void store(int m, int n, const floatx4 &v) const
+    {
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v[r] + b[m][r]), ro,
+                                                  (int)(chan_off[m][r] + pix_off[n]), 0, 0);
+    }
+};
+
+// The last stage of a one-channel-group-per-wave plan (NWK = 1), computed in
+// groups of pixel blocks with every step of the stage before moving to the
+// next group, so that each finished group's stores are issued while the
+// following groups still compute (the output write then overlaps the matrix
+// work instead of following it).  Four blocks per group keep four
+// independent accumulator chains in flight.
+template <class C>
+__device__ __forceinline__ void compute_stage_streamed(const float *xl, const AStage<C> &A,
+                                                       const int (&b_base)[C::NB], floatx4 (&acc)[C::MA][C::NB],
+                                                       const Epilogue<C> &ep)
+{
+    constexpr int kSteps = C::KK * C::G4;
+    constexpr int GB = 4;
+    constexpr int kGroups = (C::NB + GB - 1) / GB;
+    float bv[2][GB];
+    auto read = [&](int grp, int st, float(&dst)[GB]) {
+        const int t = st / C::G4, c4 = st % C::G4;
+        const int kh = t / C::KS, kw = t % C::KS;
+#pragma unroll
+        for (int j = 0; j < GB; ++j) {
+            const int n = grp * GB + j;
+            if (n < C::NB) dst[j] = xl[b_base[n] + 4 * C::NWK * c4 * C::PL + kh * C::HCP + kw];
+        }
+    };
+    read(0, 0, bv[0]);
+    __builtin_amdgcn_sched_barrier(0);
+    int cur = 0;
+#pragma unroll
+    for (int grp = 0; grp < kGroups; ++grp) {
+#pragma unroll
+        for (int st = 0; st < kSteps; ++st) {
+            const int t = st / C::G4, c4 = st % C::G4;
+            if (st + 1 < kSteps) read(grp, st + 1, bv[cur ^ 1]);
+            else if (grp + 1 < kGroups) read(grp + 1, 0, bv[cur ^ 1]);
+#pragma unroll
+            for (int m = 0; m < C::MA; ++m)
+#pragma unroll
+                for (int j = 0; j < GB; ++j) {
+                    const int n = grp * GB + j;
+                    if (n < C::NB)
+                        acc[m][n] = __builtin_amdgcn_mfma_f32_16x16x4f32(A.v[m][c4][t], bv[cur][j], acc[m][n], 0, 0, 0);
+                }
+            __builtin_amdgcn_sched_barrier(0);
+            cur ^= 1;
+        }
+#pragma unroll
+        for (int m = 0; m < C::MA; ++m)
+#pragma unroll
+            for (int j = 0; j < GB; ++j) {
+                const int n = grp * GB + j;
+                if (n < C::NB) ep.store(m, n, acc[m][n]);
+            }
+    }
+}
+
+// The last stage and the output.  NWK = 1: streamed.  NWK > 1: compute, then
+// sum the NWK channel-group partials (waves wk > 0 park theirs in LDS once
+// every wave is past the last stage, waves wk = 0 add and store).
+template <class C>
+__device__ __forceinline__ void final_stage(const float *xl, const AStage<C> &A, const int (&b_base)[C::NB],
+                                            floatx4 (&acc)[C::MA][C::NB], float *park_area, int wave, int wk,
+                                            int lane, const Epilogue<C> &ep)
+{
+    if constexpr (C::NWK == 1) {
+        compute_stage_streamed<C>(xl, A, b_base, acc, ep);
+    } else {
+        compute_stage<C>(xl, A, b_base, acc);
+        __syncthreads();
+        constexpr int per_wave = C::MA * C::NB * 4 * 64;
+        const int wcp = wave % (C::NWC * C::NWP);
+        if (wk > 0) {
+            float *park = park_area + ((wk - 1) * C::NWC * C::NWP + wcp) * per_wave + lane;
+#pragma unroll
+            for (int m = 0; m < C::MA; ++m)
+#pragma unroll
+                for (int n = 0; n < C::NB; ++n)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) park[((m * C::NB + n) * 4 + r) * 64] = acc[m][n][r];
+        }
+        __syncthreads();
+        if (wk > 0) return;
+#pragma unroll
+        for (int k = 1; k < C::NWK; ++k) {
+            const float *src = park_area + ((k - 1) * C::NWC * C::NWP + wcp) * per_wave + lane;
+#pragma unroll
+            for (int m = 0; m < C::MA; ++m)
+#pragma unroll
+                for (int n = 0; n < C::NB; ++n)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) acc[m][n][r] += src[((m * C::NB + n) * 4 + r) * 64];
+        }
+#pragma unroll
+        for (int m = 0; m < C::MA; ++m)
+#pragma unroll
+            for (int n = 0; n < C::NB; ++n) ep.store(m, n, acc[m][n]);
+    }
+}
+
 template <class C>
 __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x, const float *__restrict__ w,
                                                     const float *__restrict__ bias, float *__restrict__ out,
@@ -328,6 +467,17 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
 #pragma unroll
         for (int n = 0; n < C::NB; ++n) acc[m][n] = floatx4{0.f, 0.f, 0.f, 0.f};
 
+    // Output side, set up before the last stage so that its stores can stream
+    // out while the last blocks are still being computed.  Accumulator block
+    // (m, n), register r holds output channel co0 + wc*16*MA + 16*m + 4*g + r
+    // at tile pixel (wp*NB + n)*16 + l16.  Split workgroups write slice
+    // `split` of the partial sums, in the output's layout, without the bias.
+    // Stores go through a buffer descriptor: a lane outside the output (pixel
+    // or channel) gets an offset of at least 2^30 bytes, past the descriptor's
+    // range (< 2^30, checked when the plan is made), and its store is dropped.
+    Epilogue<C> ep;
+    ep.init(a, out, part, bias, split, co0 + wc * 16 * C::MA + 4 * g, wp, l16, oh0, ow0);
+
     int xo[C::XPT];
     halo_offsets<C>(xo, a, wave, lane, ih0, iw0);
     AStage<C> a0, a1;
@@ -335,81 +485,23 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
     load_a<C>(a0, rw, a, a_off, ci_lane, c_begin * C::CC);
     stage_ready();
 
-    for (int ch = c_begin; ch < c_end; ch += 2) {
-        if (ch + 1 < c_end) {
-            dma_halo<C>(lds1, x, a, (ch + 1) * C::CC, wave, xo);
-            load_a<C>(a1, rw, a, a_off, ci_lane, (ch + 1) * C::CC);
+    for (int ch = c_begin;; ch += 2) {
+        if (ch + 1 >= c_end) {
+            final_stage<C>(lds0, a0, b_base, acc, lds0, wave, wk, lane, ep);
+            break;
         }
+        dma_halo<C>(lds1, x, a, (ch + 1) * C::CC, wave, xo);
+        load_a<C>(a1, rw, a, a_off, ci_lane, (ch + 1) * C::CC);
         compute_stage<C>(lds0, a0, b_base, acc);
         stage_ready();
-        if (ch + 1 >= c_end) break;
-        if (ch + 2 < c_end) {
-            dma_halo<C>(lds0, x, a, (ch + 2) * C::CC, wave, xo);
-            load_a<C>(a0, rw, a, a_off, ci_lane, (ch + 2) * C::CC);
+        if (ch + 2 >= c_end) {
+            final_stage<C>(lds1, a1, b_base, acc, lds0, wave, wk, lane, ep);
+            break;
         }
+        dma_halo<C>(lds0, x, a, (ch + 2) * C::CC, wave, xo);
+        load_a<C>(a0, rw, a, a_off, ci_lane, (ch + 2) * C::CC);
         compute_stage<C>(lds1, a1, b_base, acc);
         stage_ready();
-    }
-
-    // Sum the NWK channel-group partials: waves wk > 0 park theirs in LDS
-    // (the stage buffers are free after the last barrier), waves wk = 0 add.
-    if constexpr (C::NWK > 1) {
-        constexpr int per_wave = C::MA * C::NB * 4 * 64;
-        const int wcp = wave % (C::NWC * C::NWP);
-        if (wk > 0) {
-            float *park = lds0 + ((wk - 1) * C::NWC * C::NWP + wcp) * per_wave + lane;
-#pragma unroll
-            for (int m = 0; m < C::MA; ++m)
-#pragma unroll
-                for (int n = 0; n < C::NB; ++n)
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) park[((m * C::NB + n) * 4 + r) * 64] = acc[m][n][r];
-        }
-        __syncthreads();
-        if (wk > 0) return;
-#pragma unroll
-        for (int k = 1; k < C::NWK; ++k) {
-            const float *src = lds0 + ((k - 1) * C::NWC * C::NWP + wcp) * per_wave + lane;
-#pragma unroll
-            for (int m = 0; m < C::MA; ++m)
-#pragma unroll
-                for (int n = 0; n < C::NB; ++n)
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) acc[m][n][r] += src[((m * C::NB + n) * 4 + r) * 64];
-        }
-    }
-
-    // Accumulator block (m, n), register r holds output channel
-    // co0 + wc*16*MA + m*16 + 4*g + r at tile pixel (wp*NB + n)*16 + l16.
-    // Split workgroups write slice `split` of the partial sums, in the
-    // output's layout, without the bias.  Stores go through a buffer
-    // descriptor: a lane outside the output (pixel or channel) gets an offset
-    // of at least 2^30 bytes, past the descriptor's range (< 2^30, checked
-    // when the plan is made), and its store is dropped.
-    const unsigned plane_b = (unsigned)a.h_out * a.w_out * 4u;
-    const unsigned out_b = (unsigned)a.c_out * plane_b;
-    const __amdgpu_buffer_rsrc_t ro = make_rsrc(a.splits == 1 ? out : part + (size_t)split * (out_b / 4), out_b);
-    constexpr unsigned kFar = 1u << 30;
-    unsigned pix_off[C::NB];
-#pragma unroll
-    for (int n = 0; n < C::NB; ++n) {
-        const int p = (wp * C::NB + n) * 16 + l16;
-        const int oh = oh0 + p / C::TW, ow = ow0 + p % C::TW;
-        pix_off[n] = (p < C::NPIX && oh < a.h_out && ow < a.w_out) ? (unsigned)(oh * a.w_out + ow) * 4u : kFar;
-    }
-#pragma unroll
-    for (int m = 0; m < C::MA; ++m) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int co = co0 + wc * 16 * C::MA + m * 16 + 4 * g + r;
-            const bool co_ok = co < a.c_out;
-            const float b = (a.splits == 1 && bias && co_ok) ? bias[co] : 0.f;
-            const unsigned chan_off = co_ok ? (unsigned)co * plane_b : kFar;
-#pragma unroll
-            for (int n = 0; n < C::NB; ++n)
-                __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, acc[m][n][r] + b), ro,
-                                                      (int)(chan_off + pix_off[n]), 0, 0);
-        }
     }
 }
 
