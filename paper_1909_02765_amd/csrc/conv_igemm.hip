@@ -206,6 +206,82 @@ __device__ __forceinline__ void dma_halo(float *buf, const float *__restrict__ x
     }
 }
 
+// The loads of the next stage -- its halo DMA and its weight registers --
+// as a list of single instructions that compute_stage issues a few at a time
+// between its matrix instructions.  Issued in one burst at the start of a
+// stage, they fill the memory pipeline's queue and the wave stalls at issue
+// with its matrix pipe idle; spread over the first half of the stage they
+// drain as they go and still have the second half to land.  Item i < ND is
+// DMA instruction i of this wave; the rest are the weight loads, one 16-byte
+// (or, for the tail of a tap run, 4-byte) piece each.
+template <class C>
+struct NextStage {
+    static constexpr int kPieces = C::KK / 4 + C::KK % 4;
+    static constexpr int kFull = C::NIX / C::NW;
+    static constexpr int ND = C::XPT;
+    static constexpr int N = ND + C::G4 * C::MA * kPieces;
+
+    __amdgpu_buffer_rsrc_t rx, rw;
+    float *buf;
+    AStage<C> *A;
+    const int *xo;
+    int wave;
+    unsigned a_base[C::G4][C::MA];
+
+    __device__ __forceinline__ NextStage(float *buf_, AStage<C> &A_, const float *__restrict__ x,
+                                         __amdgpu_buffer_rsrc_t rw_, const IgArgs &a, const int (&a_off)[C::MA],
+                                         int ci_lane, int ci0, int wave_, const int (&xo_)[C::XPT])
+        : rw(rw_), buf(buf_), A(&A_), xo(xo_), wave(wave_)
+    {
+        const unsigned plane = (unsigned)a.h * (unsigned)a.w;
+        rx = make_rsrc(x + (size_t)ci0 * plane, (unsigned)(a.c_in - ci0) * plane * 4u);
+#pragma unroll
+        for (int c4 = 0; c4 < C::G4; ++c4) {
+            const int ci = ci0 + ci_lane + 4 * C::NWK * c4;
+            const bool ok = ci < a.c_in;
+#pragma unroll
+            for (int m = 0; m < C::MA; ++m)
+                a_base[c4][m] = (ok && a_off[m] != kOutOfRange) ? (unsigned)(a_off[m] + ci * C::KK * 4)
+                                                                 : (unsigned)kOutOfRange;
+        }
+    }
+
+    __device__ __forceinline__ void issue(int i)
+    {
+        if (i < ND) {
+            if (i < kFull) {
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_ptr_t)(buf + (i * C::NW + wave) * 64), 4, xo[i], 0,
+                                                         0, 0);
+            } else if (kFull * C::NW + wave < C::NIX) {
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_ptr_t)(buf + (kFull * C::NW + wave) * 64), 4,
+                                                         xo[kFull], 0, 0, 0);
+            }
+            return;
+        }
+        const int q = i - ND;
+        const int c4 = q / (C::MA * kPieces), m = (q / kPieces) % C::MA, piece = q % kPieces;
+        const unsigned base = a_base[c4][m];
+        float *dst = A->v[m][c4];
+        if (piece < C::KK / 4) {
+            const floatx4 v = __builtin_bit_cast(
+                floatx4, __builtin_amdgcn_raw_buffer_load_b128(rw, (int)(base + 16u * piece), 0, 0));
+            dst[4 * piece] = v[0];
+            dst[4 * piece + 1] = v[1];
+            dst[4 * piece + 2] = v[2];
+            dst[4 * piece + 3] = v[3];
+        } else {
+            const int e = C::KK / 4 * 4 + (piece - C::KK / 4);
+            dst[e] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rw, (int)(base + 4u * e), 0, 0));
+        }
+    }
+};
+
+// No next stage (the last one).
+struct NoNextStage {
+    static constexpr int N = 0;
+    __device__ __forceinline__ void issue(int) {}
+};
+
 // Every load in flight (this wave's DMA and weight registers) has landed, and
 // then every wave's.  The wait is the builtin (vmcnt = 0, expcnt and lgkmcnt
 // left at their maxima) rather than inline assembly so that the compiler
@@ -233,11 +309,14 @@ __device__ __forceinline__ void read_b(const float *xl, const int (&b_base)[C::N
 // sinking them -- a wave issues in order, so reads placed behind a run of
 // MFMAs would only start once the whole run had issued, leaving the matrix
 // pipe to wait on them.
-template <class C>
+template <class C, class P>
 __device__ __forceinline__ void compute_stage(const float *xl, const AStage<C> &A, const int (&b_base)[C::NB],
-                                              floatx4 (&acc)[C::MA][C::NB])
+                                              floatx4 (&acc)[C::MA][C::NB], P &next)
 {
     constexpr int kSteps = C::KK * C::G4;
+    // Next-stage loads per step: all of them within the first half.
+    constexpr int kHalf = kSteps / 2 > 0 ? kSteps / 2 : 1;
+    constexpr int kRate = P::N == 0 ? 1 : (P::N + kHalf - 1) / kHalf;
     float bv[2][C::NB];
     read_b<C>(xl, b_base, 0, bv[0]);
     __builtin_amdgcn_sched_barrier(0);
@@ -245,6 +324,9 @@ __device__ __forceinline__ void compute_stage(const float *xl, const AStage<C> &
     for (int st = 0; st < kSteps; ++st) {
         const int cur = st & 1;
         const int t = st / C::G4, c4 = st % C::G4;
+#pragma unroll
+        for (int r = 0; r < kRate; ++r)
+            if (st * kRate + r < P::N) next.issue(st * kRate + r);
         if (st + 1 < kSteps) read_b<C>(xl, b_base, st + 1, bv[cur ^ 1]);
 #pragma unroll
         for (int m = 0; m < C::MA; ++m)
@@ -369,7 +451,8 @@ __device__ __forceinline__ void final_stage(const float *xl, const AStage<C> &A,
     if constexpr (C::NWK == 1) {
         compute_stage_streamed<C>(xl, A, b_base, acc, ep);
     } else {
-        compute_stage<C>(xl, A, b_base, acc);
+        NoNextStage none;
+        compute_stage<C>(xl, A, b_base, acc, none);
         __syncthreads();
         constexpr int per_wave = C::MA * C::NB * 4 * 64;
         const int wcp = wave % (C::NWC * C::NWP);
@@ -490,32 +573,72 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
             final_stage<C>(lds0, a0, b_base, acc, lds0, wave, wk, lane, ep);
             break;
         }
-        dma_halo<C>(lds1, x, a, (ch + 1) * C::CC, wave, xo);
-        load_a<C>(a1, rw, a, a_off, ci_lane, (ch + 1) * C::CC);
-        compute_stage<C>(lds0, a0, b_base, acc);
+        {
+            NextStage<C> next(lds1, a1, x, rw, a, a_off, ci_lane, (ch + 1) * C::CC, wave, xo);
+            compute_stage<C>(lds0, a0, b_base, acc, next);
+        }
         stage_ready();
         if (ch + 2 >= c_end) {
             final_stage<C>(lds1, a1, b_base, acc, lds0, wave, wk, lane, ep);
             break;
         }
-        dma_halo<C>(lds0, x, a, (ch + 2) * C::CC, wave, xo);
-        load_a<C>(a0, rw, a, a_off, ci_lane, (ch + 2) * C::CC);
-        compute_stage<C>(lds1, a1, b_base, acc);
+        {
+            NextStage<C> next(lds0, a0, x, rw, a, a_off, ci_lane, (ch + 2) * C::CC, wave, xo);
+            compute_stage<C>(lds1, a1, b_base, acc, next);
+        }
         stage_ready();
     }
 }
 
 // out[i] = part[0][i] + part[1][i] + ... + part[splits-1][i] + bias[channel(i)],
-// summed in that order.
-__global__ __launch_bounds__(256) void sum_splits(const float *__restrict__ part, const float *__restrict__ bias,
+// summed in that order.  Each thread owns V consecutive outputs (V = 4 when
+// every split slice is 16-byte aligned) and issues the loads of up to kBatch
+// slices before it adds any of them, so the latency of the partial sums (just
+// written by the conv kernel, mostly still in the last-level cache) is paid
+// once per batch rather than once per slice.
+template <int V>
+struct VecF;
+template <>
+struct VecF<1> {
+    using T = float;
+};
+template <>
+struct VecF<4> {
+    using T = float4;
+};
+
+template <int V>
+__global__ __launch_bounds__(128) void sum_splits(const float *__restrict__ part, const float *__restrict__ bias,
                                                   float *__restrict__ out, int splits, int plane, int64_t total)
 {
-    int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    const int64_t step = (int64_t)gridDim.x * 256;
-    for (; i < total; i += step) {
-        float s = part[i];
-        for (int k = 1; k < splits; ++k) s += part[(size_t)k * total + i];
-        out[i] = s + (bias ? bias[i / plane] : 0.f);
+    using T = typename VecF<V>::T;
+    constexpr int kBatch = 16;
+    const int64_t nvec = total / V;
+    const T *pv = reinterpret_cast<const T *>(part);
+    const int64_t step = (int64_t)gridDim.x * 128;
+    for (int64_t i = (int64_t)blockIdx.x * 128 + threadIdx.x; i < nvec; i += step) {
+        T s = pv[i];
+        int k = 1;
+        for (; k + kBatch <= splits; k += kBatch) {
+            T v[kBatch];
+#pragma unroll
+            for (int j = 0; j < kBatch; ++j) v[j] = pv[(size_t)(k + j) * nvec + i];
+#pragma unroll
+            for (int j = 0; j < kBatch; ++j) s += v[j];
+        }
+        {
+            T v[kBatch];
+#pragma unroll
+            for (int j = 0; j < kBatch; ++j)
+                if (k + j < splits) v[j] = pv[(size_t)(k + j) * nvec + i];
+#pragma unroll
+            for (int j = 0; j < kBatch; ++j)
+                if (k + j < splits) s += v[j];
+        }
+        float *o = out + i * V;
+        const float *sv = reinterpret_cast<const float *>(&s);
+#pragma unroll
+        for (int e = 0; e < V; ++e) o[e] = sv[e] + (bias ? bias[(i * V + e) / plane] : 0.f);
     }
 }
 
@@ -672,10 +795,16 @@ hipError_t igemm_launch(const ilpm_plan &p, const ConvShape &s, const float *x, 
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || p.splits == 1) return e;
     const int64_t total = (int64_t)s.c_out * s.h_out * s.w_out;
-    int64_t blocks = (total + 255) / 256;
-    if (blocks > 4096) blocks = 4096;
-    hipLaunchKernelGGL(sum_splits, dim3((unsigned)blocks), dim3(256), 0, stream, part, bias, out, p.splits,
-                       s.h_out * s.w_out, total);
+    const bool vec4 = total % 4 == 0;
+    const int64_t threads = vec4 ? total / 4 : total;
+    int64_t blocks = (threads + 127) / 128;
+    if (blocks > 8192) blocks = 8192;
+    if (vec4)
+        hipLaunchKernelGGL(sum_splits<4>, dim3((unsigned)blocks), dim3(128), 0, stream, part, bias, out, p.splits,
+                           s.h_out * s.w_out, total);
+    else
+        hipLaunchKernelGGL(sum_splits<1>, dim3((unsigned)blocks), dim3(128), 0, stream, part, bias, out, p.splits,
+                           s.h_out * s.w_out, total);
     return hipGetLastError();
 }
 
