@@ -81,6 +81,15 @@ struct Cfg {
     static constexpr int HCP = halo_row(HR, HC, S);
     static constexpr int PL = HR * HCP;
     static constexpr int COT = NWC * 16 * MA;
+    // A tile of 16*q + t pixels, t in 1..4, computes its last pixel block with
+    // the 4x4x1 matrix instruction (16 blocks of 4 channels x 4 pixels, one k
+    // each), a quarter of the 16x16x4 one's cycles: block b = 4*kq + cg of
+    // lane l = 16*kq + 4*cg + j takes channels 4*cg..4*cg+3 of the 16, k-slice
+    // kq of the step's 4 and pixel j -- the same A register as the 16x16x4
+    // layout -- and the four k-slice partials are summed across lane groups
+    // at the end.
+    static constexpr int TAILP = NPIX % 16;
+    static constexpr bool TAIL4 = NWP == 1 && TAILP >= 1 && TAILP <= 4;
     static constexpr int G4 = CC / 4 / NWK;  // channel groups per wave per stage
     // One stage buffer: the halo, a whole number of 64-word rows (one DMA
     // instruction each).
@@ -292,6 +301,14 @@ __device__ __forceinline__ void stage_ready()
     __syncthreads();
 }
 
+// One matrix instruction on accumulator block n.
+template <class C>
+__device__ __forceinline__ floatx4 mfma_block(int n, float a, float b, const floatx4 &c)
+{
+    if (C::TAIL4 && n == C::NB - 1) return __builtin_amdgcn_mfma_f32_4x4x1f32(a, b, c, 0, 0, 0);
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
 // B fragments (input patches) of step st for one wave.
 template <class C>
 __device__ __forceinline__ void read_b(const float *xl, const int (&b_base)[C::NB], int st, float (&bv)[C::NB])
@@ -332,7 +349,7 @@ __device__ __forceinline__ void compute_stage(const float *xl, const AStage<C> &
         for (int m = 0; m < C::MA; ++m)
 #pragma unroll
             for (int n = 0; n < C::NB; ++n)
-                acc[m][n] = __builtin_amdgcn_mfma_f32_16x16x4f32(A.v[m][c4][t], bv[cur][n], acc[m][n], 0, 0, 0);
+                acc[m][n] = mfma_block<C>(n, A.v[m][c4][t], bv[cur][n], acc[m][n]);
         // Within the step: one matrix instruction, then one read of the next
         // step, so the reads issue while the matrix pipe is busy.
 #pragma unroll
@@ -351,12 +368,18 @@ struct Epilogue {
     unsigned pix_off[C::NB];   // byte offset of each pixel block's lane pixel
     unsigned chan_off[C::MA][4];
     float b[C::MA][4];
+    // The 4x4x1 tail block (TAIL4): after the k-slice sum, lane 4*cg + j of
+    // the first 16 stores channels tail_co + 16*m + r, r = 0..3, at pixel j.
+    int tail_co, c_out;
+    unsigned tail_pix, plane_b;
+    float tail_b[C::MA][4];
 
     __device__ __forceinline__ void init(const IgArgs &a, float *out, float *part, const float *bias, int split,
-                                         int co_lane, int wp, int l16, int oh0, int ow0)
+                                         int co_lane, int wp, int g, int l16, int oh0, int ow0)
     {
         constexpr unsigned kFar = 1u << 30;
-        const unsigned plane_b = (unsigned)a.h_out * a.w_out * 4u;
+        plane_b = (unsigned)a.h_out * a.w_out * 4u;
+        c_out = a.c_out;
         const unsigned out_b = (unsigned)a.c_out * plane_b;
         ro = make_rsrc(a.splits == 1 ? out : part + (size_t)split * (out_b / 4), out_b);
 #pragma unroll
@@ -374,10 +397,41 @@ struct Epilogue {
                 b[m][r] = (a.splits == 1 && bias && ok) ? bias[co] : 0.f;
                 chan_off[m][r] = ok ? (unsigned)co * plane_b : kFar;
             }
+        if constexpr (C::TAIL4) {
+            // co_lane = co_base + 4*g; the tail uses co_base + 4*cg, cg = l16/4.
+            tail_co = co_lane - 4 * g + 4 * (l16 >> 2);
+            const int j = l16 & 3;
+            const int p = (C::NB - 1) * 16 + j;
+            const int oh = oh0 + p / C::TW, ow = ow0 + p % C::TW;
+            const bool lane_stores = g == 0 && j < C::TAILP && oh < a.h_out && ow < a.w_out;
+            tail_pix = lane_stores ? (unsigned)(oh * a.w_out + ow) * 4u : kFar;
+#pragma unroll
+            for (int m = 0; m < C::MA; ++m)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int co = tail_co + 16 * m + r;
+                    tail_b[m][r] = (a.splits == 1 && bias && co < a.c_out) ? bias[co] : 0.f;
+                }
+        }
     }
 
     __device__ __forceinline__ void store(int m, int n, const floatx4 &v) const
     {
+        if (C::TAIL4 && n == C::NB - 1) {
+            // Sum the four k-slice partials: lane l gets (v[l] + v[l^16]) +
+            // (v[l^32] + v[l^48]) for the first 16 lanes.
+            constexpr unsigned kFar = 1u << 30;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                float s = v[r] + __shfl_xor(v[r], 16);
+                s += __shfl_xor(s, 32);
+                const int co = tail_co + 16 * m + r;
+                const unsigned off = (co < c_out && tail_pix < kFar) ? (unsigned)co * plane_b + tail_pix : kFar;
+                __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, s + tail_b[m][r]), ro, (int)off,
+                                                      0, 0);
+            }
+            return;
+        }
 #pragma unroll
         for (int r = 0; r < 4; ++r)
             __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v[r] + b[m][r]), ro,
@@ -425,7 +479,7 @@ __device__ __forceinline__ void compute_stage_streamed(const float *xl, const AS
                 for (int j = 0; j < GB; ++j) {
                     const int n = grp * GB + j;
                     if (n < C::NB)
-                        acc[m][n] = __builtin_amdgcn_mfma_f32_16x16x4f32(A.v[m][c4][t], bv[cur][j], acc[m][n], 0, 0, 0);
+                        acc[m][n] = mfma_block<C>(n, A.v[m][c4][t], bv[cur][j], acc[m][n]);
                 }
             __builtin_amdgcn_sched_barrier(0);
             cur ^= 1;
@@ -539,7 +593,7 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
     int b_base[C::NB];
 #pragma unroll
     for (int nb = 0; nb < C::NB; ++nb) {
-        int p = (wp * C::NB + nb) * 16 + l16;
+        int p = (wp * C::NB + nb) * 16 + ((C::TAIL4 && nb == C::NB - 1) ? (l16 & 3) : l16);
         if (p >= C::NPIX) p = 0;  // padding lanes read a valid word; never stored
         b_base[nb] = ci_lane * C::PL + (p / C::TW) * C::S * C::HCP + (p % C::TW) * C::S;
     }
@@ -553,13 +607,14 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
     // Output side, set up before the last stage so that its stores can stream
     // out while the last blocks are still being computed.  Accumulator block
     // (m, n), register r holds output channel co0 + wc*16*MA + 16*m + 4*g + r
-    // at tile pixel (wp*NB + n)*16 + l16.  Split workgroups write slice
+    // at tile pixel (wp*NB + n)*16 + l16 (the 4x4x1 tail block is laid out
+    // as its Cfg comment says).  Split workgroups write slice
     // `split` of the partial sums, in the output's layout, without the bias.
     // Stores go through a buffer descriptor: a lane outside the output (pixel
     // or channel) gets an offset of at least 2^30 bytes, past the descriptor's
     // range (< 2^30, checked when the plan is made), and its store is dropped.
     Epilogue<C> ep;
-    ep.init(a, out, part, bias, split, co0 + wc * 16 * C::MA + 4 * g, wp, l16, oh0, ow0);
+    ep.init(a, out, part, bias, split, co0 + wc * 16 * C::MA + 4 * g, wp, g, l16, oh0, ow0);
 
     int xo[C::XPT];
     halo_offsets<C>(xo, a, wave, lane, ih0, iw0);
