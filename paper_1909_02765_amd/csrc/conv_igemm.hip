@@ -90,6 +90,13 @@ struct Cfg {
     // at the end.
     static constexpr int TAILP = NPIX % 16;
     static constexpr bool TAIL4 = NWP == 1 && TAILP >= 1 && TAILP <= 4;
+    // A 4x4x1 instruction placed between 16x16x4 ones occupies the matrix
+    // pipe as long as a 16x16x4; back to back they issue about every 9.5
+    // cycles.  So a stage's tail instructions run as one burst after its
+    // 16x16x4 work, spread over four accumulators (acc[m][NB-1+j], j < 4,
+    // folded into acc[m][NB-1] at the end) to keep them independent.
+    static constexpr int NBM = TAIL4 ? NB - 1 : NB;  // 16x16x4 blocks
+    static constexpr int NACC = TAIL4 ? NB + 3 : NB;
     static constexpr int G4 = CC / 4 / NWK;  // channel groups per wave per stage
     // One stage buffer: the halo, a whole number of 64-word rows (one DMA
     // instruction each).
@@ -301,14 +308,6 @@ __device__ __forceinline__ void stage_ready()
     __syncthreads();
 }
 
-// One matrix instruction on accumulator block n.
-template <class C>
-__device__ __forceinline__ floatx4 mfma_block(int n, float a, float b, const floatx4 &c)
-{
-    if (C::TAIL4 && n == C::NB - 1) return __builtin_amdgcn_mfma_f32_4x4x1f32(a, b, c, 0, 0, 0);
-    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
-}
-
 // B fragments (input patches) of step st for one wave.
 template <class C>
 __device__ __forceinline__ void read_b(const float *xl, const int (&b_base)[C::NB], int st, float (&bv)[C::NB])
@@ -328,13 +327,14 @@ __device__ __forceinline__ void read_b(const float *xl, const int (&b_base)[C::N
 // pipe to wait on them.
 template <class C, class P>
 __device__ __forceinline__ void compute_stage(const float *xl, const AStage<C> &A, const int (&b_base)[C::NB],
-                                              floatx4 (&acc)[C::MA][C::NB], P &next)
+                                              floatx4 (&acc)[C::MA][C::NACC], P &next)
 {
     constexpr int kSteps = C::KK * C::G4;
     // Next-stage loads per step: all of them within the first half.
     constexpr int kHalf = kSteps / 2 > 0 ? kSteps / 2 : 1;
     constexpr int kRate = P::N == 0 ? 1 : (P::N + kHalf - 1) / kHalf;
     float bv[2][C::NB];
+    float tb[C::TAIL4 ? kSteps : 1];
     read_b<C>(xl, b_base, 0, bv[0]);
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
@@ -348,16 +348,41 @@ __device__ __forceinline__ void compute_stage(const float *xl, const AStage<C> &
 #pragma unroll
         for (int m = 0; m < C::MA; ++m)
 #pragma unroll
-            for (int n = 0; n < C::NB; ++n)
-                acc[m][n] = mfma_block<C>(n, A.v[m][c4][t], bv[cur][n], acc[m][n]);
+            for (int n = 0; n < C::NBM; ++n)
+                acc[m][n] = __builtin_amdgcn_mfma_f32_16x16x4f32(A.v[m][c4][t], bv[cur][n], acc[m][n], 0, 0, 0);
+        if constexpr (C::TAIL4) tb[st] = bv[cur][C::NB - 1];
         // Within the step: one matrix instruction, then one read of the next
         // step, so the reads issue while the matrix pipe is busy.
+        constexpr int kMf = C::MA * C::NBM;
+        const int n_ds = st + 1 < kSteps ? C::NB : 0;
 #pragma unroll
-        for (int i = 0; i < C::MA * C::NB; ++i) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        for (int i = 0; i < (kMf > C::NB ? kMf : C::NB); ++i) {
+            if (i < kMf) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            if (i < n_ds) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
         }
         __builtin_amdgcn_sched_barrier(0);
+    }
+    if constexpr (C::TAIL4) {
+#pragma unroll
+        for (int st = 0; st < kSteps; ++st) {
+            const int t = st / C::G4, c4 = st % C::G4;
+#pragma unroll
+            for (int m = 0; m < C::MA; ++m)
+                acc[m][C::NB - 1 + st % 4] =
+                    __builtin_amdgcn_mfma_f32_4x4x1f32(A.v[m][c4][t], tb[st], acc[m][C::NB - 1 + st % 4], 0, 0, 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    }
+}
+
+// acc[m][NB-1] = the sum of the four tail accumulators, in a fixed order.
+template <class C>
+__device__ __forceinline__ void fold_tail(floatx4 (&acc)[C::MA][C::NACC])
+{
+    if constexpr (C::TAIL4) {
+#pragma unroll
+        for (int m = 0; m < C::MA; ++m)
+            acc[m][C::NB - 1] = (acc[m][C::NB - 1] + acc[m][C::NB]) + (acc[m][C::NB + 1] + acc[m][C::NB + 2]);
     }
 }
 
@@ -444,23 +469,31 @@ struct Epilogue {
 // next group, so that each finished group's stores are issued while the
 // following groups still compute (the output write then overlaps the matrix
 // work instead of following it).  Four blocks per group keep four
-// independent accumulator chains in flight.
+// independent accumulator chains in flight; the 4x4x1 tail block, if any,
+// is the last group, on its four accumulators.
 template <class C>
 __device__ __forceinline__ void compute_stage_streamed(const float *xl, const AStage<C> &A,
-                                                       const int (&b_base)[C::NB], floatx4 (&acc)[C::MA][C::NB],
+                                                       const int (&b_base)[C::NB], floatx4 (&acc)[C::MA][C::NACC],
                                                        const Epilogue<C> &ep)
 {
     constexpr int kSteps = C::KK * C::G4;
     constexpr int GB = 4;
-    constexpr int kGroups = (C::NB + GB - 1) / GB;
+    constexpr int kGroups = (C::NBM + GB - 1) / GB + (C::TAIL4 ? 1 : 0);
     float bv[2][GB];
+    // Group grp covers blocks [grp*GB, min(grp*GB + GB, NBM)); the tail group
+    // (grp*GB >= NBM) covers block NB-1 alone.
     auto read = [&](int grp, int st, float(&dst)[GB]) {
         const int t = st / C::G4, c4 = st % C::G4;
         const int kh = t / C::KS, kw = t % C::KS;
+        const int off = 4 * C::NWK * c4 * C::PL + kh * C::HCP + kw;
+        if (grp * GB >= C::NBM) {
+            dst[0] = xl[b_base[C::NB - 1] + off];
+            return;
+        }
 #pragma unroll
         for (int j = 0; j < GB; ++j) {
             const int n = grp * GB + j;
-            if (n < C::NB) dst[j] = xl[b_base[n] + 4 * C::NWK * c4 * C::PL + kh * C::HCP + kw];
+            if (n < C::NBM) dst[j] = xl[b_base[n] + off];
         }
     };
     read(0, 0, bv[0]);
@@ -468,29 +501,43 @@ __device__ __forceinline__ void compute_stage_streamed(const float *xl, const AS
     int cur = 0;
 #pragma unroll
     for (int grp = 0; grp < kGroups; ++grp) {
+        const bool tail = grp * GB >= C::NBM;
 #pragma unroll
         for (int st = 0; st < kSteps; ++st) {
             const int t = st / C::G4, c4 = st % C::G4;
             if (st + 1 < kSteps) read(grp, st + 1, bv[cur ^ 1]);
             else if (grp + 1 < kGroups) read(grp + 1, 0, bv[cur ^ 1]);
 #pragma unroll
+            for (int m = 0; m < C::MA; ++m) {
+                if (tail) {
+                    acc[m][C::NB - 1 + st % 4] =
+                        __builtin_amdgcn_mfma_f32_4x4x1f32(A.v[m][c4][t], bv[cur][0], acc[m][C::NB - 1 + st % 4], 0, 0, 0);
+                } else {
+#pragma unroll
+                    for (int j = 0; j < GB; ++j) {
+                        const int n = grp * GB + j;
+                        if (n < C::NBM)
+                            acc[m][n] = __builtin_amdgcn_mfma_f32_16x16x4f32(A.v[m][c4][t], bv[cur][j], acc[m][n], 0,
+                                                                             0, 0);
+                    }
+                }
+            }
+            __builtin_amdgcn_sched_barrier(0);
+            cur ^= 1;
+        }
+        if (tail) {
+            fold_tail<C>(acc);
+#pragma unroll
+            for (int m = 0; m < C::MA; ++m) ep.store(m, C::NB - 1, acc[m][C::NB - 1]);
+        } else {
+#pragma unroll
             for (int m = 0; m < C::MA; ++m)
 #pragma unroll
                 for (int j = 0; j < GB; ++j) {
                     const int n = grp * GB + j;
-                    if (n < C::NB)
-                        acc[m][n] = mfma_block<C>(n, A.v[m][c4][t], bv[cur][j], acc[m][n]);
+                    if (n < C::NBM) ep.store(m, n, acc[m][n]);
                 }
-            __builtin_amdgcn_sched_barrier(0);
-            cur ^= 1;
         }
-#pragma unroll
-        for (int m = 0; m < C::MA; ++m)
-#pragma unroll
-            for (int j = 0; j < GB; ++j) {
-                const int n = grp * GB + j;
-                if (n < C::NB) ep.store(m, n, acc[m][n]);
-            }
     }
 }
 
@@ -499,7 +546,7 @@ __device__ __forceinline__ void compute_stage_streamed(const float *xl, const AS
 // every wave is past the last stage, waves wk = 0 add and store).
 template <class C>
 __device__ __forceinline__ void final_stage(const float *xl, const AStage<C> &A, const int (&b_base)[C::NB],
-                                            floatx4 (&acc)[C::MA][C::NB], float *park_area, int wave, int wk,
+                                            floatx4 (&acc)[C::MA][C::NACC], float *park_area, int wave, int wk,
                                             int lane, const Epilogue<C> &ep)
 {
     if constexpr (C::NWK == 1) {
@@ -507,6 +554,7 @@ __device__ __forceinline__ void final_stage(const float *xl, const AStage<C> &A,
     } else {
         NoNextStage none;
         compute_stage<C>(xl, A, b_base, acc, none);
+        fold_tail<C>(acc);
         __syncthreads();
         constexpr int per_wave = C::MA * C::NB * 4 * 64;
         const int wcp = wave % (C::NWC * C::NWP);
@@ -598,11 +646,11 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
         b_base[nb] = ci_lane * C::PL + (p / C::TW) * C::S * C::HCP + (p % C::TW) * C::S;
     }
 
-    floatx4 acc[C::MA][C::NB];
+    floatx4 acc[C::MA][C::NACC];
 #pragma unroll
     for (int m = 0; m < C::MA; ++m)
 #pragma unroll
-        for (int n = 0; n < C::NB; ++n) acc[m][n] = floatx4{0.f, 0.f, 0.f, 0.f};
+        for (int n = 0; n < C::NACC; ++n) acc[m][n] = floatx4{0.f, 0.f, 0.f, 0.f};
 
     // Output side, set up before the last stage so that its stores can stream
     // out while the last blocks are still being computed.  Accumulator block
