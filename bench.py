@@ -89,8 +89,40 @@ def time_layer(torch, ilpm, x, w, b, s, p, out, steps, warmup):
     return start.elapsed_time(stop) * 1000.0 / steps
 
 
+def time_layer_graph(torch, ilpm, x, w, b, s, p, out, steps, per_graph=20):
+    """Mean µs per call when the same calls are replayed from a captured HIP
+    graph of `per_graph` launches (no host launch cost between calls).  The
+    library allocates nothing during capture: the calls made before it have
+    already sized its workspace."""
+    stream = torch.cuda.Stream()
+    stream.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(stream):
+        launch = ilpm.conv2d_launcher(x, w, b, s, p, out)
+        for _ in range(3):
+            launch()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
+            for _ in range(per_graph):
+                launch()
+    torch.cuda.synchronize()
+    reps = max(1, steps // per_graph)
+    for _ in range(max(1, reps // 10)):
+        g.replay()
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(reps):
+        g.replay()
+    stop.record()
+    torch.cuda.synchronize()
+    return start.elapsed_time(stop) * 1000.0 / (reps * per_graph)
+
+
 def cpu_baseline(case, x, w, b, y_gpu):
-    """The CPU oracle timed on this host on the whole layer (a few repeats),
+    """The CPU oracle timed on this host on the whole layer (repeated for at
+    least 10 s),
     and the same run used as a parity spot check of the GPU output."""
     import numpy as np
     import oracle
@@ -100,7 +132,7 @@ def cpu_baseline(case, x, w, b, y_gpu):
                                 b is not None)
     reps, elapsed = 0, 0.0
     ref = sab = None
-    while elapsed < 5.0 and reps < 50:
+    while elapsed < 10.0 and reps < 200:
         t0 = time.perf_counter()
         ref, sab = oracle.conv2d_f64(x, w, b, case.stride, case.pad)
         elapsed += time.perf_counter() - t0
@@ -159,7 +191,7 @@ def measure_peaks(torch):
     return res
 
 
-def bench_case(torch, ilpm, case, steps, warmup):
+def bench_case(torch, ilpm, case, steps, warmup, graph=False):
     from workloads import to_device
     x, w, b = case.inputs()
     xd, wd, bd = to_device(torch, x), to_device(torch, w), to_device(torch, b)
@@ -168,7 +200,10 @@ def bench_case(torch, ilpm, case, steps, warmup):
                                        b is not None)
     out = torch.empty((1, case.c_out, ho, wo), device="cuda", dtype=torch.float32)
     us = time_layer(torch, ilpm, xd, wd, bd, case.stride, case.pad, out, steps, warmup)
-    return dict(x=x, w=w, b=b, out=out, plan=plan, flops=flops, nbytes=nbytes, us=us)
+    res = dict(x=x, w=w, b=b, out=out, plan=plan, flops=flops, nbytes=nbytes, us=us)
+    if graph:
+        res["graph_us"] = time_layer_graph(torch, ilpm, xd, wd, bd, case.stride, case.pad, out, steps)
+    return res
 
 
 def main():
@@ -203,7 +238,7 @@ def main():
         print(f"unknown workload {args.workload}", file=sys.stderr)
         sys.exit(2)
 
-    r = bench_case(torch, ilpm, case, args.steps, args.warmup)
+    r = bench_case(torch, ilpm, case, args.steps, args.warmup, graph=True)
     us = r["us"]
     gflops = r["flops"] / (us * 1e-6) / 1e9
     floor_us, bound = roofline_floor_us(r["flops"], r["nbytes"])
@@ -223,7 +258,8 @@ def main():
     line = {
         "metric": METRIC, "value": round(gflops, 2), "unit": "GFLOP/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(us / 1000.0, 6),
-        "us_per_layer": round(us, 3), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "us_per_layer": round(us, 3), "graph_replay_us_per_layer": round(r["graph_us"], 3),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "f32", "data": "synthetic (seeded SplitMix64 inputs, He-normal weights)",
         "config": {"workload": case.name, "input": [1, case.c_in, case.h, case.w],
                    "weights": [case.c_out, case.c_in, case.k, case.k], "stride": case.stride,
@@ -255,14 +291,14 @@ def main():
     if args.all:
         rows = []
         for c in workloads.SINGLE_LAYER_CASES:
-            rr = bench_case(torch, ilpm, c, max(50, args.steps // 4), 20)
+            rr = bench_case(torch, ilpm, c, max(200, args.steps // 4), 200, graph=True)
             fl, kind = roofline_floor_us(rr["flops"], rr["nbytes"])
-            rows.append({"layer": c.name, "us": round(rr["us"], 3),
+            rows.append({"layer": c.name, "us": round(rr["us"], 3), "graph_us": round(rr["graph_us"], 3),
                          "gflops": round(rr["flops"] / rr["us"] / 1e3, 1),
                          "floor_us": round(fl, 3), "bound": kind, "frac": round(fl / rr["us"], 4),
                          "plan": rr["plan"].as_dict()})
             print(json.dumps(rows[-1]), file=sys.stderr)
-        rows += bench_vgg16(torch, ilpm, workloads, max(50, args.steps // 10))
+        rows += bench_vgg16(torch, ilpm, workloads, max(200, args.steps // 10))
         if args.report:
             with open(args.report, "w") as f:
                 json.dump(rows, f, indent=1)
@@ -274,23 +310,26 @@ def bench_vgg16(torch, ilpm, workloads, steps):
     from workloads import to_device
     rows = []
     x = to_device(torch, workloads.vgg16_input())
-    total_us = total_floor = total_flops = 0.0
+    total_us = total_graph_us = total_floor = total_flops = 0.0
     for name, ci, co, hw, pool, seed in workloads.vgg16_layers():
         w = to_device(torch, workloads.vgg16_weights(ci, co, seed))
         out = torch.empty((1, co, hw, hw), device="cuda", dtype=torch.float32)
-        us = time_layer(torch, ilpm, x, w, None, 1, 1, out, steps, 10)
+        us = time_layer(torch, ilpm, x, w, None, 1, 1, out, steps, 200)
+        gus = time_layer_graph(torch, ilpm, x, w, None, 1, 1, out, steps)
         flops, nbytes, _, _ = layer_work(ci, hw, hw, co, 3, 1, 1, False)
         fl, kind = roofline_floor_us(flops, nbytes)
         plan = ilpm.plan(ci, hw, hw, co, 3, 1, 1)
-        rows.append({"layer": f"vgg16_{name}", "us": round(us, 3), "gflops": round(flops / us / 1e3, 1),
+        rows.append({"layer": f"vgg16_{name}", "us": round(us, 3), "graph_us": round(gus, 3),
+                     "gflops": round(flops / us / 1e3, 1),
                      "floor_us": round(fl, 3), "bound": kind, "frac": round(fl / us, 4), "plan": plan.as_dict()})
         print(json.dumps(rows[-1]), file=sys.stderr)
         total_us += us
+        total_graph_us += gus
         total_floor += fl
         total_flops += flops
         ilpm.relu_(out)
         x = ilpm.maxpool2x2(out) if pool else out
-    rows.append({"layer": "vgg16_total_conv", "us": round(total_us, 3),
+    rows.append({"layer": "vgg16_total_conv", "us": round(total_us, 3), "graph_us": round(total_graph_us, 3),
                  "gflops": round(total_flops / total_us / 1e3, 1), "floor_us": round(total_floor, 3),
                  "frac": round(total_floor / total_us, 4)})
     print(json.dumps(rows[-1]), file=sys.stderr)

@@ -6,7 +6,7 @@ import pytest
 
 import oracle
 import workloads
-from gpu_common import (assert_matches, note, random_case, run_conv, small_int_case, torch_cuda)
+from gpu_common import (assert_matches, dev, note, random_case, run_conv, small_int_case, torch_cuda)
 
 pytestmark = pytest.mark.gpu
 
@@ -138,8 +138,8 @@ def test_fuzz_matrix_core_ragged(ilpm):
 
 
 def test_split_reduction_repeats_bitwise(ilpm):
-    """A split plan run several times gives identical bits (fixed reduction
-    order, arrival counters returned to zero)."""
+    """A split plan run several times gives identical bits (the partial sums
+    are added in a fixed order)."""
     case = workloads.RESNET_CONV4
     x, w, b, ref, sab = case_data(case)
     p = ilpm.plan(case.c_in, case.h, case.w, case.c_out, case.k, case.stride, case.pad)
@@ -196,3 +196,36 @@ def test_bad_arguments_raise(ilpm):
     assert rc == ilpm.ERR_INVALID_ARG
     with pytest.raises(TypeError):
         ilpm.conv2d(x.double(), w, None)
+
+
+@pytest.mark.parametrize("case", [workloads.RESNET_CONV4, workloads.TINY], ids=lambda c: c.name)
+def test_graph_replay_matches_eager(ilpm, case):
+    """Calls captured in a HIP graph and replayed several times, with eager work
+    and a synchronisation between replays, reproduce the eager result bit for
+    bit (one plan with the split-sum kernel, one without)."""
+    torch = torch_cuda()
+    x, w, b, ref, sab = case_data(case)
+    xd, wd, bd = dev(x), dev(w), dev(b)
+    ho = ilpm.out_size(case.h, case.k, case.stride, case.pad)
+    wo = ilpm.out_size(case.w, case.k, case.stride, case.pad)
+    out = torch.empty((1, case.c_out, ho, wo), device="cuda", dtype=torch.float32)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    note(f"[graph] {case.name} capture")
+    with torch.cuda.stream(s):
+        launch = ilpm.conv2d_launcher(xd, wd, bd, case.stride, case.pad, out)
+        launch()
+        torch.cuda.synchronize()
+        eager = out.cpu().numpy().copy()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            launch()
+    torch.cuda.synchronize()
+    assert_matches(eager, ref, sab, case.c_in, case.k, "eager before capture")
+    for i in range(4):
+        note(f"[graph] {case.name} replay {i}")
+        out.fill_(float("nan"))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(out.cpu().numpy(), eager)
