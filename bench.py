@@ -7,8 +7,9 @@ pad 1), with every tensor already resident in HBM.  Prints ONE JSON line.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--all]
 
---all also times every other workload (and the VGG-16 conv stack layer by
-layer) and writes the table to --report (JSON) without changing the line.
+--all also times every other workload, the rest of ResNet's 3x3 layer set and
+VGG-16's first layer, then the VGG-16 conv stack layer by layer, and writes the
+table to --report (JSON) without changing the line.
 """
 from __future__ import annotations
 
@@ -290,7 +291,7 @@ def main():
 
     if args.all:
         rows = []
-        for c in workloads.SINGLE_LAYER_CASES:
+        for c in workloads.ALL_CASES:
             rr = bench_case(torch, ilpm, c, max(200, args.steps // 4), 200, graph=True)
             fl, kind = roofline_floor_us(rr["flops"], rr["nbytes"])
             rows.append({"layer": c.name, "us": round(rr["us"], 3), "graph_us": round(rr["graph_us"], 3),

@@ -27,7 +27,7 @@ def default_shapes():
     sys.path.insert(0, ROOT)
     import workloads
     shapes = [tuple(c.dims()[k] for k in ("c_in", "h", "w", "c_out", "k", "stride", "pad"))
-              for c in workloads.SINGLE_LAYER_CASES]
+              for c in workloads.ALL_CASES]
     for _, ci, co, hw, _, _ in workloads.vgg16_layers():
         shapes.append((ci, hw, hw, co, 3, 1, 1))
     # The 3x3 layers of ResNet (Table 2 of the paper): conv2.x .. conv5.x.

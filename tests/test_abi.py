@@ -97,7 +97,7 @@ def test_variants_table():
         ilpm.variant_info(ilpm.PATH_IGEMM, n)
 
 
-@pytest.mark.parametrize("case", workloads.SINGLE_LAYER_CASES, ids=lambda c: c.name)
+@pytest.mark.parametrize("case", workloads.ALL_CASES, ids=lambda c: c.name)
 def test_plan_for_every_workload(case):
     d = case.dims()
     p = ilpm.plan(d["c_in"], d["h"], d["w"], d["c_out"], d["k"], d["stride"], d["pad"])

@@ -10,7 +10,7 @@ from gpu_common import (assert_matches, dev, note, random_case, run_conv, small_
 
 pytestmark = pytest.mark.gpu
 
-CASES = workloads.SINGLE_LAYER_CASES
+CASES = workloads.ALL_CASES
 _ORACLE = {}
 
 

@@ -145,6 +145,23 @@ DEEP_5X5 = ConvCase("deep_5x5_512to512_7x7", 512, 7, 7, 512, 5, 1, 2, 4001, 4003
 
 SINGLE_LAYER_CASES = [TINY, VGG_EARLY, RESNET_CONV4, RESNET_STRIDED, DEEP_1X1, DEEP_5X5]
 
+# The other 3x3 layers of ResNet's Table 2 set (conv2.x, conv3.x, conv5.x; conv4.x is
+# RESNET_CONV4), batch 1, post-ReLU-like inputs and He-normal weights, no bias.
+RESNET_CONV2 = ConvCase("resnet_conv2_64to64_56x56", 64, 56, 56, 64, 3, 1, 1, 3201, 3202,
+                        ("uniform", 0.0, 1.0), _he(64, 3))
+RESNET_CONV3 = ConvCase("resnet_conv3_128to128_28x28", 128, 28, 28, 128, 3, 1, 1, 3301, 3302,
+                        ("uniform", 0.0, 1.0), _he(128, 3))
+RESNET_CONV5 = ConvCase("resnet_conv5_512to512_7x7", 512, 7, 7, 512, 3, 1, 1, 3501, 3502,
+                        ("uniform", 0.0, 1.0), _he(512, 3))
+RESNET_3X3_CASES = [RESNET_CONV2, RESNET_CONV3, RESNET_CONV4, RESNET_CONV5]
+
+# The first VGG-16 layer on its own (3 input channels: the memory-bound case).
+VGG16_CONV1_1 = ConvCase("vgg16_conv1_1_3to64_224x224", 3, 224, 224, 64, 3, 1, 1, 5001, 5100,
+                         ("uniform", 0.0, 1.0), _he(3, 3))
+
+EXTRA_CASES = [RESNET_CONV2, RESNET_CONV3, RESNET_CONV5, VGG16_CONV1_1]
+ALL_CASES = SINGLE_LAYER_CASES + EXTRA_CASES
+
 # Batch-1 VGG-16 conv stack: 13 3x3/pad-1/stride-1 convs, ReLU after each,
 # 2x2/stride-2 max-pool after stages 1-4 (none after stage 5).
 VGG16_STAGES = [[(3, 64), (64, 64)],
@@ -212,7 +229,7 @@ def to_device(torch, a):
 
 
 def case_by_name(name: str) -> Optional[ConvCase]:
-    for c in SINGLE_LAYER_CASES:
+    for c in ALL_CASES:
         if c.name == name:
             return c
     return None
