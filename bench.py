@@ -121,6 +121,25 @@ def time_layer_graph(torch, ilpm, x, w, b, s, p, out, steps, per_graph=20):
     return start.elapsed_time(stop) * 1000.0 / (reps * per_graph)
 
 
+def time_prepacked(torch, ilpm, x, w, b, s, p, out, plan, steps, warmup):
+    """Mean µs per call of the same plan on weights packed beforehand
+    (ilpm_conv2d_prepack_weights, once, outside the timed calls)."""
+    c_out, _, k, _ = w.shape
+    packed = ilpm.prepack_weights(w, plan)
+    launch = ilpm.conv2d_prepacked_launcher(x, packed, c_out, k, b, s, p, out, plan)
+    for _ in range(warmup):
+        launch()
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(steps):
+        launch()
+    stop.record()
+    torch.cuda.synchronize()
+    return start.elapsed_time(stop) * 1000.0 / steps
+
+
 def cpu_baseline(case, x, w, b, y_gpu):
     """The CPU oracle timed on this host on the whole layer (repeated for at
     least 10 s),
@@ -204,6 +223,8 @@ def bench_case(torch, ilpm, case, steps, warmup, graph=False):
     res = dict(x=x, w=w, b=b, out=out, plan=plan, flops=flops, nbytes=nbytes, us=us)
     if graph:
         res["graph_us"] = time_layer_graph(torch, ilpm, xd, wd, bd, case.stride, case.pad, out, steps)
+        res["prepacked_us"] = time_prepacked(torch, ilpm, xd, wd, bd, case.stride, case.pad, out, plan, steps,
+                                             warmup)
     return res
 
 
@@ -260,6 +281,7 @@ def main():
         "metric": METRIC, "value": round(gflops, 2), "unit": "GFLOP/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(us / 1000.0, 6),
         "us_per_layer": round(us, 3), "graph_replay_us_per_layer": round(r["graph_us"], 3),
+        "prepacked_weights_us_per_layer": round(r["prepacked_us"], 3),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "f32", "data": "synthetic (seeded SplitMix64 inputs, He-normal weights)",
         "config": {"workload": case.name, "input": [1, case.c_in, case.h, case.w],
@@ -295,6 +317,7 @@ def main():
             rr = bench_case(torch, ilpm, c, max(200, args.steps // 4), 200, graph=True)
             fl, kind = roofline_floor_us(rr["flops"], rr["nbytes"])
             rows.append({"layer": c.name, "us": round(rr["us"], 3), "graph_us": round(rr["graph_us"], 3),
+                         "prepacked_us": round(rr["prepacked_us"], 3),
                          "gflops": round(rr["flops"] / rr["us"] / 1e3, 1),
                          "floor_us": round(fl, 3), "bound": kind, "frac": round(fl / rr["us"], 4),
                          "plan": rr["plan"].as_dict()})

@@ -167,6 +167,47 @@ int ilpm_conv2d_fwd_plan(const float *in, const float *w, const float *bias,
                          int C_in, int H, int W, int C_out, int K, int stride, int pad,
                          float *out, const ilpm_plan *plan, hipStream_t stream);
 
+/* ---- prepacked weights ----
+ *
+ * The paper stores the filter re-laid out ([C][R][S][K], output channel
+ * innermost) so that the per-thread weight loads of its kernel coalesce
+ * (Section 4, Algorithm 2), and treats that as offline work.  Here the same
+ * idea targets the matrix-core kernels: ilpm_conv2d_prepack_weights writes a
+ * plan's weights in the order its kernel loads them, so every weight load
+ * instruction of a wave reads one contiguous kilobyte; weights are constant
+ * across calls, so a caller packs once and then runs
+ * ilpm_conv2d_fwd_prepacked.  The packed layout belongs to the plan's kernel
+ * variant (and C_in, C_out, K); it is not meant to be read by the caller.
+ * Channels are zero-padded to whole output-channel tiles and input-channel
+ * chunks.  For a direct-path plan the packed buffer is an OIHW copy.
+ */
+
+/*
+ * ilpm_conv2d_prepacked_size -- *bytes = size of the packed weights of
+ * `plan` for C_in, C_out, K.  Pure host.  ILPM_ERR_INVALID_ARG if the plan's
+ * variant does not take K, or an argument is out of range.
+ */
+int ilpm_conv2d_prepacked_size(const ilpm_plan *plan, int C_in, int C_out, int K, size_t *bytes);
+
+/*
+ * ilpm_conv2d_prepack_weights -- write w [C_out][C_in][K][K] (OIHW) into
+ * `packed` (ilpm_conv2d_prepacked_size bytes, caller-owned device memory)
+ * in the layout of `plan`.  w and packed: 16-byte aligned, not overlapping.
+ * Enqueued on `stream`.
+ */
+int ilpm_conv2d_prepack_weights(const float *w, int C_in, int C_out, int K, const ilpm_plan *plan,
+                                float *packed, hipStream_t stream);
+
+/*
+ * ilpm_conv2d_fwd_prepacked -- ilpm_conv2d_fwd_plan with the weights given
+ * as ilpm_conv2d_prepack_weights wrote them for the same plan, C_in, C_out
+ * and K (the plan must be for this exact shape, as for fwd_plan).  The result
+ * is bit for bit that of ilpm_conv2d_fwd_plan with the OIHW weights.
+ */
+int ilpm_conv2d_fwd_prepacked(const float *in, const float *packed, const float *bias,
+                              int C_in, int H, int W, int C_out, int K, int stride, int pad,
+                              const ilpm_plan *plan, float *out, hipStream_t stream);
+
 /* ---- helpers for layer stacks (not part of the convolution) ---- */
 
 /* x[i] = max(x[i], 0) for i < n, in place.  x: device fp32, n >= 0. */

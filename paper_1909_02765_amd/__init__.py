@@ -93,6 +93,9 @@ _SIGS = {
     "ilpm_num_variants": ([_i], _i),
     "ilpm_variant_name": ([_i, _i], ctypes.c_char_p),
     "ilpm_variant_info": ([_i, _i] + [ctypes.POINTER(_i)] * 5, _i),
+    "ilpm_conv2d_prepacked_size": ([_plan_p, _i, _i, _i, ctypes.POINTER(ctypes.c_size_t)], _i),
+    "ilpm_conv2d_prepack_weights": ([_vp, _i, _i, _i, _plan_p, _vp, _vp], _i),
+    "ilpm_conv2d_fwd_prepacked": ([_vp, _vp, _vp] + [_i] * 7 + [_plan_p, _vp, _vp], _i),
     "ilpm_relu_inplace": ([_vp, ctypes.c_int64, _vp], _i),
     "ilpm_maxpool2x2": ([_vp, _i, _i, _i, _vp, _vp], _i),
 }
@@ -228,6 +231,64 @@ def conv2d_launcher(x, w, bias, stride, pad, out, stream=None):
         rc = fwd(*args)
         if rc != OK:
             raise IlpmError(rc, "ilpm_conv2d_fwd")
+    return launch
+
+
+def prepacked_size(plan_: ilpm_plan, c_in: int, c_out: int, k: int) -> int:
+    n = ctypes.c_size_t()
+    _check(lib.ilpm_conv2d_prepacked_size(ctypes.byref(plan_), c_in, c_out, k, ctypes.byref(n)),
+           "ilpm_conv2d_prepacked_size")
+    return n.value
+
+
+def prepack_weights(w, plan_: ilpm_plan, stream=None):
+    """w [C_out, C_in, K, K] re-laid out for plan_'s kernel (a new flat CUDA
+    tensor); pass it to conv2d_prepacked with the same plan."""
+    torch = _torch()
+    if w.dim() != 4 or w.shape[2] != w.shape[3]:
+        raise ValueError("w must be [C_out, C_in, K, K]")
+    c_out, c_in, k, _ = w.shape
+    n = prepacked_size(plan_, c_in, c_out, k)
+    packed = torch.empty(n // 4, device=w.device, dtype=torch.float32)
+    _check(lib.ilpm_conv2d_prepack_weights(_dev_f32(w, "w"), c_in, c_out, k, ctypes.byref(plan_),
+                                           _dev_f32(packed, "packed"), _stream_handle(stream)),
+           "ilpm_conv2d_prepack_weights")
+    return packed
+
+
+def conv2d_prepacked(x, packed, c_out: int, k: int, bias=None, stride: int = 1, pad: int = 0, *,
+                     plan: ilpm_plan, out=None, stream=None):
+    """conv2d with weights from prepack_weights(w, plan)."""
+    torch = _torch()
+    if x.dim() != 4 or x.shape[0] != 1:
+        raise ValueError("x must be [1, C_in, H, W]")
+    _, c_in, h, wd = x.shape
+    ho, wo = out_size(h, k, stride, pad), out_size(wd, k, stride, pad)
+    if out is None:
+        out = torch.empty((1, c_out, max(ho, 1), max(wo, 1)), device=x.device, dtype=torch.float32)
+    elif tuple(out.shape) != (1, c_out, ho, wo):
+        raise ValueError(f"out must be [1, {c_out}, {ho}, {wo}]")
+    _check(lib.ilpm_conv2d_fwd_prepacked(_dev_f32(x, "x"), _dev_f32(packed, "packed"),
+                                         _dev_f32(bias, "bias") if bias is not None else None,
+                                         c_in, h, wd, c_out, k, stride, pad, ctypes.byref(plan),
+                                         _dev_f32(out, "out"), _stream_handle(stream)),
+           "ilpm_conv2d_fwd_prepacked")
+    return out
+
+
+def conv2d_prepacked_launcher(x, packed, c_out, k, bias, stride, pad, out, plan, stream=None):
+    """conv2d_launcher for prepacked weights (the plan object must outlive it)."""
+    _, c_in, h, wd = x.shape
+    if tuple(out.shape) != (1, c_out, out_size(h, k, stride, pad), out_size(wd, k, stride, pad)):
+        raise ValueError("out has the wrong shape")
+    args = (_dev_f32(x, "x"), _dev_f32(packed, "packed"), _dev_f32(bias, "bias") if bias is not None else None,
+            c_in, h, wd, c_out, k, stride, pad, ctypes.byref(plan), _dev_f32(out, "out"), _stream_handle(stream))
+    fwd = lib.ilpm_conv2d_fwd_prepacked
+
+    def launch():
+        rc = fwd(*args)
+        if rc != OK:
+            raise IlpmError(rc, "ilpm_conv2d_fwd_prepacked")
     return launch
 
 

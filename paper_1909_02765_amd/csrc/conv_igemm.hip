@@ -44,6 +44,7 @@
 // planes start on different bank halves (plane = 16 mod 32 words for odd
 // strides, an odd word count for even strides).
 #include <cmath>
+#include <type_traits>
 
 #include "internal.h"
 
@@ -164,23 +165,117 @@ struct AStage {
     float v[C::MA][C::G4][C::KK];
 };
 
-// Load the weights of the stage starting at input channel ci0: lane (g, l)
-// of m-block m takes output channel co_m and, for channel group c4, input
-// channel ci0 + ci_lane + 4*NWK*c4 (ci_lane = 4*wk + g).
+// Where a lane's weights come from.  Every wave holds, per stage, the
+// weights of its 16*MA output channels for its channel groups, as
+// A.v[m][c4][t] = w[co0 + wc*16*MA + 16*m + l][ci0 + 4*wk + g + 4*NWK*c4][t]
+// for lane (g, l).  A source issues them as NA single load instructions,
+// load(q) being the q-th.
+struct WeightCtx {
+    __amdgpu_buffer_rsrc_t rw;
+    int c_in, nchunks;
+    int co_lane0;  // co0 + wc*16*MA + l16 (output channel of m-block 0)
+    int ci_lane;   // 4*wk + g
+    int block0;    // prepacked layout: (co_t*nchunks)*NWK*NWC + wk*NWC + wc
+    int lane;
+};
+
+// OIHW weights: lane (g, l) reads its own contiguous run of KK taps per
+// (m, c4), in 16-byte pieces plus 4-byte ones for the tail of the run.
 template <class C>
-__device__ __forceinline__ void load_a(AStage<C> &A, __amdgpu_buffer_rsrc_t rw, const IgArgs &a,
-                                       const int (&a_off)[C::MA], int ci_lane, int ci0)
-{
+struct OihwWeights {
+    static constexpr int kPieces = C::KK / 4 + C::KK % 4;
+    static constexpr int NA = C::G4 * C::MA * kPieces;
+    __amdgpu_buffer_rsrc_t rw;
+    unsigned a_base[C::G4][C::MA];
+
+    __device__ __forceinline__ OihwWeights(const WeightCtx &k, int c_out, int ci0) : rw(k.rw)
+    {
 #pragma unroll
-    for (int c4 = 0; c4 < C::G4; ++c4) {
-        const int ci = ci0 + ci_lane + 4 * C::NWK * c4;
-        const bool ok = ci < a.c_in;
+        for (int c4 = 0; c4 < C::G4; ++c4) {
+            const int ci = ci0 + k.ci_lane + 4 * C::NWK * c4;
 #pragma unroll
-        for (int m = 0; m < C::MA; ++m) {
-            const int off = (ok && a_off[m] != kOutOfRange) ? a_off[m] + ci * C::KK * 4 : kOutOfRange;
-            load_taps<C::KK>(rw, off, A.v[m][c4]);
+            for (int m = 0; m < C::MA; ++m) {
+                const int co = k.co_lane0 + 16 * m;
+                a_base[c4][m] = (ci < k.c_in && co < c_out) ? (unsigned)((co * k.c_in + ci) * C::KK * 4)
+                                                             : (unsigned)kOutOfRange;
+            }
         }
     }
+
+    __device__ __forceinline__ void load(int q, AStage<C> &A) const
+    {
+        const int c4 = q / (C::MA * kPieces), m = (q / kPieces) % C::MA, piece = q % kPieces;
+        const unsigned base = a_base[c4][m];
+        float *dst = A.v[m][c4];
+        if (piece < C::KK / 4) {
+            const floatx4 v = __builtin_bit_cast(
+                floatx4, __builtin_amdgcn_raw_buffer_load_b128(rw, (int)(base + 16u * piece), 0, 0));
+            dst[4 * piece] = v[0];
+            dst[4 * piece + 1] = v[1];
+            dst[4 * piece + 2] = v[2];
+            dst[4 * piece + 3] = v[3];
+        } else {
+            const int e = C::KK / 4 * 4 + (piece - C::KK / 4);
+            dst[e] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rw, (int)(base + 4u * e), 0, 0));
+        }
+    }
+};
+
+// Prepacked weights (ilpm_conv2d_prepack_weights): for each (output-channel
+// tile, chunk of CC input channels, wk, wc) one block of 64*EPL floats, EPL =
+// MA*G4*KK, holding lane l's A.v in flat order; floats 4i..4i+3 of every lane
+// lie together ([i][lane][4]), so load instruction i of a wave reads one
+// contiguous kilobyte, and the last EPL mod 4 floats of each lane follow as
+// [j][lane] (one 256-byte load each).  Channels past C_out or C_in are
+// stored as zeros.
+template <class C>
+struct PackedWeights {
+    static constexpr int EPL = C::MA * C::G4 * C::KK;
+    static constexpr int N4 = EPL / 4, REM = EPL % 4;
+    static constexpr int NA = N4 + REM;
+    __amdgpu_buffer_rsrc_t rw;
+    unsigned base;  // bytes: this wave's block for the stage
+
+    __device__ __forceinline__ PackedWeights(const WeightCtx &k, int, int ci0) : rw(k.rw)
+    {
+        const int block = k.block0 + (ci0 / C::CC) * C::NWK * C::NWC;
+        base = (unsigned)block * (64u * EPL * 4u);
+        lane = k.lane;
+    }
+    int lane;
+
+    // Element e of the lane's flat order is A.v[m][c4][t] with
+    // e = (m*G4 + c4)*KK + t.
+    __device__ __forceinline__ static void put(AStage<C> &A, int e, float v)
+    {
+        A.v[e / (C::G4 * C::KK)][(e / C::KK) % C::G4][e % C::KK] = v;
+    }
+
+    __device__ __forceinline__ void load(int q, AStage<C> &A) const
+    {
+        if (q < N4) {
+            const floatx4 v = __builtin_bit_cast(
+                floatx4, __builtin_amdgcn_raw_buffer_load_b128(rw, (int)(base + 1024u * q + 16u * lane), 0, 0));
+#pragma unroll
+            for (int j = 0; j < 4; ++j) put(A, 4 * q + j, v[j]);
+        } else {
+            // Remainder float j = q - N4, one 4-byte load (in this toolchain
+            // the 8- and 12-byte buffer-load builtins come out as a single
+            // 4-byte load copied into every element, so they are not used).
+            const int j = q - N4;
+            put(A, 4 * N4 + j,
+                __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                              rw, (int)(base + 1024u * N4 + 256u * j + 4u * lane), 0, 0)));
+        }
+    }
+};
+
+// All of a stage's weights at once (the first stage).
+template <class C, class WS>
+__device__ __forceinline__ void load_a(AStage<C> &A, const WS &ws)
+{
+#pragma unroll
+    for (int q = 0; q < WS::NA; ++q) ws.load(q, A);
 }
 
 // Per-lane offsets of the halo DMA, the same for every stage: DMA instruction
@@ -230,36 +325,25 @@ __device__ __forceinline__ void dma_halo(float *buf, const float *__restrict__ x
 // drain as they go and still have the second half to land.  Item i < ND is
 // DMA instruction i of this wave; the rest are the weight loads, one 16-byte
 // (or, for the tail of a tap run, 4-byte) piece each.
-template <class C>
+template <class C, class WS>
 struct NextStage {
-    static constexpr int kPieces = C::KK / 4 + C::KK % 4;
     static constexpr int kFull = C::NIX / C::NW;
     static constexpr int ND = C::XPT;
-    static constexpr int N = ND + C::G4 * C::MA * kPieces;
+    static constexpr int N = ND + WS::NA;
 
-    __amdgpu_buffer_rsrc_t rx, rw;
+    __amdgpu_buffer_rsrc_t rx;
     float *buf;
     AStage<C> *A;
     const int *xo;
     int wave;
-    unsigned a_base[C::G4][C::MA];
+    WS ws;
 
-    __device__ __forceinline__ NextStage(float *buf_, AStage<C> &A_, const float *__restrict__ x,
-                                         __amdgpu_buffer_rsrc_t rw_, const IgArgs &a, const int (&a_off)[C::MA],
-                                         int ci_lane, int ci0, int wave_, const int (&xo_)[C::XPT])
-        : rw(rw_), buf(buf_), A(&A_), xo(xo_), wave(wave_)
+    __device__ __forceinline__ NextStage(float *buf_, AStage<C> &A_, const float *__restrict__ x, const IgArgs &a,
+                                         const WeightCtx &wk, int ci0, int wave_, const int (&xo_)[C::XPT])
+        : buf(buf_), A(&A_), xo(xo_), wave(wave_), ws(wk, a.c_out, ci0)
     {
         const unsigned plane = (unsigned)a.h * (unsigned)a.w;
         rx = make_rsrc(x + (size_t)ci0 * plane, (unsigned)(a.c_in - ci0) * plane * 4u);
-#pragma unroll
-        for (int c4 = 0; c4 < C::G4; ++c4) {
-            const int ci = ci0 + ci_lane + 4 * C::NWK * c4;
-            const bool ok = ci < a.c_in;
-#pragma unroll
-            for (int m = 0; m < C::MA; ++m)
-                a_base[c4][m] = (ok && a_off[m] != kOutOfRange) ? (unsigned)(a_off[m] + ci * C::KK * 4)
-                                                                 : (unsigned)kOutOfRange;
-        }
     }
 
     __device__ __forceinline__ void issue(int i)
@@ -274,21 +358,7 @@ struct NextStage {
             }
             return;
         }
-        const int q = i - ND;
-        const int c4 = q / (C::MA * kPieces), m = (q / kPieces) % C::MA, piece = q % kPieces;
-        const unsigned base = a_base[c4][m];
-        float *dst = A->v[m][c4];
-        if (piece < C::KK / 4) {
-            const floatx4 v = __builtin_bit_cast(
-                floatx4, __builtin_amdgcn_raw_buffer_load_b128(rw, (int)(base + 16u * piece), 0, 0));
-            dst[4 * piece] = v[0];
-            dst[4 * piece + 1] = v[1];
-            dst[4 * piece + 2] = v[2];
-            dst[4 * piece + 3] = v[3];
-        } else {
-            const int e = C::KK / 4 * 4 + (piece - C::KK / 4);
-            dst[e] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rw, (int)(base + 4u * e), 0, 0));
-        }
+        ws.load(i - ND, *A);
     }
 };
 
@@ -586,7 +656,7 @@ __device__ __forceinline__ void final_stage(const float *xl, const AStage<C> &A,
     }
 }
 
-template <class C>
+template <class C, bool PK>
 __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x, const float *__restrict__ w,
                                                     const float *__restrict__ bias, float *__restrict__ out,
                                                     float *__restrict__ part, IgArgs a)
@@ -626,16 +696,19 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
     const int c_begin = split * a.chunks_per_split;
     const int c_end = min(c_begin + a.chunks_per_split, a.nchunks);
 
-    // Weight operand: lane (g, l16) of m-block m loads output channel
-    // co0 + wc*16*MA + 16*m + l16.
-    const __amdgpu_buffer_rsrc_t rw = make_rsrc(w, (unsigned)a.c_out * a.c_in * C::KK * 4u);
+    // Weight operand: lane (g, l16) of m-block m holds output channel
+    // co0 + wc*16*MA + 16*m + l16, from OIHW or from the prepacked layout.
+    using WS = typename std::conditional<PK, PackedWeights<C>, OihwWeights<C>>::type;
     const int ci_lane = 4 * wk + g;
-    int a_off[C::MA];
-#pragma unroll
-    for (int m = 0; m < C::MA; ++m) {
-        const int co = co0 + wc * 16 * C::MA + 16 * m + l16;
-        a_off[m] = co < a.c_out ? co * a.c_in * C::KK * 4 : kOutOfRange;
-    }
+    WeightCtx wctx;
+    wctx.rw = make_rsrc(w, PK ? (unsigned)a.co_tiles * a.nchunks * (C::COT * C::CC * C::KK * 4u)
+                              : (unsigned)a.c_out * a.c_in * C::KK * 4u);
+    wctx.c_in = a.c_in;
+    wctx.nchunks = a.nchunks;
+    wctx.co_lane0 = co0 + wc * 16 * C::MA + l16;
+    wctx.ci_lane = ci_lane;
+    wctx.block0 = (co_t * a.nchunks * C::NWK + wk) * C::NWC + wc;
+    wctx.lane = lane;
 
     // Input operand: LDS base of each pixel block for this lane.
     int b_base[C::NB];
@@ -668,7 +741,7 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
     halo_offsets<C>(xo, a, wave, lane, ih0, iw0);
     AStage<C> a0, a1;
     dma_halo<C>(lds0, x, a, c_begin * C::CC, wave, xo);
-    load_a<C>(a0, rw, a, a_off, ci_lane, c_begin * C::CC);
+    load_a<C>(a0, WS(wctx, a.c_out, c_begin * C::CC));
     stage_ready();
 
     for (int ch = c_begin;; ch += 2) {
@@ -677,7 +750,7 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
             break;
         }
         {
-            NextStage<C> next(lds1, a1, x, rw, a, a_off, ci_lane, (ch + 1) * C::CC, wave, xo);
+            NextStage<C, WS> next(lds1, a1, x, a, wctx, (ch + 1) * C::CC, wave, xo);
             compute_stage<C>(lds0, a0, b_base, acc, next);
         }
         stage_ready();
@@ -686,7 +759,7 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
             break;
         }
         {
-            NextStage<C> next(lds0, a0, x, rw, a, a_off, ci_lane, (ch + 2) * C::CC, wave, xo);
+            NextStage<C, WS> next(lds0, a0, x, a, wctx, (ch + 2) * C::CC, wave, xo);
             compute_stage<C>(lds1, a1, b_base, acc, next);
         }
         stage_ready();
@@ -745,19 +818,57 @@ __global__ __launch_bounds__(128) void sum_splits(const float *__restrict__ part
     }
 }
 
+// The prepacked weight layout of a variant (see PackedWeights), one thread
+// per packed float; channels past C_out or C_in become zeros.
+struct PackGeom {
+    int c_in, c_out, kk, cot, cc, nwc, nwk, ma, g4, nchunks;
+};
+
+__global__ __launch_bounds__(256) void pack_weights(const float *__restrict__ w, float *__restrict__ packed,
+                                                    PackGeom g, int64_t total)
+{
+    const int epl = g.ma * g.g4 * g.kk;
+    const int n4 = epl / 4;
+    const int64_t step = (int64_t)gridDim.x * 256;
+    for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < total; idx += step) {
+        const int64_t block = idx / (64 * epl);
+        const int within = (int)(idx - block * (64 * epl));
+        int lane, e;
+        if (within < n4 * 256) {
+            lane = (within % 256) / 4;
+            e = 4 * (within / 256) + within % 4;
+        } else {
+            const int r = within - n4 * 256;
+            lane = r % 64;
+            e = 4 * n4 + r / 64;
+        }
+        const int wc = (int)(block % g.nwc);
+        const int64_t b1 = block / g.nwc;
+        const int wk = (int)(b1 % g.nwk);
+        const int64_t b2 = b1 / g.nwk;
+        const int chunk = (int)(b2 % g.nchunks);
+        const int co_t = (int)(b2 / g.nchunks);
+        const int m = e / (g.g4 * g.kk), c4 = (e / g.kk) % g.g4, tap = e % g.kk;
+        const int co = co_t * g.cot + wc * 16 * g.ma + 16 * m + (lane & 15);
+        const int ci = chunk * g.cc + 4 * wk + (lane >> 4) + 4 * g.nwk * c4;
+        packed[idx] = (co < g.c_out && ci < g.c_in) ? w[((int64_t)co * g.c_in + ci) * g.kk + tap] : 0.f;
+    }
+}
+
 struct Variant {
     const char *name;
     int ks, s, th, tw, nwc, nwp, nwk, ma, cc;
     int nt, cot, lds;
     void (*launch)(dim3 grid, hipStream_t st, const float *, const float *, const float *, float *, float *,
-                   const IgArgs &);
+                   const IgArgs &, bool packed);
 };
 
 template <class C>
 void launch_cfg(dim3 grid, hipStream_t st, const float *x, const float *w, const float *b, float *o, float *ws,
-                const IgArgs &a)
+                const IgArgs &a, bool packed)
 {
-    hipLaunchKernelGGL(conv_igemm<C>, grid, dim3(C::NT), 0, st, x, w, b, o, ws, a);
+    if (packed) hipLaunchKernelGGL((conv_igemm<C, true>), grid, dim3(C::NT), 0, st, x, w, b, o, ws, a);
+    else hipLaunchKernelGGL((conv_igemm<C, false>), grid, dim3(C::NT), 0, st, x, w, b, o, ws, a);
 }
 
 template <class C>
@@ -818,6 +929,9 @@ bool igemm_make_plan(const ConvShape &s, int variant, int splits, ilpm_plan *p)
     if ((int64_t)s.c_in * s.h * s.w * 4 >= (1LL << 31)) return false;
     if ((int64_t)s.c_out * s.c_in * s.k * s.k * 4 >= (1LL << 31)) return false;
     if ((int64_t)s.c_out * s.h_out * s.w_out * 4 >= (1LL << 30)) return false;
+    // ... and so are those of the prepacked weights (padded to whole tiles).
+    if ((int64_t)ceil_div(s.c_out, d.cot) * d.cot * ceil_div(s.c_in, d.cc) * d.cc * s.k * s.k * 4 >= (1LL << 31))
+        return false;
     const long tiles = (long)ceil_div(s.h_out, d.th) * ceil_div(s.w_out, d.tw) * ceil_div(s.c_out, d.cot);
     if (tiles > 0x7fffffffL) return false;
     const int nchunks = ceil_div(s.c_in, d.cc);
@@ -875,8 +989,35 @@ double igemm_plan_cost(const ConvShape &s, const ilpm_plan &p)
     return cycles;
 }
 
+int64_t igemm_packed_floats(const ilpm_plan &p, int c_in, int c_out)
+{
+    const Variant &d = kVariants[p.variant];
+    return (int64_t)ceil_div(c_out, d.cot) * ceil_div(c_in, d.cc) * d.cot * d.cc * d.ks * d.ks;
+}
+
+hipError_t igemm_pack(const ilpm_plan &p, int c_in, int c_out, const float *w, float *packed, hipStream_t stream)
+{
+    const Variant &d = kVariants[p.variant];
+    PackGeom g;
+    g.c_in = c_in;
+    g.c_out = c_out;
+    g.kk = d.ks * d.ks;
+    g.cot = d.cot;
+    g.cc = d.cc;
+    g.nwc = d.nwc;
+    g.nwk = d.nwk;
+    g.ma = d.ma;
+    g.g4 = d.cc / 4 / d.nwk;
+    g.nchunks = ceil_div(c_in, d.cc);
+    const int64_t total = igemm_packed_floats(p, c_in, c_out);
+    int64_t blocks = (total + 255) / 256;
+    if (blocks > 65536) blocks = 65536;
+    hipLaunchKernelGGL(pack_weights, dim3((unsigned)blocks), dim3(256), 0, stream, w, packed, g, total);
+    return hipGetLastError();
+}
+
 hipError_t igemm_launch(const ilpm_plan &p, const ConvShape &s, const float *x, const float *w,
-                        const float *bias, float *out, void *workspace, hipStream_t stream)
+                        const float *bias, float *out, void *workspace, hipStream_t stream, bool packed)
 {
     const Variant &d = kVariants[p.variant];
     IgArgs a;
@@ -894,7 +1035,7 @@ hipError_t igemm_launch(const ilpm_plan &p, const ConvShape &s, const float *x, 
     a.splits = p.splits;
     const int tiles = p.grid / p.splits;
     float *part = static_cast<float *>(workspace);
-    d.launch(dim3(tiles * p.splits), stream, x, w, bias, out, part, a);
+    d.launch(dim3(tiles * p.splits), stream, x, w, bias, out, part, a, packed);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || p.splits == 1) return e;
     const int64_t total = (int64_t)s.c_out * s.h_out * s.w_out;

@@ -197,7 +197,7 @@ void log_plan(const ConvShape &s, const ilpm_plan &p)
 }
 
 int run(const float *in, const float *w, const float *bias, const ConvShape &s, float *out, const ilpm_plan &p,
-        hipStream_t stream)
+        hipStream_t stream, bool packed = false)
 {
     int dev = 0;
     int rc = device_check(&dev);
@@ -210,9 +210,31 @@ int run(const float *in, const float *w, const float *bias, const ConvShape &s, 
     // earlier, unrelated runtime call of this thread left behind.
     (void)hipGetLastError();
     hipError_t e;
-    if (p.path == ILPM_PATH_IGEMM) e = igemm_launch(p, s, in, w, bias, out, ws, stream);
+    if (p.path == ILPM_PATH_IGEMM) e = igemm_launch(p, s, in, w, bias, out, ws, stream, packed);
     else e = direct_launch(p, s, in, w, bias, out, stream);
     return e == hipSuccess ? ILPM_OK : hip_fail(e);
+}
+
+// Bytes of the prepacked weights of plan p (0 with *rc set on a bad plan).
+size_t prepacked_bytes(const ilpm_plan &p, int c_in, int c_out, int k, int *rc)
+{
+    *rc = ILPM_OK;
+    if (c_in <= 0 || c_out <= 0 || k <= 0 || (int64_t)c_out * c_in * k * k > kMaxElems) {
+        *rc = ILPM_ERR_INVALID_ARG;
+        return 0;
+    }
+    int kk = 0, st = 0, th, tw, ct;
+    if (p.path == ILPM_PATH_IGEMM) {
+        if (!igemm_variant_info(p.variant, &kk, &st, &th, &tw, &ct) || kk != k) {
+            *rc = ILPM_ERR_INVALID_ARG;
+            return 0;
+        }
+        return sizeof(float) * (size_t)igemm_packed_floats(p, c_in, c_out);
+    }
+    if (p.path == ILPM_PATH_DIRECT && p.variant >= 0 && p.variant < direct_num_variants())
+        return sizeof(float) * (size_t)c_out * c_in * k * k;
+    *rc = ILPM_ERR_INVALID_ARG;
+    return 0;
 }
 
 }  // namespace
@@ -347,6 +369,56 @@ int ilpm_conv2d_fwd_plan(const float *in, const float *w, const float *bias, int
     rc = check_plan(s, *plan);
     if (rc != ILPM_OK) return rc;
     return run(in, w, bias, s, out, *plan, stream);
+}
+
+int ilpm_conv2d_prepacked_size(const ilpm_plan *plan, int C_in, int C_out, int K, size_t *bytes)
+{
+    if (!plan || !bytes) return ILPM_ERR_INVALID_ARG;
+    int rc;
+    const size_t b = prepacked_bytes(*plan, C_in, C_out, K, &rc);
+    if (rc != ILPM_OK) return rc;
+    *bytes = b;
+    return ILPM_OK;
+}
+
+int ilpm_conv2d_prepack_weights(const float *w, int C_in, int C_out, int K, const ilpm_plan *plan, float *packed,
+                                hipStream_t stream)
+{
+    if (!plan || !w || !packed) return ILPM_ERR_INVALID_ARG;
+    int rc;
+    const size_t pb = prepacked_bytes(*plan, C_in, C_out, K, &rc);
+    if (rc != ILPM_OK) return rc;
+    if (((uintptr_t)w | (uintptr_t)packed) & 15u) return ILPM_ERR_INVALID_ARG;
+    if (overlaps(w, sizeof(float) * (size_t)C_out * C_in * K * K, packed, pb)) return ILPM_ERR_INVALID_ARG;
+    int dev = 0;
+    rc = device_check(&dev);
+    if (rc != ILPM_OK) return rc;
+    (void)hipGetLastError();
+    hipError_t e;
+    if (plan->path == ILPM_PATH_IGEMM) e = igemm_pack(*plan, C_in, C_out, w, packed, stream);
+    else e = hipMemcpyAsync(packed, w, pb, hipMemcpyDeviceToDevice, stream);
+    return e == hipSuccess ? ILPM_OK : hip_fail(e);
+}
+
+int ilpm_conv2d_fwd_prepacked(const float *in, const float *packed, const float *bias, int C_in, int H, int W,
+                              int C_out, int K, int stride, int pad, const ilpm_plan *plan, float *out,
+                              hipStream_t stream)
+{
+    if (!plan || !packed) return ILPM_ERR_INVALID_ARG;
+    ConvShape s;
+    int rc = check_dims(C_in, H, W, C_out, K, stride, pad, &s);
+    if (rc != ILPM_OK) return rc;
+    // The OIHW-size checks of validate() cover in, bias and out; the packed
+    // buffer gets its own size.
+    rc = validate(in, packed, bias, s, out);
+    if (rc != ILPM_OK) return rc;
+    const size_t pb = prepacked_bytes(*plan, C_in, C_out, K, &rc);
+    if (rc != ILPM_OK) return rc;
+    if (((uintptr_t)packed & 15u) || overlaps(out, sizeof(float) * (size_t)C_out * s.h_out * s.w_out, packed, pb))
+        return ILPM_ERR_INVALID_ARG;
+    rc = check_plan(s, *plan);
+    if (rc != ILPM_OK) return rc;
+    return run(in, packed, bias, s, out, *plan, stream, true);
 }
 
 int ilpm_relu_inplace(float *x, int64_t n, hipStream_t stream)

@@ -31,8 +31,13 @@ bool igemm_make_plan(const ConvShape &s, int variant, int splits, ilpm_plan *p);
 // Modelled cost of a plan in SIMD cycles of the slowest compute unit, used to
 // rank variants; lower is better.
 double igemm_plan_cost(const ConvShape &s, const ilpm_plan &p);
+// packed: w is in the variant's prepacked layout (igemm_pack) instead of OIHW.
 hipError_t igemm_launch(const ilpm_plan &p, const ConvShape &s, const float *x, const float *w,
-                        const float *bias, float *out, void *workspace, hipStream_t stream);
+                        const float *bias, float *out, void *workspace, hipStream_t stream, bool packed);
+// Floats of the prepacked weights of a variant for C_in, C_out (zero-padded
+// to whole output-channel tiles and input-channel chunks).
+int64_t igemm_packed_floats(const ilpm_plan &p, int c_in, int c_out);
+hipError_t igemm_pack(const ilpm_plan &p, int c_in, int c_out, const float *w, float *packed, hipStream_t stream);
 
 // ---- measured plan table (tuned_plans.inc) ----
 // The plan the offline sweep found fastest for this exact shape, if any.

@@ -164,3 +164,40 @@ def test_tuned_table_entries_resolve():
             assert plan.splits == splits
         n += 1
     assert n >= 10
+
+
+def test_prepacked_size():
+    """Packed weights of a matrix-core plan are padded to whole output-channel
+    tiles and input-channel chunks; a direct plan's are an OIHW copy."""
+    import ctypes
+    for (c_in, c_out, k, s) in [(64, 64, 3, 1), (13, 40, 3, 1), (512, 512, 5, 1), (37, 70, 1, 1), (128, 256, 3, 2)]:
+        for v in range(ilpm.num_variants(ilpm.PATH_IGEMM)):
+            info = ilpm.variant_info(ilpm.PATH_IGEMM, v)
+            if info["k"] != k or info["stride"] != s:
+                continue
+            p = ilpm.plan_variant(c_in, 16, 16, c_out, k, s, k // 2, ilpm.PATH_IGEMM, v, 1)
+            cot, cc = p.co_tile, p.ci_chunk
+            want = -(-c_out // cot) * cot * (-(-c_in // cc) * cc) * k * k * 4
+            assert ilpm.prepacked_size(p, c_in, c_out, k) == want
+            with pytest.raises(ilpm.IlpmError):
+                ilpm.prepacked_size(p, c_in, c_out, k + 2)
+    p = ilpm.plan_variant(3, 16, 16, 8, 7, 1, 3, ilpm.PATH_DIRECT, 0)
+    assert ilpm.prepacked_size(p, 3, 8, 7) == 8 * 3 * 49 * 4
+
+
+def test_prepacked_rejects_before_any_launch():
+    import ctypes
+    p = ilpm.plan(64, 56, 56, 64, 3, 1, 1)
+    lib = ilpm.lib
+    assert lib.ilpm_conv2d_prepack_weights(None, 64, 64, 3, ctypes.byref(p), 0x100000, None) == ilpm.ERR_INVALID_ARG
+    assert lib.ilpm_conv2d_prepack_weights(0x1000 + 4, 64, 64, 3, ctypes.byref(p), 0x100000, None) \
+        == ilpm.ERR_INVALID_ARG                                        # misaligned
+    assert lib.ilpm_conv2d_prepack_weights(0x1000, 64, 64, 5, ctypes.byref(p), 0x100000, None) \
+        == ilpm.ERR_INVALID_ARG                                        # K the plan does not take
+    assert lib.ilpm_conv2d_prepack_weights(0x1000, 64, 64, 3, ctypes.byref(p), 0x1000 + 256, None) \
+        == ilpm.ERR_INVALID_ARG                                        # overlap
+    # a plan for another shape is refused
+    assert lib.ilpm_conv2d_fwd_prepacked(0x1000, 0x10000000, None, 64, 28, 28, 64, 3, 1, 1, ctypes.byref(p),
+                                         0x20000000, None) == ilpm.ERR_INVALID_ARG
+    assert lib.ilpm_conv2d_fwd_prepacked(0x1000, None, None, 64, 56, 56, 64, 3, 1, 1, ctypes.byref(p),
+                                         0x20000000, None) == ilpm.ERR_INVALID_ARG

@@ -229,3 +229,55 @@ def test_graph_replay_matches_eager(ilpm, case):
         g.replay()
         torch.cuda.synchronize()
         np.testing.assert_array_equal(out.cpu().numpy(), eager)
+
+
+def _prepacked_vs_oihw(ilpm, x, w, b, stride, pad, plan, label):
+    torch = torch_cuda()
+    c_out, c_in, k, _ = w.shape
+    xd, wd, bd = dev(x), dev(w), dev(b)
+    ho, wo = ilpm.out_size(x.shape[2], k, stride, pad), ilpm.out_size(x.shape[3], k, stride, pad)
+    note(f"[prepacked] {label} {describe(plan)}")
+    want = ilpm.conv2d(xd, wd, bd, stride, pad, plan=plan)
+    packed = ilpm.prepack_weights(wd, plan)
+    assert packed.numel() * 4 == ilpm.prepacked_size(plan, c_in, c_out, k)
+    got = ilpm.conv2d_prepacked(xd, packed, c_out, k, bd, stride, pad, plan=plan)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(got.cpu().numpy(), want.cpu().numpy(), err_msg=f"{label} {describe(plan)}")
+    assert got.shape == (1, c_out, ho, wo)
+
+
+@pytest.mark.parametrize("case", CASES, ids=lambda c: c.name)
+def test_prepacked_matches_oihw_bitwise(ilpm, case):
+    """Every variant run on prepacked weights gives exactly the bits of the same
+    plan on the OIHW weights (the packing moves data, it changes no
+    arithmetic); the OIHW path is checked against the oracle elsewhere."""
+    x, w, b, ref, sab = case_data(case)
+    for plan in plans_for(ilpm, case.c_in, case.h, case.w, case.c_out, case.k, case.stride, case.pad):
+        if plan.path == ilpm.PATH_DIRECT and plan.variant == 1 and case.c_in * case.c_out * case.h * case.w > 5e7:
+            continue  # the plain-global direct kernel is slow on the large layers; it reads OIHW either way
+        _prepacked_vs_oihw(ilpm, x, w, b, case.stride, case.pad, plan, case.name)
+
+
+def test_prepacked_ragged_channels(ilpm):
+    """Channel counts that leave partial output-channel tiles and partial
+    input-channel chunks (the packed layout's zero padding), against the
+    oracle as well."""
+    for seed, (c_in, h, w_, c_out, k, s, p) in enumerate([(13, 17, 19, 40, 3, 1, 1), (37, 9, 9, 70, 1, 1, 0),
+                                                         (21, 11, 10, 33, 5, 1, 2), (29, 15, 15, 17, 3, 2, 1)]):
+        x, w, b = random_case(7000 + 10 * seed, c_in, h, w_, c_out, k)
+        ref, sab = oracle.conv2d_f64(x, w, b, s, p)
+        for v in range(ilpm.num_variants(ilpm.PATH_IGEMM)):
+            info = ilpm.variant_info(ilpm.PATH_IGEMM, v)
+            if info["k"] != k or info["stride"] != s:
+                continue
+            for splits in (1, 0):
+                try:
+                    plan = ilpm.plan_variant(c_in, h, w_, c_out, k, s, p, ilpm.PATH_IGEMM, v, splits)
+                except ilpm.IlpmError:
+                    continue
+                _prepacked_vs_oihw(ilpm, x, w, b, s, p, plan, f"ragged{seed}")
+                torch = torch_cuda()
+                packed = ilpm.prepack_weights(dev(w), plan)
+                got = ilpm.conv2d_prepacked(dev(x), packed, c_out, k, dev(b), s, p, plan=plan)
+                torch.cuda.synchronize()
+                assert_matches(got.cpu().numpy(), ref, sab, c_in, k, f"prepacked ragged{seed} v{v}")
