@@ -353,10 +353,73 @@ def bench_vgg16(torch, ilpm, workloads, steps):
         total_flops += flops
         ilpm.relu_(out)
         x = ilpm.maxpool2x2(out) if pool else out
+    rows += bench_vgg16_stack(torch, ilpm, workloads, max(20, steps // 10))
     rows.append({"layer": "vgg16_total_conv", "us": round(total_us, 3), "graph_us": round(total_graph_us, 3),
                  "gflops": round(total_flops / total_us / 1e3, 1), "floor_us": round(total_floor, 3),
                  "frac": round(total_floor / total_us, 4)})
     print(json.dumps(rows[-1]), file=sys.stderr)
+    return rows
+
+
+def bench_vgg16_stack(torch, ilpm, workloads, reps):
+    """The whole 13-conv stack end to end (ReLU after every conv, 2x2 max-pool
+    after stages 1-4), timed over `reps` back-to-back passes: once with the
+    separate ReLU and pool kernels, once with the fused epilogue."""
+    from workloads import to_device
+    layers = workloads.vgg16_layers()
+    x0 = to_device(torch, workloads.vgg16_input())
+    ws = [to_device(torch, workloads.vgg16_weights(ci, co, seed)) for _, ci, co, _, _, seed in layers]
+    # unfused: conv -> relu_ -> (pool)
+    bufs, launches = [], []
+    x = x0
+    for (name, ci, co, hw, pool, _), w in zip(layers, ws):
+        y = torch.empty((1, co, hw, hw), device="cuda", dtype=torch.float32)
+        conv = ilpm.conv2d_launcher(x, w, None, 1, 1, y)
+        launches.append(conv)
+        launches.append(lambda y=y: ilpm.relu_(y))
+        if pool:
+            z = torch.empty((1, co, hw // 2, hw // 2), device="cuda", dtype=torch.float32)
+            launches.append(lambda y=y, z=z: ilpm.lib.ilpm_maxpool2x2(
+                ilpm._dev_f32(y, "y"), y.shape[1], y.shape[2], y.shape[3], ilpm._dev_f32(z, "z"),
+                ilpm._stream_handle()))
+            x = z
+        else:
+            x = y
+        bufs.append(y)
+    out_unfused = x
+    # fused: one call per layer
+    fused = []
+    x = x0
+    for (name, ci, co, hw, pool, _), w in zip(layers, ws):
+        epi = ilpm.EPI_RELU | (ilpm.EPI_MAXPOOL2 if pool else 0)
+        y = torch.empty(ilpm.epilogue_out_shape(co, hw, hw, 3, 1, 1, epi), device="cuda", dtype=torch.float32)
+        fused.append(ilpm.conv2d_epilogue_launcher(x, w, None, 1, 1, epi, y))
+        x = y
+    out_fused = x
+
+    def timed(fns):
+        for _ in range(3):
+            for f in fns:
+                f()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            for f in fns:
+                f()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) * 1000.0 / reps
+
+    t_unfused = timed(launches)
+    t_fused = timed(fused)
+    same = bool(torch.equal(out_unfused, out_fused))
+    rows = [{"layer": "vgg16_stack_unfused", "us": round(t_unfused, 3),
+             "note": "13 convs + 13 ReLU + 4 max-pool kernels, end to end"},
+            {"layer": "vgg16_stack_fused", "us": round(t_fused, 3),
+             "note": "13 convs with the fused ReLU / ReLU+max-pool epilogue", "same_output_bits": same}]
+    for r in rows:
+        print(json.dumps(r), file=sys.stderr)
     return rows
 
 

@@ -208,6 +208,35 @@ int ilpm_conv2d_fwd_prepacked(const float *in, const float *packed, const float 
                               int C_in, int H, int W, int C_out, int K, int stride, int pad,
                               const ilpm_plan *plan, float *out, hipStream_t stream);
 
+/* ---- fused epilogue ----
+ *
+ * A CNN layer follows the convolution with ReLU and, between stages, a 2x2
+ * max-pool (the ResNet and VGG networks the paper evaluates, Section 5).
+ * Applying them as the convolution's results are written saves writing the
+ * full-size output and reading it back.
+ */
+#define ILPM_EPI_RELU 1     /* out = max(conv + bias, 0) */
+#define ILPM_EPI_MAXPOOL2 2 /* out[c][i][j] = max of the 2x2 window at (2i, 2j) of (conv + bias),
+                               [C_out][H_out/2][W_out/2] (floor); needs H_out, W_out >= 2 */
+
+/*
+ * ilpm_conv2d_fwd_epilogue -- ilpm_conv2d_fwd followed by `epilogue`, a
+ * combination of the ILPM_EPI_* bits (0 = none).  With both bits set the
+ * result is max-pool of ReLU, which equals ReLU of max-pool.  `out` has the
+ * pooled shape when ILPM_EPI_MAXPOOL2 is set.  plan: NULL for the default
+ * plan of the shape, or one made for this exact shape.  Pooling uses
+ * workspace for the full-size convolution output (see
+ * ilpm_conv2d_epilogue_workspace_size).  The values are exactly those of the
+ * unfused sequence conv (same plan) -> ReLU -> max-pool.
+ */
+int ilpm_conv2d_fwd_epilogue(const float *in, const float *w, const float *bias,
+                             int C_in, int H, int W, int C_out, int K, int stride, int pad,
+                             int epilogue, const ilpm_plan *plan, float *out, hipStream_t stream);
+
+/* Workspace bytes ilpm_conv2d_fwd_epilogue needs (plan NULL = default plan). */
+int ilpm_conv2d_epilogue_workspace_size(int C_in, int H, int W, int C_out, int K, int stride, int pad,
+                                        int epilogue, const ilpm_plan *plan, size_t *bytes);
+
 /* ---- helpers for layer stacks (not part of the convolution) ---- */
 
 /* x[i] = max(x[i], 0) for i < n, in place.  x: device fp32, n >= 0. */

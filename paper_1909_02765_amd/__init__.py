@@ -96,6 +96,8 @@ _SIGS = {
     "ilpm_conv2d_prepacked_size": ([_plan_p, _i, _i, _i, ctypes.POINTER(ctypes.c_size_t)], _i),
     "ilpm_conv2d_prepack_weights": ([_vp, _i, _i, _i, _plan_p, _vp, _vp], _i),
     "ilpm_conv2d_fwd_prepacked": ([_vp, _vp, _vp] + [_i] * 7 + [_plan_p, _vp, _vp], _i),
+    "ilpm_conv2d_fwd_epilogue": ([_vp, _vp, _vp] + [_i] * 8 + [_plan_p, _vp, _vp], _i),
+    "ilpm_conv2d_epilogue_workspace_size": ([_i] * 8 + [_plan_p, ctypes.POINTER(ctypes.c_size_t)], _i),
     "ilpm_relu_inplace": ([_vp, ctypes.c_int64, _vp], _i),
     "ilpm_maxpool2x2": ([_vp, _i, _i, _i, _vp, _vp], _i),
 }
@@ -289,6 +291,61 @@ def conv2d_prepacked_launcher(x, packed, c_out, k, bias, stride, pad, out, plan,
         rc = fwd(*args)
         if rc != OK:
             raise IlpmError(rc, "ilpm_conv2d_fwd_prepacked")
+    return launch
+
+
+EPI_RELU = 1
+EPI_MAXPOOL2 = 2
+
+
+def epilogue_out_shape(c_out, h, w, k, stride, pad, epilogue):
+    ho, wo = out_size(h, k, stride, pad), out_size(w, k, stride, pad)
+    if epilogue & EPI_MAXPOOL2:
+        ho, wo = ho // 2, wo // 2
+    return (1, c_out, ho, wo)
+
+
+def epilogue_workspace_size(c_in, h, w, c_out, k, stride, pad, epilogue, plan_=None) -> int:
+    n = ctypes.c_size_t()
+    _check(lib.ilpm_conv2d_epilogue_workspace_size(c_in, h, w, c_out, k, stride, pad, epilogue,
+                                                   ctypes.byref(plan_) if plan_ is not None else None,
+                                                   ctypes.byref(n)), "ilpm_conv2d_epilogue_workspace_size")
+    return n.value
+
+
+def conv2d_epilogue(x, w, bias=None, stride: int = 1, pad: int = 0, epilogue: int = EPI_RELU, *,
+                    plan: Optional[ilpm_plan] = None, out=None, stream=None):
+    """conv2d (+ bias) followed by ReLU and/or a 2x2 max-pool (EPI_* bits)."""
+    torch = _torch()
+    _, c_in, h, wd = x.shape
+    c_out, _, k, _ = w.shape
+    shape = epilogue_out_shape(c_out, h, wd, k, stride, pad, epilogue)
+    if out is None:
+        out = torch.empty(tuple(max(d, 1) for d in shape), device=x.device, dtype=torch.float32)
+    elif tuple(out.shape) != shape:
+        raise ValueError(f"out must be {list(shape)}")
+    _check(lib.ilpm_conv2d_fwd_epilogue(_dev_f32(x, "x"), _dev_f32(w, "w"),
+                                        _dev_f32(bias, "bias") if bias is not None else None,
+                                        c_in, h, wd, c_out, k, stride, pad, epilogue,
+                                        ctypes.byref(plan) if plan is not None else None,
+                                        _dev_f32(out, "out"), _stream_handle(stream)), "ilpm_conv2d_fwd_epilogue")
+    return out
+
+
+def conv2d_epilogue_launcher(x, w, bias, stride, pad, epilogue, out, stream=None):
+    """conv2d_launcher for ilpm_conv2d_fwd_epilogue with the default plan."""
+    _, c_in, h, wd = x.shape
+    c_out, _, k, _ = w.shape
+    if tuple(out.shape) != epilogue_out_shape(c_out, h, wd, k, stride, pad, epilogue):
+        raise ValueError("out has the wrong shape")
+    args = (_dev_f32(x, "x"), _dev_f32(w, "w"), _dev_f32(bias, "bias") if bias is not None else None,
+            c_in, h, wd, c_out, k, stride, pad, epilogue, None, _dev_f32(out, "out"), _stream_handle(stream))
+    fwd = lib.ilpm_conv2d_fwd_epilogue
+
+    def launch():
+        rc = fwd(*args)
+        if rc != OK:
+            raise IlpmError(rc, "ilpm_conv2d_fwd_epilogue")
     return launch
 
 

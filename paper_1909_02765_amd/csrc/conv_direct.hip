@@ -29,6 +29,7 @@ constexpr int kLdsFloats = 16384;  // 64 KiB
 struct DirectArgs {
     int c_in, h, w, c_out, k, stride, pad, h_out, w_out;
     int halo_h, halo_w, chunk, tiles_w;
+    int relu;  // store max(., 0)
 };
 
 __global__ __launch_bounds__(kThreads) void conv_direct_lds(const float *__restrict__ x,
@@ -109,7 +110,8 @@ __global__ __launch_bounds__(kThreads) void conv_direct_lds(const float *__restr
             const int co = co0 + j;
             if (co < a.c_out) {
                 const float b = bias ? bias[co] : 0.f;
-                out[((size_t)co * a.h_out + oh) * a.w_out + ow] = acc[j] + b;
+                const float v = acc[j] + b;
+                out[((size_t)co * a.h_out + oh) * a.w_out + ow] = a.relu && v < 0.f ? 0.f : v;
             }
         }
     }
@@ -139,7 +141,8 @@ __global__ __launch_bounds__(kThreads) void conv_direct_global(const float *__re
             }
         }
     }
-    out[i] = acc + (bias ? bias[co] : 0.f);
+    const float v = acc + (bias ? bias[co] : 0.f);
+    out[i] = a.relu && v < 0.f ? 0.f : v;
 }
 
 DirectArgs make_args(const ConvShape &s)
@@ -230,9 +233,10 @@ bool direct_make_plan(const ConvShape &s, int variant, ilpm_plan *p)
 }
 
 hipError_t direct_launch(const ilpm_plan &p, const ConvShape &s, const float *x, const float *w,
-                         const float *bias, float *out, hipStream_t stream)
+                         const float *bias, float *out, hipStream_t stream, bool relu)
 {
     DirectArgs a = make_args(s);
+    a.relu = relu ? 1 : 0;
     if (p.variant == 0) {
         a.chunk = p.ci_chunk;
         const int tiles = ceil_div(s.h_out, kTileH) * ceil_div(s.w_out, kTileW);

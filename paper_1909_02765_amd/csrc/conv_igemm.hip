@@ -116,6 +116,8 @@ struct Cfg {
 struct IgArgs {
     int c_in, h, w, c_out, pad, h_out, w_out;
     int tiles_w, co_tiles, nchunks, chunks_per_split, splits;
+    int to_part;  // write raw partial sums to slice `split` of the workspace (a finishing kernel follows)
+    int relu;     // otherwise: store max(conv + bias, 0)
 };
 
 // Buffer descriptors give branch-free loads: a lane whose element lies in the
@@ -465,9 +467,11 @@ struct Epilogue {
     float b[C::MA][4];
     // The 4x4x1 tail block (TAIL4): after the k-slice sum, lane 4*cg + j of
     // the first 16 stores channels tail_co + 16*m + r, r = 0..3, at pixel j.
-    int tail_co, c_out;
+    int tail_co, c_out, relu;
     unsigned tail_pix, plane_b;
     float tail_b[C::MA][4];
+
+    __device__ __forceinline__ float fin(float v) const { return relu && v < 0.f ? 0.f : v; }
 
     __device__ __forceinline__ void init(const IgArgs &a, float *out, float *part, const float *bias, int split,
                                          int co_lane, int wp, int g, int l16, int oh0, int ow0)
@@ -475,8 +479,9 @@ struct Epilogue {
         constexpr unsigned kFar = 1u << 30;
         plane_b = (unsigned)a.h_out * a.w_out * 4u;
         c_out = a.c_out;
+        relu = a.to_part ? 0 : a.relu;
         const unsigned out_b = (unsigned)a.c_out * plane_b;
-        ro = make_rsrc(a.splits == 1 ? out : part + (size_t)split * (out_b / 4), out_b);
+        ro = make_rsrc(a.to_part ? part + (size_t)split * (out_b / 4) : out, out_b);
 #pragma unroll
         for (int n = 0; n < C::NB; ++n) {
             const int p = (wp * C::NB + n) * 16 + l16;
@@ -489,7 +494,7 @@ struct Epilogue {
             for (int r = 0; r < 4; ++r) {
                 const int co = co_lane + 16 * m + r;
                 const bool ok = co < a.c_out;
-                b[m][r] = (a.splits == 1 && bias && ok) ? bias[co] : 0.f;
+                b[m][r] = (!a.to_part && bias && ok) ? bias[co] : 0.f;
                 chan_off[m][r] = ok ? (unsigned)co * plane_b : kFar;
             }
         if constexpr (C::TAIL4) {
@@ -505,7 +510,7 @@ struct Epilogue {
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
                     const int co = tail_co + 16 * m + r;
-                    tail_b[m][r] = (a.splits == 1 && bias && co < a.c_out) ? bias[co] : 0.f;
+                    tail_b[m][r] = (!a.to_part && bias && co < a.c_out) ? bias[co] : 0.f;
                 }
         }
     }
@@ -522,14 +527,14 @@ struct Epilogue {
                 s += __shfl_xor(s, 32);
                 const int co = tail_co + 16 * m + r;
                 const unsigned off = (co < c_out && tail_pix < kFar) ? (unsigned)co * plane_b + tail_pix : kFar;
-                __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, s + tail_b[m][r]), ro, (int)off,
-                                                      0, 0);
+                __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, fin(s + tail_b[m][r])), ro,
+                                                      (int)off, 0, 0);
             }
             return;
         }
 #pragma unroll
         for (int r = 0; r < 4; ++r)
-            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v[r] + b[m][r]), ro,
+            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, fin(v[r] + b[m][r])), ro,
                                                   (int)(chan_off[m][r] + pix_off[n]), 0, 0);
     }
 };
@@ -729,8 +734,8 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
     // out while the last blocks are still being computed.  Accumulator block
     // (m, n), register r holds output channel co0 + wc*16*MA + 16*m + 4*g + r
     // at tile pixel (wp*NB + n)*16 + l16 (the 4x4x1 tail block is laid out
-    // as its Cfg comment says).  Split workgroups write slice
-    // `split` of the partial sums, in the output's layout, without the bias.
+    // as its Cfg comment says).  With to_part, workgroups write slice `split`
+    // of the partial sums, in the output's layout, without bias or ReLU.
     // Stores go through a buffer descriptor: a lane outside the output (pixel
     // or channel) gets an offset of at least 2^30 bytes, past the descriptor's
     // range (< 2^30, checked when the plan is made), and its store is dropped.
@@ -766,12 +771,12 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
     }
 }
 
-// out[i] = part[0][i] + part[1][i] + ... + part[splits-1][i] + bias[channel(i)],
-// summed in that order.  Each thread owns V consecutive outputs (V = 4 when
-// every split slice is 16-byte aligned) and issues the loads of up to kBatch
-// slices before it adds any of them, so the latency of the partial sums (just
-// written by the conv kernel, mostly still in the last-level cache) is paid
-// once per batch rather than once per slice.
+// out[i] = part[0][i] + part[1][i] + ... + part[splits-1][i] + bias[channel(i)]
+// (then max(., 0) with relu), summed in that order.  Each thread owns V
+// consecutive outputs (V = 4 when every split slice is 16-byte aligned) and
+// issues the loads of up to kBatch slices before it adds any of them, so the
+// latency of the partial sums (just written by the conv kernel, mostly still
+// in the last-level cache) is paid once per batch rather than once per slice.
 template <int V>
 struct VecF;
 template <>
@@ -783,38 +788,76 @@ struct VecF<4> {
     using T = float4;
 };
 
+constexpr int kBatch = 16;
+
+// Sum of the `splits` slices at element i of a T-typed view, in slice order.
+template <class T>
+__device__ __forceinline__ T sum_slices(const T *pv, int64_t stride, int64_t i, int splits)
+{
+    T s = pv[i];
+    int k = 1;
+    for (; k + kBatch <= splits; k += kBatch) {
+        T v[kBatch];
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j) v[j] = pv[(size_t)(k + j) * stride + i];
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j) s += v[j];
+    }
+    T v[kBatch];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j)
+        if (k + j < splits) v[j] = pv[(size_t)(k + j) * stride + i];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j)
+        if (k + j < splits) s += v[j];
+    return s;
+}
+
 template <int V>
 __global__ __launch_bounds__(128) void sum_splits(const float *__restrict__ part, const float *__restrict__ bias,
-                                                  float *__restrict__ out, int splits, int plane, int64_t total)
+                                                  float *__restrict__ out, int splits, int plane, int64_t total,
+                                                  int relu)
 {
     using T = typename VecF<V>::T;
-    constexpr int kBatch = 16;
     const int64_t nvec = total / V;
     const T *pv = reinterpret_cast<const T *>(part);
     const int64_t step = (int64_t)gridDim.x * 128;
     for (int64_t i = (int64_t)blockIdx.x * 128 + threadIdx.x; i < nvec; i += step) {
-        T s = pv[i];
-        int k = 1;
-        for (; k + kBatch <= splits; k += kBatch) {
-            T v[kBatch];
-#pragma unroll
-            for (int j = 0; j < kBatch; ++j) v[j] = pv[(size_t)(k + j) * nvec + i];
-#pragma unroll
-            for (int j = 0; j < kBatch; ++j) s += v[j];
-        }
-        {
-            T v[kBatch];
-#pragma unroll
-            for (int j = 0; j < kBatch; ++j)
-                if (k + j < splits) v[j] = pv[(size_t)(k + j) * nvec + i];
-#pragma unroll
-            for (int j = 0; j < kBatch; ++j)
-                if (k + j < splits) s += v[j];
-        }
+        const T s = sum_slices<T>(pv, nvec, i, splits);
         float *o = out + i * V;
         const float *sv = reinterpret_cast<const float *>(&s);
 #pragma unroll
-        for (int e = 0; e < V; ++e) o[e] = sv[e] + (bias ? bias[(i * V + e) / plane] : 0.f);
+        for (int e = 0; e < V; ++e) {
+            const float v = sv[e] + (bias ? bias[(i * V + e) / plane] : 0.f);
+            o[e] = relu && v < 0.f ? 0.f : v;
+        }
+    }
+}
+
+// The same sum for the four outputs of each 2x2 window, each plus its bias
+// (and ReLU), then their maximum: out [c][h_out/2][w_out/2].
+__global__ __launch_bounds__(128) void sum_splits_pool(const float *__restrict__ part,
+                                                       const float *__restrict__ bias, float *__restrict__ out,
+                                                       int splits, int c, int h_out, int w_out, int relu)
+{
+    const int hp = h_out / 2, wp = w_out / 2;
+    const int64_t total = (int64_t)c * hp * wp;
+    const int64_t slice = (int64_t)c * h_out * w_out;
+    const int64_t step = (int64_t)gridDim.x * 128;
+    for (int64_t i = (int64_t)blockIdx.x * 128 + threadIdx.x; i < total; i += step) {
+        const int j = (int)(i % wp);
+        const int r = (int)((i / wp) % hp);
+        const int ch = (int)(i / ((int64_t)wp * hp));
+        const int64_t base = ((int64_t)ch * h_out + 2 * r) * w_out + 2 * j;
+        const float b = bias ? bias[ch] : 0.f;
+        float m = sum_slices<float>(part, slice, base, splits) + b;
+        float v = sum_slices<float>(part, slice, base + 1, splits) + b;
+        m = v > m ? v : m;
+        v = sum_slices<float>(part, slice, base + w_out, splits) + b;
+        m = v > m ? v : m;
+        v = sum_slices<float>(part, slice, base + w_out + 1, splits) + b;
+        m = v > m ? v : m;
+        out[i] = relu && m < 0.f ? 0.f : m;
     }
 }
 
@@ -1016,10 +1059,19 @@ hipError_t igemm_pack(const ilpm_plan &p, int c_in, int c_out, const float *w, f
     return hipGetLastError();
 }
 
+size_t igemm_workspace_bytes(const ilpm_plan &p, const ConvShape &s, int epilogue)
+{
+    const bool to_part = p.splits > 1 || (epilogue & ILPM_EPI_MAXPOOL2);
+    return to_part ? sizeof(float) * (size_t)s.c_out * s.h_out * s.w_out * p.splits : 0;
+}
+
 hipError_t igemm_launch(const ilpm_plan &p, const ConvShape &s, const float *x, const float *w,
-                        const float *bias, float *out, void *workspace, hipStream_t stream, bool packed)
+                        const float *bias, float *out, void *workspace, hipStream_t stream, bool packed,
+                        int epilogue)
 {
     const Variant &d = kVariants[p.variant];
+    const bool pool = (epilogue & ILPM_EPI_MAXPOOL2) != 0;
+    const bool relu = (epilogue & ILPM_EPI_RELU) != 0;
     IgArgs a;
     a.c_in = s.c_in;
     a.h = s.h;
@@ -1033,11 +1085,21 @@ hipError_t igemm_launch(const ilpm_plan &p, const ConvShape &s, const float *x, 
     a.nchunks = ceil_div(s.c_in, d.cc);
     a.chunks_per_split = ceil_div(a.nchunks, p.splits);
     a.splits = p.splits;
+    a.to_part = (p.splits > 1 || pool) ? 1 : 0;
+    a.relu = relu ? 1 : 0;
     const int tiles = p.grid / p.splits;
     float *part = static_cast<float *>(workspace);
     d.launch(dim3(tiles * p.splits), stream, x, w, bias, out, part, a, packed);
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess || p.splits == 1) return e;
+    if (e != hipSuccess || !a.to_part) return e;
+    if (pool) {
+        const int64_t total = (int64_t)s.c_out * (s.h_out / 2) * (s.w_out / 2);
+        int64_t blocks = (total + 127) / 128;
+        if (blocks > 8192) blocks = 8192;
+        hipLaunchKernelGGL(sum_splits_pool, dim3((unsigned)blocks), dim3(128), 0, stream, part, bias, out, p.splits,
+                           s.c_out, s.h_out, s.w_out, a.relu);
+        return hipGetLastError();
+    }
     const int64_t total = (int64_t)s.c_out * s.h_out * s.w_out;
     const bool vec4 = total % 4 == 0;
     const int64_t threads = vec4 ? total / 4 : total;
@@ -1045,10 +1107,10 @@ hipError_t igemm_launch(const ilpm_plan &p, const ConvShape &s, const float *x, 
     if (blocks > 8192) blocks = 8192;
     if (vec4)
         hipLaunchKernelGGL(sum_splits<4>, dim3((unsigned)blocks), dim3(128), 0, stream, part, bias, out, p.splits,
-                           s.h_out * s.w_out, total);
+                           s.h_out * s.w_out, total, a.relu);
     else
         hipLaunchKernelGGL(sum_splits<1>, dim3((unsigned)blocks), dim3(128), 0, stream, part, bias, out, p.splits,
-                           s.h_out * s.w_out, total);
+                           s.h_out * s.w_out, total, a.relu);
     return hipGetLastError();
 }
 

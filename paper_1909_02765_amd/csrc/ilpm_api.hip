@@ -65,13 +65,20 @@ int check_dims(int c_in, int h, int w, int c_out, int k, int stride, int pad, Co
     return ILPM_OK;
 }
 
-int validate(const void *in, const void *w, const void *bias, const ConvShape &s, const void *out)
+// Output bytes of a call: the conv output, or its 2x2-pooled version.
+size_t out_bytes(const ConvShape &s, int epilogue)
+{
+    if (epilogue & ILPM_EPI_MAXPOOL2) return sizeof(float) * (size_t)s.c_out * (s.h_out / 2) * (s.w_out / 2);
+    return sizeof(float) * (size_t)s.c_out * s.h_out * s.w_out;
+}
+
+int validate(const void *in, const void *w, const void *bias, const ConvShape &s, const void *out, int epilogue = 0)
 {
     if (!in || !w || !out) return ILPM_ERR_INVALID_ARG;
     const size_t in_b = sizeof(float) * (size_t)s.c_in * s.h * s.w;
     const size_t w_b = sizeof(float) * (size_t)s.c_out * s.c_in * s.k * s.k;
     const size_t b_b = sizeof(float) * (size_t)s.c_out;
-    const size_t o_b = sizeof(float) * (size_t)s.c_out * s.h_out * s.w_out;
+    const size_t o_b = out_bytes(s, epilogue);
     if (((uintptr_t)in | (uintptr_t)w | (uintptr_t)out | (uintptr_t)bias) & 3u) return ILPM_ERR_INVALID_ARG;
     if (overlaps(out, o_b, in, in_b) || overlaps(out, o_b, w, w_b) || overlaps(out, o_b, bias, b_b))
         return ILPM_ERR_INVALID_ARG;
@@ -196,22 +203,39 @@ void log_plan(const ConvShape &s, const ilpm_plan &p)
                  p.workspace_bytes);
 }
 
+// Workspace bytes a plan needs with an epilogue: the split partial sums, and
+// with pooling the full-size conv output (as partial sums for the
+// matrix-core path, conv + bias for the direct path).
+size_t workspace_need(const ilpm_plan &p, const ConvShape &s, int epilogue)
+{
+    if (p.path == ILPM_PATH_IGEMM) return igemm_workspace_bytes(p, s, epilogue);
+    return (epilogue & ILPM_EPI_MAXPOOL2) ? sizeof(float) * (size_t)s.c_out * s.h_out * s.w_out : 0;
+}
+
 int run(const float *in, const float *w, const float *bias, const ConvShape &s, float *out, const ilpm_plan &p,
-        hipStream_t stream, bool packed = false)
+        hipStream_t stream, bool packed = false, int epilogue = 0)
 {
     int dev = 0;
     int rc = device_check(&dev);
     if (rc != ILPM_OK) return rc;
     void *ws = nullptr;
-    rc = get_workspace(dev, p.workspace_bytes, &ws);
+    rc = get_workspace(dev, workspace_need(p, s, epilogue), &ws);
     if (rc != ILPM_OK) return rc;
     log_plan(s, p);
     // Launch errors are read back with hipGetLastError; drop any error an
     // earlier, unrelated runtime call of this thread left behind.
     (void)hipGetLastError();
     hipError_t e;
-    if (p.path == ILPM_PATH_IGEMM) e = igemm_launch(p, s, in, w, bias, out, ws, stream, packed);
-    else e = direct_launch(p, s, in, w, bias, out, stream);
+    const bool relu = (epilogue & ILPM_EPI_RELU) != 0;
+    if (p.path == ILPM_PATH_IGEMM) {
+        e = igemm_launch(p, s, in, w, bias, out, ws, stream, packed, epilogue);
+    } else if (epilogue & ILPM_EPI_MAXPOOL2) {
+        float *full = static_cast<float *>(ws);
+        e = direct_launch(p, s, in, w, bias, full, stream, false);
+        if (e == hipSuccess) e = launch_maxpool2x2(full, s.c_out, s.h_out, s.w_out, out, stream, relu);
+    } else {
+        e = direct_launch(p, s, in, w, bias, out, stream, relu);
+    }
     return e == hipSuccess ? ILPM_OK : hip_fail(e);
 }
 
@@ -327,6 +351,25 @@ int ilpm_conv2d_workspace_size(int C_in, int H, int W, int C_out, int K, int str
     return ILPM_OK;
 }
 
+int ilpm_conv2d_epilogue_workspace_size(int C_in, int H, int W, int C_out, int K, int stride, int pad,
+                                        int epilogue, const ilpm_plan *plan, size_t *bytes)
+{
+    if (!bytes || (epilogue & ~(ILPM_EPI_RELU | ILPM_EPI_MAXPOOL2))) return ILPM_ERR_INVALID_ARG;
+    ConvShape s;
+    int rc = check_dims(C_in, H, W, C_out, K, stride, pad, &s);
+    if (rc != ILPM_OK) return rc;
+    ilpm_plan p;
+    if (plan) {
+        rc = check_plan(s, *plan);
+        p = *plan;
+    } else {
+        rc = choose_plan(s, &p);
+    }
+    if (rc != ILPM_OK) return rc;
+    *bytes = workspace_need(p, s, epilogue);
+    return ILPM_OK;
+}
+
 int ilpm_last_hip_error(void) { return g_last_hip; }
 
 int ilpm_set_workspace(void *ptr, size_t bytes, hipStream_t stream)
@@ -421,6 +464,28 @@ int ilpm_conv2d_fwd_prepacked(const float *in, const float *packed, const float 
     return run(in, packed, bias, s, out, *plan, stream, true);
 }
 
+int ilpm_conv2d_fwd_epilogue(const float *in, const float *w, const float *bias, int C_in, int H, int W, int C_out,
+                             int K, int stride, int pad, int epilogue, const ilpm_plan *plan, float *out,
+                             hipStream_t stream)
+{
+    if (epilogue & ~(ILPM_EPI_RELU | ILPM_EPI_MAXPOOL2)) return ILPM_ERR_INVALID_ARG;
+    ConvShape s;
+    int rc = check_dims(C_in, H, W, C_out, K, stride, pad, &s);
+    if (rc != ILPM_OK) return rc;
+    if ((epilogue & ILPM_EPI_MAXPOOL2) && (s.h_out < 2 || s.w_out < 2)) return ILPM_ERR_INVALID_ARG;
+    rc = validate(in, w, bias, s, out, epilogue);
+    if (rc != ILPM_OK) return rc;
+    ilpm_plan p;
+    if (plan) {
+        rc = check_plan(s, *plan);
+        p = *plan;
+    } else {
+        rc = choose_plan(s, &p);
+    }
+    if (rc != ILPM_OK) return rc;
+    return run(in, w, bias, s, out, p, stream, false, epilogue);
+}
+
 int ilpm_relu_inplace(float *x, int64_t n, hipStream_t stream)
 {
     if (n < 0 || (!x && n > 0) || ((uintptr_t)x & 3u)) return ILPM_ERR_INVALID_ARG;
@@ -445,7 +510,7 @@ int ilpm_maxpool2x2(const float *in, int C, int H, int W, float *out, hipStream_
     int rc = device_check(&dev);
     if (rc != ILPM_OK) return rc;
     (void)hipGetLastError();
-    const hipError_t e = launch_maxpool2x2(in, C, H, W, out, stream);
+    const hipError_t e = launch_maxpool2x2(in, C, H, W, out, stream, false);
     return e == hipSuccess ? ILPM_OK : hip_fail(e);
 }
 

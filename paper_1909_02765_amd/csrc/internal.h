@@ -19,8 +19,9 @@ int direct_num_variants();
 bool direct_variant_info(int v, int *k, int *stride, int *tile_h, int *tile_w, int *co_tile);
 const char *direct_variant_name(int v);
 bool direct_make_plan(const ConvShape &s, int variant, ilpm_plan *p);
+// relu: store max(conv + bias, 0).
 hipError_t direct_launch(const ilpm_plan &p, const ConvShape &s, const float *x, const float *w,
-                         const float *bias, float *out, hipStream_t stream);
+                         const float *bias, float *out, hipStream_t stream, bool relu);
 
 // ---- implicit-GEMM (fp32 MFMA) family ----
 int igemm_num_variants();
@@ -32,8 +33,13 @@ bool igemm_make_plan(const ConvShape &s, int variant, int splits, ilpm_plan *p);
 // rank variants; lower is better.
 double igemm_plan_cost(const ConvShape &s, const ilpm_plan &p);
 // packed: w is in the variant's prepacked layout (igemm_pack) instead of OIHW.
+// epilogue: ILPM_EPI_* bits.  With ILPM_EPI_MAXPOOL2, out is the pooled
+// [C_out][H_out/2][W_out/2] tensor and the workspace holds every split's
+// full-size partial sums (igemm_workspace_bytes).
 hipError_t igemm_launch(const ilpm_plan &p, const ConvShape &s, const float *x, const float *w,
-                        const float *bias, float *out, void *workspace, hipStream_t stream, bool packed);
+                        const float *bias, float *out, void *workspace, hipStream_t stream, bool packed,
+                        int epilogue);
+size_t igemm_workspace_bytes(const ilpm_plan &p, const ConvShape &s, int epilogue);
 // Floats of the prepacked weights of a variant for C_in, C_out (zero-padded
 // to whole output-channel tiles and input-channel chunks).
 int64_t igemm_packed_floats(const ilpm_plan &p, int c_in, int c_out);
@@ -45,7 +51,7 @@ bool tuned_plan(const ConvShape &s, ilpm_plan *p);
 
 // ---- helpers ----
 hipError_t launch_relu(float *x, int64_t n, hipStream_t stream);
-hipError_t launch_maxpool2x2(const float *in, int c, int h, int w, float *out, hipStream_t stream);
+hipError_t launch_maxpool2x2(const float *in, int c, int h, int w, float *out, hipStream_t stream, bool relu);
 
 inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
 

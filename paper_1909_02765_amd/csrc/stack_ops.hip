@@ -16,7 +16,7 @@ __global__ __launch_bounds__(256) void relu_kernel(float *x, int64_t n)
 }
 
 __global__ __launch_bounds__(256) void maxpool2x2_kernel(const float *__restrict__ in, int c, int h, int w,
-                                                         float *__restrict__ out)
+                                                         float *__restrict__ out, int relu)
 {
     const int ho = h / 2, wo = w / 2;
     const int64_t total = (int64_t)c * ho * wo;
@@ -31,7 +31,7 @@ __global__ __launch_bounds__(256) void maxpool2x2_kernel(const float *__restrict
         m = p[1] > m ? p[1] : m;
         m = p[w] > m ? p[w] : m;
         m = p[w + 1] > m ? p[w + 1] : m;
-        out[i] = m;
+        out[i] = relu && m < 0.f ? 0.f : m;
     }
 }
 
@@ -52,11 +52,12 @@ hipError_t launch_relu(float *x, int64_t n, hipStream_t stream)
     return hipGetLastError();
 }
 
-hipError_t launch_maxpool2x2(const float *in, int c, int h, int w, float *out, hipStream_t stream)
+hipError_t launch_maxpool2x2(const float *in, int c, int h, int w, float *out, hipStream_t stream, bool relu)
 {
     const int64_t total = (int64_t)c * (h / 2) * (w / 2);
     if (total == 0) return hipSuccess;
-    hipLaunchKernelGGL(maxpool2x2_kernel, dim3(grid_for(total)), dim3(256), 0, stream, in, c, h, w, out);
+    hipLaunchKernelGGL(maxpool2x2_kernel, dim3(grid_for(total)), dim3(256), 0, stream, in, c, h, w, out,
+                       relu ? 1 : 0);
     return hipGetLastError();
 }
 

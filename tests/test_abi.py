@@ -201,3 +201,30 @@ def test_prepacked_rejects_before_any_launch():
                                          0x20000000, None) == ilpm.ERR_INVALID_ARG
     assert lib.ilpm_conv2d_fwd_prepacked(0x1000, None, None, 64, 56, 56, 64, 3, 1, 1, ctypes.byref(p),
                                          0x20000000, None) == ilpm.ERR_INVALID_ARG
+
+
+def test_epilogue_argument_checks():
+    lib = ilpm.lib
+    # unknown epilogue bits
+    assert lib.ilpm_conv2d_fwd_epilogue(0x1000, 0x100000, None, 3, 8, 8, 4, 3, 1, 1, 4, None, 0x200000, None) \
+        == ilpm.ERR_INVALID_ARG
+    # pooling needs a 2x2 window: H_out = 1
+    assert lib.ilpm_conv2d_fwd_epilogue(0x1000, 0x100000, None, 3, 1, 8, 4, 1, 1, 0, ilpm.EPI_MAXPOOL2, None,
+                                        0x200000, None) == ilpm.ERR_INVALID_ARG
+    # the pooled output is a quarter of the conv output: placing it right after
+    # the input is fine for the overlap check, one float earlier is not
+    in_b = 4 * 3 * 8 * 8
+    assert lib.ilpm_conv2d_validate(0x1000, 0x100000, None, 3, 8, 8, 4, 3, 1, 1, 0x1000 + in_b) == ilpm.OK
+    assert lib.ilpm_conv2d_fwd_epilogue(0x1000, 0x100000, None, 3, 8, 8, 4, 3, 1, 1, ilpm.EPI_MAXPOOL2, None,
+                                        0x1000 + in_b - 4, None) == ilpm.ERR_INVALID_ARG
+
+
+def test_epilogue_workspace_size():
+    # pooling keeps the full-size convolution output (times the splits) in the workspace
+    for shape in [(64, 56, 56, 64, 3, 1, 1), (512, 7, 7, 512, 3, 1, 1), (3, 224, 224, 64, 3, 1, 1)]:
+        c_in, h, w, c_out, k, s, p = shape
+        plan = ilpm.plan(*shape)
+        full = 4 * c_out * ilpm.out_size(h, k, s, p) * ilpm.out_size(w, k, s, p)
+        assert ilpm.epilogue_workspace_size(*shape, 0) == plan.workspace_bytes
+        assert ilpm.epilogue_workspace_size(*shape, ilpm.EPI_RELU) == plan.workspace_bytes
+        assert ilpm.epilogue_workspace_size(*shape, ilpm.EPI_MAXPOOL2) == full * max(plan.splits, 1)

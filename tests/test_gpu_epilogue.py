@@ -1,0 +1,105 @@
+"""GPU: the fused epilogue (bias + ReLU, 2x2 max-pool) of every variant and
+split count gives exactly the unfused sequence -- the same plan's convolution,
+then ReLU, then the pool, applied to its fp32 output -- and, anchored to the
+oracle, max-pool(ReLU(exact conv)) within the tolerance."""
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+from gpu_common import dev, note, random_case, torch_cuda
+
+pytestmark = pytest.mark.gpu
+
+EPIS = (1, 2, 3)  # RELU, MAXPOOL2, both
+
+
+@pytest.fixture(scope="module")
+def ilpm():
+    torch_cuda()
+    import paper_1909_02765_amd as m
+    oracle.set_threads(16)
+    return m
+
+
+def pool_relu_np(y, epi):
+    """ReLU and/or 2x2 max-pool (floor) of a [1,C,H,W] float32 array, exactly."""
+    if epi & 1:
+        y = np.maximum(y, np.float32(0))
+    if epi & 2:
+        _, c, h, w = y.shape
+        y = y[:, :, : h // 2 * 2, : w // 2 * 2].reshape(1, c, h // 2, 2, w // 2, 2).max(axis=(3, 5))
+    return y
+
+
+def all_plans(ilpm, c_in, h, w, c_out, k, s, p):
+    plans = []
+    for v in range(ilpm.num_variants(ilpm.PATH_DIRECT)):
+        try:
+            plans.append(ilpm.plan_variant(c_in, h, w, c_out, k, s, p, ilpm.PATH_DIRECT, v))
+        except ilpm.IlpmError:
+            pass
+    for v in range(ilpm.num_variants(ilpm.PATH_IGEMM)):
+        seen = set()
+        for splits in (1, 0, 3):
+            try:
+                q = ilpm.plan_variant(c_in, h, w, c_out, k, s, p, ilpm.PATH_IGEMM, v, splits)
+            except ilpm.IlpmError:
+                continue
+            if q.splits not in seen:
+                seen.add(q.splits)
+                plans.append(q)
+    return plans
+
+
+def check_case(ilpm, name, x, w, b, s, p, skip_slow=False):
+    torch = torch_cuda()
+    c_out, c_in, k, _ = w.shape
+    h, wd = x.shape[2], x.shape[3]
+    xd, wdv, bd = dev(x), dev(w), dev(b)
+    for plan in all_plans(ilpm, c_in, h, wd, c_out, k, s, p):
+        if skip_slow and plan.path == ilpm.PATH_DIRECT and plan.variant == 1:
+            continue
+        unfused = ilpm.conv2d(xd, wdv, bd, s, p, plan=plan)
+        torch.cuda.synchronize()
+        base = unfused.cpu().numpy()
+        for epi in EPIS:
+            note(f"[epilogue] {name} path={plan.path} v={plan.variant} splits={plan.splits} epi={epi}")
+            got = ilpm.conv2d_epilogue(xd, wdv, bd, s, p, epi, plan=plan)
+            torch.cuda.synchronize()
+            np.testing.assert_array_equal(got.cpu().numpy(), pool_relu_np(base, epi),
+                                          err_msg=f"{name} plan {plan.path}/{plan.variant}/{plan.splits} epi {epi}")
+
+
+@pytest.mark.parametrize("case", workloads.ALL_CASES, ids=lambda c: c.name)
+def test_epilogue_matches_unfused(ilpm, case):
+    x, w, b = case.inputs()
+    big = case.c_in * case.c_out * case.h * case.w > 5e7
+    check_case(ilpm, case.name, x, w, b, case.stride, case.pad, skip_slow=big)
+
+
+def test_epilogue_ragged(ilpm):
+    """Odd output sizes (the pool drops the last row/column), partial tiles,
+    and channel counts that fill no tile exactly."""
+    for seed, (c_in, h, w_, c_out, k, s, p) in enumerate([(13, 17, 19, 40, 3, 1, 1), (37, 9, 9, 70, 1, 1, 0),
+                                                         (21, 11, 10, 33, 5, 1, 2), (29, 15, 15, 17, 3, 2, 1)]):
+        x, w, b = random_case(8000 + 10 * seed, c_in, h, w_, c_out, k)
+        check_case(ilpm, f"ragged{seed}", x, w, b, s, p)
+
+
+def test_epilogue_against_oracle(ilpm):
+    """Default plan, both bits: max-pool(ReLU(exact conv)) within the
+    tolerance of the window element the maximum comes from (max and ReLU are
+    1-Lipschitz, so the largest window tolerance bounds the difference)."""
+    torch = torch_cuda()
+    for case in (workloads.VGG_EARLY, workloads.RESNET_CONV2, workloads.RESNET_CONV5):
+        x, w, b = case.inputs()
+        ref, sab = oracle.conv2d_f64(x, w, b, case.stride, case.pad)
+        tol = 1e-4 * (1.0 + sab / (case.c_in * case.k * case.k))
+        want = pool_relu_np(ref, 3)
+        tw = pool_relu_np(tol, 2)  # largest tolerance per window
+        note(f"[epilogue-oracle] {case.name}")
+        got = ilpm.conv2d_epilogue(dev(x), dev(w), dev(b), case.stride, case.pad, 3)
+        torch.cuda.synchronize()
+        err = np.abs(got.cpu().numpy().astype(np.float64) - want)
+        assert (err <= tw).all(), f"{case.name}: worst {np.max(err / tw)}"
