@@ -140,6 +140,27 @@ def time_prepacked(torch, ilpm, x, w, b, s, p, out, plan, steps, warmup):
     return start.elapsed_time(stop) * 1000.0 / steps
 
 
+def time_winograd(torch, ilpm, x, w, b, p, out, steps, warmup):
+    """Mean µs per call of the Winograd F(2x2,3x3) comparison path (filter
+    transform done once beforehand), or None when it cannot run here."""
+    try:
+        u = ilpm.winograd_transform_filter(w)
+        launch = ilpm.conv2d_winograd_launcher(x, u, b, p, out)
+        for _ in range(warmup):
+            launch()
+    except ilpm.IlpmError:
+        return None
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(steps):
+        launch()
+    stop.record()
+    torch.cuda.synchronize()
+    return start.elapsed_time(stop) * 1000.0 / steps
+
+
 def cpu_baseline(case, x, w, b, y_gpu):
     """The CPU oracle timed on this host on the whole layer (repeated for at
     least 10 s),
@@ -225,6 +246,9 @@ def bench_case(torch, ilpm, case, steps, warmup, graph=False):
         res["graph_us"] = time_layer_graph(torch, ilpm, xd, wd, bd, case.stride, case.pad, out, steps)
         res["prepacked_us"] = time_prepacked(torch, ilpm, xd, wd, bd, case.stride, case.pad, out, plan, steps,
                                              warmup)
+        if case.k == 3 and case.stride == 1:
+            out_w = torch.empty_like(out)
+            res["winograd_us"] = time_winograd(torch, ilpm, xd, wd, bd, case.pad, out_w, steps, warmup)
     return res
 
 
@@ -318,6 +342,8 @@ def main():
             fl, kind = roofline_floor_us(rr["flops"], rr["nbytes"])
             rows.append({"layer": c.name, "us": round(rr["us"], 3), "graph_us": round(rr["graph_us"], 3),
                          "prepacked_us": round(rr["prepacked_us"], 3),
+                         "winograd_us": (round(rr["winograd_us"], 3) if rr.get("winograd_us") is not None
+                                         else None),
                          "gflops": round(rr["flops"] / rr["us"] / 1e3, 1),
                          "floor_us": round(fl, 3), "bound": kind, "frac": round(fl / rr["us"], 4),
                          "plan": rr["plan"].as_dict()})

@@ -237,6 +237,26 @@ int ilpm_conv2d_fwd_epilogue(const float *in, const float *w, const float *bias,
 int ilpm_conv2d_epilogue_workspace_size(int C_in, int H, int W, int C_out, int K, int stride, int pad,
                                         int epilogue, const ilpm_plan *plan, size_t *bytes);
 
+/* ---- Winograd F(2x2, 3x3): a comparison path ----
+ *
+ * Not the ILP-M method: the competitor the paper measures it against
+ * (Section 3, Winograd; Section 5).  3x3 filters, stride 1, any padding.  The
+ * filter transform U = G g G^T (16 floats per (C_out, C_in) pair, layout
+ * [16][C_out][C_in]) is done once by ilpm_winograd_transform_filter; each
+ * call transforms the input, runs 16 channel-contraction GEMMs through the
+ * rocBLAS the process already loaded (loaded at run time; without it the call
+ * returns ILPM_ERR_UNSUPPORTED) and transforms the output back.  Workspace:
+ * ilpm_conv2d_winograd_workspace_size bytes (same registered / library-owned
+ * workspace as the split plans).  Results agree with the definition within
+ * the same tolerance; the rounding is that of Winograd's transforms, not of
+ * a direct sum.
+ */
+int ilpm_winograd_filter_size(int C_in, int C_out, size_t *bytes);
+int ilpm_winograd_transform_filter(const float *w, int C_in, int C_out, float *u, hipStream_t stream);
+int ilpm_conv2d_winograd_workspace_size(int C_in, int H, int W, int C_out, int pad, size_t *bytes);
+int ilpm_conv2d_fwd_winograd(const float *in, const float *u, const float *bias,
+                             int C_in, int H, int W, int C_out, int pad, float *out, hipStream_t stream);
+
 /* ---- helpers for layer stacks (not part of the convolution) ---- */
 
 /* x[i] = max(x[i], 0) for i < n, in place.  x: device fp32, n >= 0. */

@@ -98,6 +98,10 @@ _SIGS = {
     "ilpm_conv2d_fwd_prepacked": ([_vp, _vp, _vp] + [_i] * 7 + [_plan_p, _vp, _vp], _i),
     "ilpm_conv2d_fwd_epilogue": ([_vp, _vp, _vp] + [_i] * 8 + [_plan_p, _vp, _vp], _i),
     "ilpm_conv2d_epilogue_workspace_size": ([_i] * 8 + [_plan_p, ctypes.POINTER(ctypes.c_size_t)], _i),
+    "ilpm_winograd_filter_size": ([_i, _i, ctypes.POINTER(ctypes.c_size_t)], _i),
+    "ilpm_winograd_transform_filter": ([_vp, _i, _i, _vp, _vp], _i),
+    "ilpm_conv2d_winograd_workspace_size": ([_i] * 5 + [ctypes.POINTER(ctypes.c_size_t)], _i),
+    "ilpm_conv2d_fwd_winograd": ([_vp, _vp, _vp] + [_i] * 5 + [_vp, _vp], _i),
     "ilpm_relu_inplace": ([_vp, ctypes.c_int64, _vp], _i),
     "ilpm_maxpool2x2": ([_vp, _i, _i, _i, _vp, _vp], _i),
 }
@@ -346,6 +350,47 @@ def conv2d_epilogue_launcher(x, w, bias, stride, pad, epilogue, out, stream=None
         rc = fwd(*args)
         if rc != OK:
             raise IlpmError(rc, "ilpm_conv2d_fwd_epilogue")
+    return launch
+
+
+def winograd_transform_filter(w, stream=None):
+    """U = G g G^T of 3x3 weights [C_out, C_in, 3, 3] as a [16, C_out, C_in] CUDA tensor."""
+    torch = _torch()
+    if w.dim() != 4 or w.shape[2] != 3 or w.shape[3] != 3:
+        raise ValueError("w must be [C_out, C_in, 3, 3]")
+    c_out, c_in = w.shape[0], w.shape[1]
+    u = torch.empty((16, c_out, c_in), device=w.device, dtype=torch.float32)
+    _check(lib.ilpm_winograd_transform_filter(_dev_f32(w, "w"), c_in, c_out, _dev_f32(u, "u"),
+                                              _stream_handle(stream)), "ilpm_winograd_transform_filter")
+    return u
+
+
+def conv2d_winograd(x, u, bias=None, pad: int = 1, out=None, stream=None):
+    """3x3 / stride-1 conv2d by Winograd F(2x2,3x3) from transformed weights u [16, C_out, C_in]."""
+    torch = _torch()
+    _, c_in, h, wd = x.shape
+    c_out = u.shape[1]
+    ho, wo = out_size(h, 3, 1, pad), out_size(wd, 3, 1, pad)
+    if out is None:
+        out = torch.empty((1, c_out, max(ho, 1), max(wo, 1)), device=x.device, dtype=torch.float32)
+    _check(lib.ilpm_conv2d_fwd_winograd(_dev_f32(x, "x"), _dev_f32(u, "u"),
+                                        _dev_f32(bias, "bias") if bias is not None else None,
+                                        c_in, h, wd, c_out, pad, _dev_f32(out, "out"), _stream_handle(stream)),
+           "ilpm_conv2d_fwd_winograd")
+    return out
+
+
+def conv2d_winograd_launcher(x, u, bias, pad, out, stream=None):
+    _, c_in, h, wd = x.shape
+    c_out = u.shape[1]
+    args = (_dev_f32(x, "x"), _dev_f32(u, "u"), _dev_f32(bias, "bias") if bias is not None else None,
+            c_in, h, wd, c_out, pad, _dev_f32(out, "out"), _stream_handle(stream))
+    fwd = lib.ilpm_conv2d_fwd_winograd
+
+    def launch():
+        rc = fwd(*args)
+        if rc != OK:
+            raise IlpmError(rc, "ilpm_conv2d_fwd_winograd")
     return launch
 
 

@@ -486,6 +486,66 @@ int ilpm_conv2d_fwd_epilogue(const float *in, const float *w, const float *bias,
     return run(in, w, bias, s, out, p, stream, false, epilogue);
 }
 
+int ilpm_winograd_filter_size(int C_in, int C_out, size_t *bytes)
+{
+    if (!bytes || C_in <= 0 || C_out <= 0 || (int64_t)C_out * C_in * 16 > kMaxElems) return ILPM_ERR_INVALID_ARG;
+    *bytes = sizeof(float) * 16 * (size_t)C_out * C_in;
+    return ILPM_OK;
+}
+
+int ilpm_winograd_transform_filter(const float *w, int C_in, int C_out, float *u, hipStream_t stream)
+{
+    size_t ub = 0;
+    int rc = ilpm_winograd_filter_size(C_in, C_out, &ub);
+    if (rc != ILPM_OK) return rc;
+    if (!w || !u || (((uintptr_t)w | (uintptr_t)u) & 3u)) return ILPM_ERR_INVALID_ARG;
+    if (overlaps(w, sizeof(float) * 9 * (size_t)C_out * C_in, u, ub)) return ILPM_ERR_INVALID_ARG;
+    int dev = 0;
+    rc = device_check(&dev);
+    if (rc != ILPM_OK) return rc;
+    (void)hipGetLastError();
+    const hipError_t e = winograd_filter_launch(w, C_in, C_out, u, stream);
+    return e == hipSuccess ? ILPM_OK : hip_fail(e);
+}
+
+int ilpm_conv2d_winograd_workspace_size(int C_in, int H, int W, int C_out, int pad, size_t *bytes)
+{
+    if (!bytes) return ILPM_ERR_INVALID_ARG;
+    ConvShape s;
+    int rc = check_dims(C_in, H, W, C_out, 3, 1, pad, &s);
+    if (rc != ILPM_OK) return rc;
+    *bytes = winograd_workspace_bytes(s);
+    return ILPM_OK;
+}
+
+int ilpm_conv2d_fwd_winograd(const float *in, const float *u, const float *bias, int C_in, int H, int W, int C_out,
+                             int pad, float *out, hipStream_t stream)
+{
+    ConvShape s;
+    int rc = check_dims(C_in, H, W, C_out, 3, 1, pad, &s);
+    if (rc != ILPM_OK) return rc;
+    if (!in || !u || !out) return ILPM_ERR_INVALID_ARG;
+    if (((uintptr_t)in | (uintptr_t)u | (uintptr_t)out | (uintptr_t)bias) & 3u) return ILPM_ERR_INVALID_ARG;
+    const size_t in_b = sizeof(float) * (size_t)C_in * H * W, u_b = sizeof(float) * 16 * (size_t)C_out * C_in;
+    const size_t o_b = sizeof(float) * (size_t)C_out * s.h_out * s.w_out, b_b = sizeof(float) * (size_t)C_out;
+    if (overlaps(out, o_b, in, in_b) || overlaps(out, o_b, u, u_b) || overlaps(out, o_b, bias, b_b))
+        return ILPM_ERR_INVALID_ARG;
+    // Offsets and the library GEMM's sizes are 32-bit.
+    const int64_t t = winograd_tiles(s);
+    if (16 * (int64_t)C_in * t > kMaxElems || 16 * (int64_t)C_out * t > kMaxElems) return ILPM_ERR_UNSUPPORTED;
+    int dev = 0;
+    rc = device_check(&dev);
+    if (rc != ILPM_OK) return rc;
+    void *ws = nullptr;
+    rc = get_workspace(dev, winograd_workspace_bytes(s), &ws);
+    if (rc != ILPM_OK) return rc;
+    (void)hipGetLastError();
+    hipError_t e;
+    rc = winograd_launch(s, in, u, bias, out, ws, dev, stream, &e);
+    if (rc == ILPM_ERR_HIP && e != hipSuccess) return hip_fail(e);
+    return rc;
+}
+
 int ilpm_relu_inplace(float *x, int64_t n, hipStream_t stream)
 {
     if (n < 0 || (!x && n > 0) || ((uintptr_t)x & 3u)) return ILPM_ERR_INVALID_ARG;

@@ -45,6 +45,14 @@ size_t igemm_workspace_bytes(const ilpm_plan &p, const ConvShape &s, int epilogu
 int64_t igemm_packed_floats(const ilpm_plan &p, int c_in, int c_out);
 hipError_t igemm_pack(const ilpm_plan &p, int c_in, int c_out, const float *w, float *packed, hipStream_t stream);
 
+// ---- Winograd F(2x2, 3x3) comparison path (3x3, stride 1) ----
+int64_t winograd_tiles(const ConvShape &s);
+// V and M of the transformed problem (the filter transform U is the caller's).
+size_t winograd_workspace_bytes(const ConvShape &s);
+hipError_t winograd_filter_launch(const float *w, int c_in, int c_out, float *u, hipStream_t stream);
+int winograd_launch(const ConvShape &s, const float *x, const float *u, const float *bias, float *out,
+                    void *workspace, int dev, hipStream_t stream, hipError_t *err);
+
 // ---- measured plan table (tuned_plans.inc) ----
 // The plan the offline sweep found fastest for this exact shape, if any.
 bool tuned_plan(const ConvShape &s, ilpm_plan *p);

@@ -228,3 +228,20 @@ def test_epilogue_workspace_size():
         assert ilpm.epilogue_workspace_size(*shape, 0) == plan.workspace_bytes
         assert ilpm.epilogue_workspace_size(*shape, ilpm.EPI_RELU) == plan.workspace_bytes
         assert ilpm.epilogue_workspace_size(*shape, ilpm.EPI_MAXPOOL2) == full * max(plan.splits, 1)
+
+
+def test_winograd_sizes_and_argument_checks():
+    import ctypes
+    n = ctypes.c_size_t()
+    assert ilpm.lib.ilpm_winograd_filter_size(64, 128, ctypes.byref(n)) == ilpm.OK and n.value == 16 * 64 * 128 * 4
+    assert ilpm.lib.ilpm_winograd_filter_size(0, 128, ctypes.byref(n)) == ilpm.ERR_INVALID_ARG
+    assert ilpm.lib.ilpm_conv2d_winograd_workspace_size(64, 224, 224, 64, 1, ctypes.byref(n)) == ilpm.OK
+    assert n.value == 4 * 16 * (64 + 64) * 112 * 112
+    # odd output: 9x11 with pad 1 -> 5x6 tiles
+    assert ilpm.lib.ilpm_conv2d_winograd_workspace_size(3, 9, 11, 2, 1, ctypes.byref(n)) == ilpm.OK
+    assert n.value == 4 * 16 * (3 + 2) * 5 * 6
+    lib = ilpm.lib
+    assert lib.ilpm_conv2d_fwd_winograd(None, 0x100000, None, 3, 8, 8, 4, 1, 0x200000, None) == ilpm.ERR_INVALID_ARG
+    assert lib.ilpm_conv2d_fwd_winograd(0x1002, 0x100000, None, 3, 8, 8, 4, 1, 0x200000, None) == ilpm.ERR_INVALID_ARG
+    assert lib.ilpm_conv2d_fwd_winograd(0x1000, 0x100000, None, 3, 1, 8, 4, 0, 0x200000, None) == ilpm.ERR_INVALID_ARG
+    assert lib.ilpm_winograd_transform_filter(0x1000, 3, 4, 0x1000 + 64, None) == ilpm.ERR_INVALID_ARG  # overlap
