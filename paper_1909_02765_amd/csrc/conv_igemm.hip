@@ -930,6 +930,7 @@ const Variant kVariants[] = {
     make_variant<Cfg<3, 1, 14, 14, 4, 1, 2, 1, 16>>("k3s1_t14x14_co64_w8_cc16"),
     make_variant<Cfg<3, 1, 14, 14, 4, 1, 1, 1, 16>>("k3s1_t14x14_co64_cc16"),
     make_variant<Cfg<3, 1, 14, 14, 4, 1, 1, 2, 8>>("k3s1_t14x14_co128"),
+    make_variant<Cfg<3, 1, 14, 14, 2, 1, 2, 1, 8>>("k3s1_t14x14_co32_k2"),
     make_variant<Cfg<3, 1, 7, 7, 4, 1, 1, 1, 8>>("k3s1_t7x7_co64"),
     make_variant<Cfg<3, 1, 7, 7, 4, 1, 4, 1, 16>>("k3s1_t7x7_co64_k4"),
     make_variant<Cfg<3, 1, 8, 32, 2, 2, 1, 2, 8>>("k3s1_t8x32_co64"),
