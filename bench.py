@@ -140,6 +140,28 @@ def time_prepacked(torch, ilpm, x, w, b, s, p, out, plan, steps, warmup):
     return start.elapsed_time(stop) * 1000.0 / steps
 
 
+def time_cold(torch, ilpm, x, w, b, s, p, out, reps=20, scrub_mib=512):
+    """Median µs of `reps` individually timed calls, each after a 512 MiB
+    write that evicts the inputs, weights and output from L2 and the
+    last-level cache (so every byte the call moves comes from or goes to
+    HBM)."""
+    launch = ilpm.conv2d_launcher(x, w, b, s, p, out)
+    scrub = torch.empty(scrub_mib << 18, device="cuda", dtype=torch.float32)
+    launch()
+    times = []
+    for i in range(reps):
+        scrub.fill_(float(i))
+        a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        launch()
+        e.record()
+        torch.cuda.synchronize()
+        times.append(a.elapsed_time(e) * 1000.0)
+    del scrub
+    times.sort()
+    return times[len(times) // 2]
+
+
 def time_winograd(torch, ilpm, x, w, b, p, out, steps, warmup):
     """Mean µs per call of the Winograd F(2x2,3x3) comparison path (filter
     transform done once beforehand), or None when it cannot run here."""
@@ -179,10 +201,29 @@ def cpu_baseline(case, x, w, b, y_gpu):
         elapsed += time.perf_counter() - t0
         reps += 1
     ok, ratio, _ = oracle.check(y_gpu, ref, sab, case.c_in, case.k)
+    # the same oracle on one thread, one run
+    oracle.set_threads(1)
+    t0 = time.perf_counter()
+    oracle.conv2d_f64(x, w, b, case.stride, case.pad)
+    one = time.perf_counter() - t0
+    oracle.set_threads(used)
     return {"value": round(flops * reps / elapsed / 1e9, 3), "unit": "GFLOP/s", "cores": used,
             "kind": "oracle",
             "sample": f"whole layer, {reps} run(s), fp64 seven-loop oracle, {elapsed:.2f} s",
+            "one_thread_gflops": round(flops / one / 1e9, 3),
+            "host_cpu": _cpu_model(), "host_threads": os.cpu_count(),
             "parity_max_tol_ratio": round(ratio, 4), "parity_ok": bool(ok)}
+
+
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def measure_peaks(torch):
@@ -246,6 +287,7 @@ def bench_case(torch, ilpm, case, steps, warmup, graph=False):
         res["graph_us"] = time_layer_graph(torch, ilpm, xd, wd, bd, case.stride, case.pad, out, steps)
         res["prepacked_us"] = time_prepacked(torch, ilpm, xd, wd, bd, case.stride, case.pad, out, plan, steps,
                                              warmup)
+        res["cold_us"] = time_cold(torch, ilpm, xd, wd, bd, case.stride, case.pad, out)
         if case.k == 3 and case.stride == 1:
             out_w = torch.empty_like(out)
             res["winograd_us"] = time_winograd(torch, ilpm, xd, wd, bd, case.pad, out_w, steps, warmup)
@@ -341,7 +383,8 @@ def main():
             rr = bench_case(torch, ilpm, c, max(200, args.steps // 4), 200, graph=True)
             fl, kind = roofline_floor_us(rr["flops"], rr["nbytes"])
             rows.append({"layer": c.name, "us": round(rr["us"], 3), "graph_us": round(rr["graph_us"], 3),
-                         "prepacked_us": round(rr["prepacked_us"], 3),
+                         "prepacked_us": round(rr["prepacked_us"], 3), "cold_us": round(rr["cold_us"], 3),
+                         "cold_hbm_gbs": round(rr["nbytes"] / rr["cold_us"] / 1e3, 1),
                          "winograd_us": (round(rr["winograd_us"], 3) if rr.get("winograd_us") is not None
                                          else None),
                          "gflops": round(rr["flops"] / rr["us"] / 1e3, 1),
