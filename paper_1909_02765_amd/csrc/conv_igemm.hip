@@ -79,8 +79,17 @@ struct Cfg {
     static constexpr int KK = KS * KS;
     static constexpr int HR = (TH - 1) * S + KS;
     static constexpr int HC = (TW - 1) * S + KS;
-    static constexpr int HCP = halo_row(HR, HC, S);
-    static constexpr int PL = HR * HCP;
+    // A 16-column halo (14-wide tiles, 3x3, stride 1) is stored unpadded, 16
+    // words a row, so one DMA instruction fills four whole rows of one channel
+    // and a wave always fills the same four rows (QUAD): its lanes' offsets are
+    // computed once and stepped by a channel plane.  (The unpadded rows put
+    // the four channel groups of an MFMA step on the same LDS banks; the
+    // matrix-core loop runs at full rate with that pattern all the same.)
+    static constexpr bool QUAD = S == 1 && HC == 16 && HR == 16 && NW % 4 == 0;
+    static constexpr int HCP = QUAD ? 16 : halo_row(HR, HC, S);
+    // Channel plane stride in LDS.  QUAD pads each plane by 16 words so that
+    // the four channel groups of an MFMA step fall on different LDS banks.
+    static constexpr int PL = HR * HCP + (QUAD ? 16 : 0);
     static constexpr int COT = NWC * 16 * MA;
     // A tile of 16*q + t pixels, t in 1..4, computes its last pixel block with
     // the 4x4x1 matrix instruction (16 blocks of 4 channels x 4 pixels, one k
@@ -102,8 +111,11 @@ struct Cfg {
     // One stage buffer: the halo, a whole number of 64-word rows (one DMA
     // instruction each).
     static constexpr int XSZ = round64(CC * PL);
-    static constexpr int NIX = XSZ / 64;
+    // DMA instructions per stage: QUAD, four per channel (rows 4q..4q+3 of
+    // channel c to LDS word c*PL + 64q); otherwise one per 64 LDS words.
+    static constexpr int NIX = QUAD ? CC * HR / 4 : XSZ / 64;
     static constexpr int XPT = (NIX + NW - 1) / NW;  // DMA instructions per wave
+    __device__ static constexpr int dma_dst(int e) { return QUAD ? (e / (HR / 4)) * PL + (e % (HR / 4)) * 64 : e * 64; }
     // LDS for the cross-wave sum of the NWK partial accumulators.
     static constexpr int RED = (NWK - 1) * NWC * NWP * MA * NB * 4 * 64;
     static constexpr int BUF0 = cmax(XSZ, RED);
@@ -287,16 +299,30 @@ template <class C>
 __device__ __forceinline__ void halo_offsets(int (&xo)[C::XPT], const IgArgs &a, int wave, int lane, int ih0,
                                              int iw0)
 {
+    if constexpr (C::QUAD) {
+        // Instruction j of wave w covers channel (j*NW + w)/4, rows 4q..4q+3
+        // with q = w % 4: lane l at row 4q + l/16, column l % 16.
+        const int ih = ih0 + 4 * (wave % 4) + (lane >> 4), iw = iw0 + (lane & 15);
+        const bool ok = ih >= 0 && ih < a.h && iw >= 0 && iw < a.w;
+        const unsigned base = (unsigned)(ih * a.w + iw) * 4u;
+        const unsigned plane = (unsigned)a.h * (unsigned)a.w * 4u;
 #pragma unroll
-    for (int j = 0; j < C::XPT; ++j) {
-        const int e = (j * C::NW + wave) * 64 + lane;
-        const int c = e / C::PL;
-        const int rem = e - c * C::PL;
-        const int r = rem / C::HCP;
-        const int col = rem - r * C::HCP;
-        const int ih = ih0 + r, iw = iw0 + col;
-        const bool ok = c < C::CC && col < C::HC && ih >= 0 && ih < a.h && iw >= 0 && iw < a.w;
-        xo[j] = ok ? ((c * a.h + ih) * a.w + iw) * 4 : kOutOfRange;
+        for (int j = 0; j < C::XPT; ++j) {
+            const unsigned c = (unsigned)((j * C::NW + wave) / 4);
+            xo[j] = ok ? (int)(base + c * plane) : kOutOfRange;
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < C::XPT; ++j) {
+            const int e = (j * C::NW + wave) * 64 + lane;
+            const int c = e / C::PL;
+            const int rem = e - c * C::PL;
+            const int r = rem / C::HCP;
+            const int col = rem - r * C::HCP;
+            const int ih = ih0 + r, iw = iw0 + col;
+            const bool ok = c < C::CC && col < C::HC && ih >= 0 && ih < a.h && iw >= 0 && iw < a.w;
+            xo[j] = ok ? ((c * a.h + ih) * a.w + iw) * 4 : kOutOfRange;
+        }
     }
 }
 
@@ -311,10 +337,11 @@ __device__ __forceinline__ void dma_halo(float *buf, const float *__restrict__ x
     constexpr int kFull = C::NIX / C::NW;  // rounds in which every wave issues one
 #pragma unroll
     for (int j = 0; j < kFull; ++j)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_ptr_t)(buf + (j * C::NW + wave) * 64), 4, xo[j], 0, 0, 0);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_ptr_t)(buf + C::dma_dst(j * C::NW + wave)), 4, xo[j], 0, 0,
+                                                 0);
     if constexpr (kFull < C::XPT) {
         if (kFull * C::NW + wave < C::NIX)
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_ptr_t)(buf + (kFull * C::NW + wave) * 64), 4,
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_ptr_t)(buf + C::dma_dst(kFull * C::NW + wave)), 4,
                                                      xo[kFull], 0, 0, 0);
     }
 }
@@ -352,10 +379,10 @@ struct NextStage {
     {
         if (i < ND) {
             if (i < kFull) {
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_ptr_t)(buf + (i * C::NW + wave) * 64), 4, xo[i], 0,
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_ptr_t)(buf + C::dma_dst(i * C::NW + wave)), 4, xo[i], 0,
                                                          0, 0);
             } else if (kFull * C::NW + wave < C::NIX) {
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_ptr_t)(buf + (kFull * C::NW + wave) * 64), 4,
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_ptr_t)(buf + C::dma_dst(kFull * C::NW + wave)), 4,
                                                          xo[kFull], 0, 0, 0);
             }
             return;
@@ -715,6 +742,16 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
     wctx.block0 = (co_t * a.nchunks * C::NWK + wk) * C::NWC + wc;
     wctx.lane = lane;
 
+    // The first stage's loads go out before the rest of the set-up: with one
+    // wave per SIMD every vector instruction of the set-up costs its full
+    // issue time, so it runs while the loads are in flight.
+    int xo[C::XPT];
+    halo_offsets<C>(xo, a, wave, lane, ih0, iw0);
+    AStage<C> a0, a1;
+    dma_halo<C>(lds0, x, a, c_begin * C::CC, wave, xo);
+    load_a<C>(a0, WS(wctx, a.c_out, c_begin * C::CC));
+    __builtin_amdgcn_sched_barrier(0);
+
     // Input operand: LDS base of each pixel block for this lane.
     int b_base[C::NB];
 #pragma unroll
@@ -742,11 +779,6 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
     Epilogue<C> ep;
     ep.init(a, out, part, bias, split, co0 + wc * 16 * C::MA + 4 * g, wp, g, l16, oh0, ow0);
 
-    int xo[C::XPT];
-    halo_offsets<C>(xo, a, wave, lane, ih0, iw0);
-    AStage<C> a0, a1;
-    dma_halo<C>(lds0, x, a, c_begin * C::CC, wave, xo);
-    load_a<C>(a0, WS(wctx, a.c_out, c_begin * C::CC));
     stage_ready();
 
     for (int ch = c_begin;; ch += 2) {
@@ -931,6 +963,8 @@ const Variant kVariants[] = {
     make_variant<Cfg<3, 1, 14, 14, 4, 1, 1, 1, 16>>("k3s1_t14x14_co64_cc16"),
     make_variant<Cfg<3, 1, 14, 14, 4, 1, 1, 2, 8>>("k3s1_t14x14_co128"),
     make_variant<Cfg<3, 1, 14, 14, 2, 1, 2, 1, 8>>("k3s1_t14x14_co32_k2"),
+    make_variant<Cfg<3, 1, 14, 14, 4, 1, 1, 1, 4>>("k3s1_t14x14_co64_cc4"),
+    make_variant<Cfg<3, 1, 7, 7, 4, 1, 1, 1, 4>>("k3s1_t7x7_co64_cc4"),
     make_variant<Cfg<3, 1, 7, 7, 4, 1, 1, 1, 8>>("k3s1_t7x7_co64"),
     make_variant<Cfg<3, 1, 7, 7, 4, 1, 4, 1, 16>>("k3s1_t7x7_co64_k4"),
     make_variant<Cfg<3, 1, 8, 32, 2, 2, 1, 2, 8>>("k3s1_t8x32_co64"),
