@@ -1,7 +1,7 @@
 // Implicit-GEMM convolution on the fp32 matrix cores (v_mfma_f32_16x16x4_f32).
 //
 // The convolution is the product D = A * B with
-//   A [C_out x C_in*K*K]  = the OIHW weights, read as they are,
+//   A [C_out x C_in*K*K]  = the weights (OIHW as they are, or prepacked),
 //   B [C_in*K*K x pixels] = input patches, never materialised: every B element
 //                           is read from a zero-padded input halo tile in LDS,
 //   D [C_out x pixels]    = the NCHW output.
@@ -13,7 +13,9 @@
 //    output channel straight from global memory into registers, the paper's
 //    filter_reg, with no shared-memory copy of the weights.  In OIHW the K*K
 //    taps of one (output, input) channel pair are contiguous, so a lane
-//    fetches them with 16-byte loads.  They are loaded one stage ahead.
+//    fetches them with 16-byte loads; the prepacked layout makes every such
+//    load instruction of a wave one contiguous kilobyte.  They are loaded one
+//    stage ahead, a few instructions per step of the current stage.
 //  * The input tile is staged once in LDS for the whole workgroup, by DMA
 //    (buffer loads that write LDS directly), and read by every wavefront:
 //    lanes own output pixels for the B operand.
@@ -33,16 +35,15 @@
 // accumulators of a tile are summed through LDS at the end.
 //
 // Work split across workgroups: output tiles (TH x TW pixels x COT channels)
-// and, optionally, `splits` contiguous ranges of input-channel stages (grid
-// y).  With splits > 1 each workgroup writes its partial output, in the
-// output's own layout, to slice `split` of the workspace, and a second kernel
-// sums the slices in split order and adds the bias, so the result does not
-// depend on the order in which workgroups run.
+// and, optionally, `splits` contiguous ranges of input-channel stages.  With
+// splits > 1 (or a pooled epilogue) each workgroup writes its partial output,
+// in the output's own layout, to slice `split` of the workspace, and a second
+// kernel sums the slices in split order and applies bias, ReLU and the pool,
+// so the result does not depend on the order in which workgroups run.
 //
 // LDS: two stage buffers of the halo [CC][HR][HCP] -- (TH-1)*S+K rows of
-// (TW-1)*S+K pixels, rows padded to HCP words so that consecutive channel
-// planes start on different bank halves (plane = 16 mod 32 words for odd
-// strides, an odd word count for even strides).
+// (TW-1)*S+K pixels -- laid out so that the four channel groups of a step
+// read different banks (see Cfg).
 #include <cmath>
 #include <type_traits>
 
@@ -79,17 +80,16 @@ struct Cfg {
     static constexpr int KK = KS * KS;
     static constexpr int HR = (TH - 1) * S + KS;
     static constexpr int HC = (TW - 1) * S + KS;
-    // A 16-column halo (14-wide tiles, 3x3, stride 1) is stored unpadded, 16
-    // words a row, so one DMA instruction fills four whole rows of one channel
-    // and a wave always fills the same four rows (QUAD): its lanes' offsets are
-    // computed once and stepped by a channel plane.  (The unpadded rows put
-    // the four channel groups of an MFMA step on the same LDS banks; the
-    // matrix-core loop runs at full rate with that pattern all the same.)
+    // A 16 x 16 halo (14 x 14 tiles, 3x3, stride 1) is stored with unpadded
+    // 16-word rows, so one DMA instruction fills four whole rows of one
+    // channel and a wave always fills the same four rows (QUAD): its lanes'
+    // offsets are computed once and stepped by a channel plane.  Each plane
+    // is then padded by 16 words, which puts the four channel groups of an
+    // MFMA step on different LDS banks (with 256-word planes they share
+    // banks, and the stages run ~25% slower).  Other halos pad the rows.
     static constexpr bool QUAD = S == 1 && HC == 16 && HR == 16 && NW % 4 == 0;
     static constexpr int HCP = QUAD ? 16 : halo_row(HR, HC, S);
-    // Channel plane stride in LDS.  QUAD pads each plane by 16 words so that
-    // the four channel groups of an MFMA step fall on different LDS banks.
-    static constexpr int PL = HR * HCP + (QUAD ? 16 : 0);
+    static constexpr int PL = HR * HCP + (QUAD ? 16 : 0);  // channel plane stride
     static constexpr int COT = NWC * 16 * MA;
     // A tile of 16*q + t pixels, t in 1..4, computes its last pixel block with
     // the 4x4x1 matrix instruction (16 blocks of 4 channels x 4 pixels, one k
@@ -150,27 +150,6 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const float *base, u
     const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(b >> 32));
     float *p = reinterpret_cast<float *>(((uint64_t)hi << 32) | lo);
     return __builtin_amdgcn_make_buffer_rsrc(p, (short)0, (int)__builtin_amdgcn_readfirstlane(bytes), kBufferWord3);
-}
-
-// The KK contiguous floats at byte offset `off`, in 16-byte pieces.  (An
-// out-of-range `off` stays out of range for every piece: the sums are taken
-// unsigned and stay below 2^32.)
-template <int KK>
-__device__ __forceinline__ void load_taps(__amdgpu_buffer_rsrc_t r, int off, float (&dst)[KK])
-{
-    const unsigned base = (unsigned)off;
-#pragma unroll
-    for (int i = 0; i + 4 <= KK; i += 4) {
-        const floatx4 v =
-            __builtin_bit_cast(floatx4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)(base + 4u * i), 0, 0));
-        dst[i] = v[0];
-        dst[i + 1] = v[1];
-        dst[i + 2] = v[2];
-        dst[i + 3] = v[3];
-    }
-#pragma unroll
-    for (int i = KK / 4 * 4; i < KK; ++i)
-        dst[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, (int)(base + 4u * i), 0, 0));
 }
 
 // Weight registers of one stage for one lane: [m-block][channel group][tap].
