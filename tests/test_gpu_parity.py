@@ -281,3 +281,34 @@ def test_prepacked_ragged_channels(ilpm):
                 got = ilpm.conv2d_prepacked(dev(x), packed, c_out, k, dev(b), s, p, plan=plan)
                 torch.cuda.synchronize()
                 assert_matches(got.cpu().numpy(), ref, sab, c_in, k, f"prepacked ragged{seed} v{v}")
+
+
+def test_wide_channels_many_splits(ilpm):
+    """Channel counts that are not multiples of the stage size, split into
+    uneven ranges across many workgroups (the small-layer plans).  The values
+    follow the workloads' recipe (inputs uniform[0,1], He-normal weights):
+    with thousands of terms per output, weights of unit scale would make the
+    outputs large and the plain fp32 rounding of a long sum alone exceed the
+    tolerance, which is stated for that recipe."""
+    for j, (c_in, h, w_, c_out, k, s, p) in enumerate([(300, 9, 9, 200, 3, 1, 1), (513, 7, 7, 130, 1, 1, 0),
+                                                       (257, 12, 12, 96, 5, 1, 2), (190, 15, 13, 70, 3, 2, 1)]):
+        x = workloads.uniform(6100 + 10 * j, (1, c_in, h, w_), 0.0, 1.0)
+        w = workloads.normal(6101 + 10 * j, (c_out, c_in, k, k), 0.0, workloads.he_std(c_in, k))
+        b = workloads.normal(6102 + 10 * j, (c_out,), 0.0, 0.01) if j % 2 == 0 else None
+        ref, sab = oracle.conv2d_f64(x, w, b, s, p)
+        for v in range(ilpm.num_variants(ilpm.PATH_IGEMM)):
+            info = ilpm.variant_info(ilpm.PATH_IGEMM, v)
+            if info["k"] != k or info["stride"] != s:
+                continue
+            seen = set()
+            for splits in (1, 5, 7, 0, 64):
+                try:
+                    plan = ilpm.plan_variant(c_in, h, w_, c_out, k, s, p, ilpm.PATH_IGEMM, v, splits)
+                except ilpm.IlpmError:
+                    continue
+                if plan.splits in seen:
+                    continue
+                seen.add(plan.splits)
+                note(f"[wide {j}] v={v} {describe(plan)}")
+                got = run_conv(x, w, b, s, p, plan=plan)
+                assert_matches(got, ref, sab, c_in, k, f"wide {j} v={v} {describe(plan)}")
