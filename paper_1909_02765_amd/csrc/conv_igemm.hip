@@ -125,9 +125,31 @@ struct Cfg {
     static_assert(NT <= 1024, "workgroup size");
 };
 
+// Unsigned division by a divisor d >= 1 fixed at launch, for dividends below
+// 2^31: q = (mulhi(n, m) + n) >> l with l = ceil(log2 d) and
+// m = floor(2^32 (2^l - d) / d) + 1 (Granlund and Montgomery, "Division by
+// invariant integers using multiplication", 1994, Section 4).  The sum stays
+// below 2^32 because mulhi(n, m) < n.  Three scalar instructions instead of
+// the ~30 of a general division, which matter in a set-up issued by one wave
+// per SIMD.
+struct FastDiv {
+    unsigned d, m, l;
+};
+
+inline FastDiv make_fastdiv(unsigned d)
+{
+    unsigned l = 0;
+    while ((1ull << l) < d) ++l;
+    const uint64_t m = (((1ull << l) - d) << 32) / d + 1;
+    return FastDiv{d, (unsigned)m, l};
+}
+
+__device__ __forceinline__ unsigned fast_div(unsigned n, const FastDiv &f) { return (__umulhi(n, f.m) + n) >> f.l; }
+
 struct IgArgs {
     int c_in, h, w, c_out, pad, h_out, w_out;
-    int tiles_w, co_tiles, nchunks, chunks_per_split, splits;
+    int nchunks, chunks_per_split;
+    FastDiv ntiles, co_tiles, tiles_w;  // workgroup -> (split, output-channel tile, spatial tile)
     int to_part;  // write raw partial sums to slice `split` of the workspace (a finishing kernel follows)
     int relu;     // otherwise: store max(conv + bias, 0)
 };
@@ -183,15 +205,24 @@ struct OihwWeights {
 
     __device__ __forceinline__ OihwWeights(const WeightCtx &k, int c_out, int ci0) : rw(k.rw)
     {
+        // One row product per m-block, then additions: no branches, and only
+        // MA full 32-bit multiplies.
+        const unsigned row_b = (unsigned)k.c_in * (C::KK * 4u);
+        unsigned row[C::MA];
+        bool co_ok[C::MA];
+#pragma unroll
+        for (int m = 0; m < C::MA; ++m) {
+            const int co = k.co_lane0 + 16 * m;
+            co_ok[m] = co < c_out;
+            row[m] = (unsigned)co * row_b;
+        }
 #pragma unroll
         for (int c4 = 0; c4 < C::G4; ++c4) {
             const int ci = ci0 + k.ci_lane + 4 * C::NWK * c4;
 #pragma unroll
-            for (int m = 0; m < C::MA; ++m) {
-                const int co = k.co_lane0 + 16 * m;
-                a_base[c4][m] = (ci < k.c_in && co < c_out) ? (unsigned)((co * k.c_in + ci) * C::KK * 4)
-                                                             : (unsigned)kOutOfRange;
-            }
+            for (int m = 0; m < C::MA; ++m)
+                a_base[c4][m] =
+                    (ci < k.c_in && co_ok[m]) ? row[m] + (unsigned)ci * (C::KK * 4u) : (unsigned)kOutOfRange;
         }
     }
 
@@ -281,14 +312,16 @@ __device__ __forceinline__ void halo_offsets(int (&xo)[C::XPT], const IgArgs &a,
     if constexpr (C::QUAD) {
         // Instruction j of wave w covers channel (j*NW + w)/4, rows 4q..4q+3
         // with q = w % 4: lane l at row 4q + l/16, column l % 16.
+        // A lane outside the image starts at 2^31: plus any channel offset
+        // (below 2^31) it stays past every descriptor's range.
         const int ih = ih0 + 4 * (wave % 4) + (lane >> 4), iw = iw0 + (lane & 15);
         const bool ok = ih >= 0 && ih < a.h && iw >= 0 && iw < a.w;
-        const unsigned base = (unsigned)(ih * a.w + iw) * 4u;
+        const unsigned base = ok ? (unsigned)(ih * a.w + iw) * 4u : 0x80000000u;
         const unsigned plane = (unsigned)a.h * (unsigned)a.w * 4u;
 #pragma unroll
         for (int j = 0; j < C::XPT; ++j) {
             const unsigned c = (unsigned)((j * C::NW + wave) / 4);
-            xo[j] = ok ? (int)(base + c * plane) : kOutOfRange;
+            xo[j] = (int)(base + c * plane);
         }
     } else {
 #pragma unroll
@@ -397,42 +430,55 @@ __device__ __forceinline__ void read_b(const float *xl, const int (&b_base)[C::N
 }
 
 // One stage of MFMA work for one wave: every tap, this wave's channel groups,
-// all MA x NB accumulator blocks.  The B fragments are software pipelined by
-// one step: the LDS reads of step s+1 are issued before the matrix
-// instructions of step s, and scheduling barriers keep the compiler from
-// sinking them -- a wave issues in order, so reads placed behind a run of
-// MFMAs would only start once the whole run had issued, leaving the matrix
-// pipe to wait on them.
+// all MA x NB accumulator blocks.  The B fragments are software pipelined:
+// the LDS reads of step s+D are issued before the matrix instructions of
+// step s, and scheduling barriers keep the compiler from sinking them -- a
+// wave issues in order, so reads placed behind a run of MFMAs would only
+// start once the whole run had issued, leaving the matrix pipe to wait on
+// them.  D is one step when a step has three or more matrix instructions
+// (their 96+ cycles cover an LDS read); waves with one or two blocks per
+// step read two or four steps ahead.
+template <class C>
+struct BPipe {
+    static constexpr int kMf = C::MA * C::NBM;
+    static constexpr int kSteps = C::KK * C::G4;
+    static constexpr int kWant = kMf >= 3 ? 1 : (kMf == 2 ? 2 : 4);
+    static constexpr int D = kWant < kSteps ? kWant : (kSteps > 1 ? kSteps - 1 : 1);
+    static constexpr int R = D + 1;  // ring slots
+};
+
 template <class C, class P>
 __device__ __forceinline__ void compute_stage(const float *xl, const AStage<C> &A, const int (&b_base)[C::NB],
                                               floatx4 (&acc)[C::MA][C::NACC], P &next)
 {
     constexpr int kSteps = C::KK * C::G4;
+    constexpr int D = BPipe<C>::D, R = BPipe<C>::R;
     // Next-stage loads per step: all of them within the first half.
     constexpr int kHalf = kSteps / 2 > 0 ? kSteps / 2 : 1;
     constexpr int kRate = P::N == 0 ? 1 : (P::N + kHalf - 1) / kHalf;
-    float bv[2][C::NB];
+    float bv[R][C::NB];
     float tb[C::TAIL4 ? kSteps : 1];
-    read_b<C>(xl, b_base, 0, bv[0]);
+#pragma unroll
+    for (int s = 0; s < D && s < kSteps; ++s) read_b<C>(xl, b_base, s, bv[s]);
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int st = 0; st < kSteps; ++st) {
-        const int cur = st & 1;
+        const int cur = st % R;
         const int t = st / C::G4, c4 = st % C::G4;
 #pragma unroll
         for (int r = 0; r < kRate; ++r)
             if (st * kRate + r < P::N) next.issue(st * kRate + r);
-        if (st + 1 < kSteps) read_b<C>(xl, b_base, st + 1, bv[cur ^ 1]);
+        if (st + D < kSteps) read_b<C>(xl, b_base, st + D, bv[(st + D) % R]);
 #pragma unroll
         for (int m = 0; m < C::MA; ++m)
 #pragma unroll
             for (int n = 0; n < C::NBM; ++n)
                 acc[m][n] = __builtin_amdgcn_mfma_f32_16x16x4f32(A.v[m][c4][t], bv[cur][n], acc[m][n], 0, 0, 0);
         if constexpr (C::TAIL4) tb[st] = bv[cur][C::NB - 1];
-        // Within the step: one matrix instruction, then one read of the next
+        // Within the step: one matrix instruction, then one read of a later
         // step, so the reads issue while the matrix pipe is busy.
         constexpr int kMf = C::MA * C::NBM;
-        const int n_ds = st + 1 < kSteps ? C::NB : 0;
+        const int n_ds = st + D < kSteps ? C::NB : 0;
 #pragma unroll
         for (int i = 0; i < (kMf > C::NB ? kMf : C::NB); ++i) {
             if (i < kMf) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
@@ -475,7 +521,6 @@ struct Epilogue {
     // the first 16 stores channels tail_co + 16*m + r, r = 0..3, at pixel j.
     int tail_co, c_out, relu;
     unsigned tail_pix, plane_b;
-    float tail_b[C::MA][4];
 
     __device__ __forceinline__ float fin(float v) const { return relu && v < 0.f ? 0.f : v; }
 
@@ -488,70 +533,87 @@ struct Epilogue {
         relu = a.to_part ? 0 : a.relu;
         const unsigned out_b = (unsigned)a.c_out * plane_b;
         ro = make_rsrc(a.to_part ? part + (size_t)split * (out_b / 4) : out, out_b);
+        // Output rows and columns left from this tile's corner (wave-uniform);
+        // image sizes below 2^23 (checked with the plan) make the 24-bit
+        // multiplies exact.
+        const int rows = a.h_out - oh0, cols = a.w_out - ow0;
+        const unsigned obase = (unsigned)(oh0 * a.w_out + ow0) * 4u;
 #pragma unroll
         for (int n = 0; n < C::NB; ++n) {
             const int p = (wp * C::NB + n) * 16 + l16;
-            const int oh = oh0 + p / C::TW, ow = ow0 + p % C::TW;
-            pix_off[n] = (p < C::NPIX && oh < a.h_out && ow < a.w_out) ? (unsigned)(oh * a.w_out + ow) * 4u : kFar;
+            const int q = p / C::TW, r = p - q * C::TW;
+            const bool ok = p < C::NPIX && q < rows && r < cols;
+            pix_off[n] = ok ? obase + (unsigned)(__mul24(q, a.w_out) + r) * 4u : kFar;
         }
 #pragma unroll
         for (int m = 0; m < C::MA; ++m)
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int co = co_lane + 16 * m + r;
-                const bool ok = co < a.c_out;
-                b[m][r] = (!a.to_part && bias && ok) ? bias[co] : 0.f;
-                chan_off[m][r] = ok ? (unsigned)co * plane_b : kFar;
+                chan_off[m][r] = co < a.c_out ? (unsigned)co * plane_b : kFar;
+                b[m][r] = 0.f;
             }
+        // A lane's channels past C_out never store, so their bias is read
+        // from the last channel instead of being masked.
+        if (!a.to_part && bias != nullptr) {
+#pragma unroll
+            for (int m = 0; m < C::MA; ++m)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) b[m][r] = bias[min(co_lane + 16 * m + r, a.c_out - 1)];
+        }
         if constexpr (C::TAIL4) {
             // co_lane = co_base + 4*g; the tail uses co_base + 4*cg, cg = l16/4.
             tail_co = co_lane - 4 * g + 4 * (l16 >> 2);
             const int j = l16 & 3;
             const int p = (C::NB - 1) * 16 + j;
-            const int oh = oh0 + p / C::TW, ow = ow0 + p % C::TW;
-            const bool lane_stores = g == 0 && j < C::TAILP && oh < a.h_out && ow < a.w_out;
-            tail_pix = lane_stores ? (unsigned)(oh * a.w_out + ow) * 4u : kFar;
-#pragma unroll
-            for (int m = 0; m < C::MA; ++m)
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int co = tail_co + 16 * m + r;
-                    tail_b[m][r] = (!a.to_part && bias && co < a.c_out) ? bias[co] : 0.f;
-                }
+            const int q = p / C::TW, r = p - q * C::TW;
+            const bool lane_stores = g == 0 && j < C::TAILP && q < rows && r < cols;
+            tail_pix = lane_stores ? obase + (unsigned)(__mul24(q, a.w_out) + r) * 4u : kFar;
         }
+    }
+
+    // Row r of 16x16 block (m, n).
+    __device__ __forceinline__ void store_one(int m, int n, int r, float v) const
+    {
+        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, fin(v + b[m][r])), ro,
+                                              (int)(chan_off[m][r] + pix_off[n]), 0, 0);
+    }
+
+    // Row r of the 4x4x1 tail block of m-block m: sum the four k-slice
+    // partials, lane l getting (v[l] + v[l^16]) + (v[l^32] + v[l^48]) for
+    // the first 16 lanes; lane 4*cg + j stores the channels that lanes
+    // 16*cg.. hold the bias of.
+    __device__ __forceinline__ void store_tail_one(int m, int r, float v) const
+    {
+        constexpr unsigned kFar = 1u << 30;
+        const int src = 16 * ((__lane_id() & 15) >> 2);
+        float s = v + __shfl_xor(v, 16);
+        s += __shfl_xor(s, 32);
+        const float tb = __shfl(b[m][r], src);
+        const int co = tail_co + 16 * m + r;
+        const unsigned off = (co < c_out && tail_pix < kFar) ? (unsigned)co * plane_b + tail_pix : kFar;
+        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, fin(s + tb)), ro, (int)off, 0, 0);
     }
 
     __device__ __forceinline__ void store(int m, int n, const floatx4 &v) const
     {
-        if (C::TAIL4 && n == C::NB - 1) {
-            // Sum the four k-slice partials: lane l gets (v[l] + v[l^16]) +
-            // (v[l^32] + v[l^48]) for the first 16 lanes.
-            constexpr unsigned kFar = 1u << 30;
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                float s = v[r] + __shfl_xor(v[r], 16);
-                s += __shfl_xor(s, 32);
-                const int co = tail_co + 16 * m + r;
-                const unsigned off = (co < c_out && tail_pix < kFar) ? (unsigned)co * plane_b + tail_pix : kFar;
-                __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, fin(s + tail_b[m][r])), ro,
-                                                      (int)off, 0, 0);
-            }
-            return;
+        for (int r = 0; r < 4; ++r) {
+            if (C::TAIL4 && n == C::NB - 1) store_tail_one(m, r, v[r]);
+            else store_one(m, n, r, v[r]);
         }
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, fin(v[r] + b[m][r])), ro,
-                                                  (int)(chan_off[m][r] + pix_off[n]), 0, 0);
     }
 };
 
 // The last stage of a one-channel-group-per-wave plan (NWK = 1), computed in
 // groups of pixel blocks with every step of the stage before moving to the
-// next group, so that each finished group's stores are issued while the
-// following groups still compute (the output write then overlaps the matrix
-// work instead of following it).  Four blocks per group keep four
-// independent accumulator chains in flight; the 4x4x1 tail block, if any,
-// is the last group, on its four accumulators.
+// next group, so that the output write overlaps the matrix work instead of
+// following it: a finished group's stores are issued a few per step during
+// the next group's steps.  (Issued in one burst they stall the wave, since
+// every workgroup reaches the same group at about the same time and the
+// burst is HBM-write bound.)  Four blocks per group keep four independent
+// accumulator chains in flight; the 4x4x1 tail block, if any, follows group
+// 0 as one burst on its four accumulators and is stored with group 0.
 template <class C>
 __device__ __forceinline__ void compute_stage_streamed(const float *xl, const AStage<C> &A,
                                                        const int (&b_base)[C::NB], floatx4 (&acc)[C::MA][C::NACC],
@@ -559,22 +621,39 @@ __device__ __forceinline__ void compute_stage_streamed(const float *xl, const AS
 {
     constexpr int kSteps = C::KK * C::G4;
     constexpr int GB = 4;
-    constexpr int kGroups = (C::NBM + GB - 1) / GB + (C::TAIL4 ? 1 : 0);
+    constexpr int kGroups = (C::NBM + GB - 1) / GB;  // 16x16x4 groups
+    static_assert(!C::TAIL4 || kGroups > 0, "the tail burst follows group 0");
+    // Stores of one group, and of the tail (stored with group 0).
+    constexpr int kGroupStores = C::MA * GB * 4;
+    constexpr int kTailStores = C::TAIL4 ? C::MA * 4 : 0;
+    constexpr int kDeferred = kGroupStores + kTailStores;
+    constexpr int kStoreRate = (kDeferred + kSteps - 1) / kSteps;
     float bv[2][GB];
-    // Group grp covers blocks [grp*GB, min(grp*GB + GB, NBM)); the tail group
-    // (grp*GB >= NBM) covers block NB-1 alone.
+    // The tail block's B values, read alongside group 0's (one more LDS read
+    // per step) so that its instructions run back to back: a group of its
+    // own would wait on an LDS read every ~10-cycle instruction.
+    float tb[C::TAIL4 ? kSteps : 1];
+    // Group grp covers blocks [grp*GB, min(grp*GB + GB, NBM)).
     auto read = [&](int grp, int st, float(&dst)[GB]) {
         const int t = st / C::G4, c4 = st % C::G4;
         const int kh = t / C::KS, kw = t % C::KS;
         const int off = 4 * C::NWK * c4 * C::PL + kh * C::HCP + kw;
-        if (grp * GB >= C::NBM) {
-            dst[0] = xl[b_base[C::NB - 1] + off];
-            return;
-        }
 #pragma unroll
         for (int j = 0; j < GB; ++j) {
             const int n = grp * GB + j;
             if (n < C::NBM) dst[j] = xl[b_base[n] + off];
+        }
+        if (C::TAIL4 && grp == 0) tb[st] = xl[b_base[C::NB - 1] + off];
+    };
+    // Store i of group grp (rows of its blocks, then, for group 0, the tail's).
+    auto store_item = [&](int grp, int i) {
+        if (i < kGroupStores) {
+            const int m = i / (GB * 4), j = (i / 4) % GB, r = i % 4;
+            const int n = grp * GB + j;
+            if (n < C::NBM) ep.store_one(m, n, r, acc[m][n][r]);
+        } else if (C::TAIL4 && grp == 0 && i < kDeferred) {
+            const int m = (i - kGroupStores) / 4, r = (i - kGroupStores) % 4;
+            ep.store_tail_one(m, r, acc[m][C::NB - 1][r]);
         }
     };
     read(0, 0, bv[0]);
@@ -582,44 +661,42 @@ __device__ __forceinline__ void compute_stage_streamed(const float *xl, const AS
     int cur = 0;
 #pragma unroll
     for (int grp = 0; grp < kGroups; ++grp) {
-        const bool tail = grp * GB >= C::NBM;
 #pragma unroll
         for (int st = 0; st < kSteps; ++st) {
             const int t = st / C::G4, c4 = st % C::G4;
             if (st + 1 < kSteps) read(grp, st + 1, bv[cur ^ 1]);
             else if (grp + 1 < kGroups) read(grp + 1, 0, bv[cur ^ 1]);
+            if (grp > 0) {
 #pragma unroll
-            for (int m = 0; m < C::MA; ++m) {
-                if (tail) {
-                    acc[m][C::NB - 1 + st % 4] =
-                        __builtin_amdgcn_mfma_f32_4x4x1f32(A.v[m][c4][t], bv[cur][0], acc[m][C::NB - 1 + st % 4], 0, 0, 0);
-                } else {
-#pragma unroll
-                    for (int j = 0; j < GB; ++j) {
-                        const int n = grp * GB + j;
-                        if (n < C::NBM)
-                            acc[m][n] = __builtin_amdgcn_mfma_f32_16x16x4f32(A.v[m][c4][t], bv[cur][j], acc[m][n], 0,
-                                                                             0, 0);
-                    }
-                }
+                for (int k = 0; k < kStoreRate; ++k) store_item(grp - 1, st * kStoreRate + k);
             }
-            __builtin_amdgcn_sched_barrier(0);
-            cur ^= 1;
-        }
-        if (tail) {
-            fold_tail<C>(acc);
-#pragma unroll
-            for (int m = 0; m < C::MA; ++m) ep.store(m, C::NB - 1, acc[m][C::NB - 1]);
-        } else {
 #pragma unroll
             for (int m = 0; m < C::MA; ++m)
 #pragma unroll
                 for (int j = 0; j < GB; ++j) {
                     const int n = grp * GB + j;
-                    if (n < C::NBM) ep.store(m, n, acc[m][n]);
+                    if (n < C::NBM)
+                        acc[m][n] = __builtin_amdgcn_mfma_f32_16x16x4f32(A.v[m][c4][t], bv[cur][j], acc[m][n], 0, 0, 0);
                 }
+            __builtin_amdgcn_sched_barrier(0);
+            cur ^= 1;
+        }
+        if (C::TAIL4 && grp == 0) {
+#pragma unroll
+            for (int st = 0; st < kSteps; ++st) {
+                const int t = st / C::G4, c4 = st % C::G4;
+#pragma unroll
+                for (int m = 0; m < C::MA; ++m)
+                    acc[m][C::NB - 1 + st % 4] =
+                        __builtin_amdgcn_mfma_f32_4x4x1f32(A.v[m][c4][t], tb[st], acc[m][C::NB - 1 + st % 4], 0, 0, 0);
+            }
+            fold_tail<C>(acc);
+            __builtin_amdgcn_sched_barrier(0);
         }
     }
+    // The last group's stores (and, with a single group, the tail's).
+#pragma unroll
+    for (int i = 0; i < kDeferred; ++i) store_item(kGroups - 1, i);
 }
 
 // The last stage and the output.  NWK = 1: streamed.  NWK > 1: compute, then
@@ -680,6 +757,7 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    __builtin_assume(wave >= 0 && wave < C::NW);  // lets per-wave index arithmetic fold
     const int wc = wave % C::NWC;
     const int wp = (wave / C::NWC) % C::NWP;
     const int wk = wave / (C::NWC * C::NWP);
@@ -694,13 +772,12 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
     const int xcd = (int)blockIdx.x % 8, slot = (int)blockIdx.x / 8;
     const int per = nwg / 8, extra = nwg % 8;
     const int lin = xcd * per + min(xcd, extra) + slot;
-    const int ntiles = nwg / a.splits;
-    const int split = lin / ntiles;
-    const int tile = lin - split * ntiles;
-    const int co_t = tile % a.co_tiles;
-    const int sp = tile / a.co_tiles;
-    const int tw_i = sp % a.tiles_w;
-    const int th_i = sp / a.tiles_w;
+    const int split = (int)fast_div((unsigned)lin, a.ntiles);
+    const int tile = lin - split * (int)a.ntiles.d;
+    const int sp = (int)fast_div((unsigned)tile, a.co_tiles);
+    const int co_t = tile - sp * (int)a.co_tiles.d;
+    const int th_i = (int)fast_div((unsigned)sp, a.tiles_w);
+    const int tw_i = sp - th_i * (int)a.tiles_w.d;
     const int co0 = co_t * C::COT;
     const int oh0 = th_i * C::TH, ow0 = tw_i * C::TW;
     const int ih0 = oh0 * C::S - a.pad, iw0 = ow0 * C::S - a.pad;
@@ -712,7 +789,7 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
     using WS = typename std::conditional<PK, PackedWeights<C>, OihwWeights<C>>::type;
     const int ci_lane = 4 * wk + g;
     WeightCtx wctx;
-    wctx.rw = make_rsrc(w, PK ? (unsigned)a.co_tiles * a.nchunks * (C::COT * C::CC * C::KK * 4u)
+    wctx.rw = make_rsrc(w, PK ? a.co_tiles.d * (unsigned)a.nchunks * (C::COT * C::CC * C::KK * 4u)
                               : (unsigned)a.c_out * a.c_in * C::KK * 4u);
     wctx.c_in = a.c_in;
     wctx.nchunks = a.nchunks;
@@ -947,13 +1024,20 @@ const Variant kVariants[] = {
     make_variant<Cfg<3, 1, 7, 7, 4, 1, 1, 1, 8>>("k3s1_t7x7_co64"),
     make_variant<Cfg<3, 1, 7, 7, 4, 1, 4, 1, 16>>("k3s1_t7x7_co64_k4"),
     make_variant<Cfg<3, 1, 8, 32, 2, 2, 1, 2, 8>>("k3s1_t8x32_co64"),
+    make_variant<Cfg<3, 1, 4, 4, 1, 1, 4, 1, 64>>("k3s1_t4x4_co16_k4"),
+    make_variant<Cfg<3, 1, 4, 4, 1, 1, 4, 1, 32>>("k3s1_t4x4_co16_k4_cc32"),
+    make_variant<Cfg<3, 1, 4, 4, 1, 1, 4, 2, 32>>("k3s1_t4x4_co32_k4"),
+    make_variant<Cfg<3, 1, 4, 4, 1, 1, 4, 4, 16>>("k3s1_t4x4_co64_k4"),
     make_variant<Cfg<3, 2, 7, 7, 4, 1, 1, 1, 8>>("k3s2_t7x7_co64"),
     make_variant<Cfg<3, 2, 7, 7, 4, 1, 4, 1, 16>>("k3s2_t7x7_co64_k4"),
+    make_variant<Cfg<3, 2, 4, 4, 1, 1, 4, 1, 64>>("k3s2_t4x4_co16_k4"),
     make_variant<Cfg<1, 1, 7, 7, 4, 1, 1, 1, 16>>("k1s1_t7x7_co64"),
     make_variant<Cfg<1, 1, 7, 7, 4, 1, 4, 1, 32>>("k1s1_t7x7_co64_k4"),
     make_variant<Cfg<1, 1, 14, 14, 4, 1, 1, 1, 16>>("k1s1_t14x14_co64"),
+    make_variant<Cfg<1, 1, 4, 4, 1, 1, 4, 1, 64>>("k1s1_t4x4_co16_k4"),
     make_variant<Cfg<5, 1, 7, 7, 4, 1, 1, 1, 4>>("k5s1_t7x7_co64"),
     make_variant<Cfg<5, 1, 7, 7, 4, 1, 2, 1, 8>>("k5s1_t7x7_co64_k2"),
+    make_variant<Cfg<5, 1, 4, 4, 1, 1, 4, 1, 32>>("k5s1_t4x4_co16_k4"),
 };
 constexpr int kNumVariants = sizeof(kVariants) / sizeof(kVariants[0]);
 
@@ -989,6 +1073,10 @@ bool igemm_make_plan(const ConvShape &s, int variant, int splits, ilpm_plan *p)
     // ... and so are those of the prepacked weights (padded to whole tiles).
     if ((int64_t)ceil_div(s.c_out, d.cot) * d.cot * ceil_div(s.c_in, d.cc) * d.cc * s.k * s.k * 4 >= (1LL << 31))
         return false;
+    // Spatial sizes below 2^23: the kernel's 24-bit multiplies are exact.
+    if (s.h >= (1 << 23) || s.w >= (1 << 23) || s.h_out >= (1 << 23) || s.w_out >= (1 << 23)) return false;
+    // A stage's channels (up to CC, past C_in too) stay within 31-bit offsets.
+    if ((int64_t)(s.c_in > d.cc ? s.c_in : d.cc) * s.h * s.w * 4 >= (1LL << 31)) return false;
     const long tiles = (long)ceil_div(s.h_out, d.th) * ceil_div(s.w_out, d.tw) * ceil_div(s.c_out, d.cot);
     if (tiles > 0x7fffffffL) return false;
     const int nchunks = ceil_div(s.c_in, d.cc);
@@ -1002,6 +1090,7 @@ bool igemm_make_plan(const ConvShape &s, int variant, int splits, ilpm_plan *p)
     const int cps = ceil_div(nchunks, splits);
     splits = ceil_div(nchunks, cps);  // no empty split
     if (splits > 65535) return false;
+    if ((int64_t)tiles * splits > 0x7fffffffL) return false;  // workgroup indices are divided as 31-bit values
     const size_t out_elems = (size_t)s.c_out * s.h_out * s.w_out;
     ilpm_plan q = {};
     q.path = ILPM_PATH_IGEMM;
@@ -1094,11 +1183,11 @@ hipError_t igemm_launch(const ilpm_plan &p, const ConvShape &s, const float *x, 
     a.pad = s.pad;
     a.h_out = s.h_out;
     a.w_out = s.w_out;
-    a.tiles_w = ceil_div(s.w_out, d.tw);
-    a.co_tiles = ceil_div(s.c_out, d.cot);
     a.nchunks = ceil_div(s.c_in, d.cc);
     a.chunks_per_split = ceil_div(a.nchunks, p.splits);
-    a.splits = p.splits;
+    a.ntiles = make_fastdiv((unsigned)(p.grid / p.splits));
+    a.co_tiles = make_fastdiv((unsigned)ceil_div(s.c_out, d.cot));
+    a.tiles_w = make_fastdiv((unsigned)ceil_div(s.w_out, d.tw));
     a.to_part = (p.splits > 1 || pool) ? 1 : 0;
     a.relu = relu ? 1 : 0;
     const int tiles = p.grid / p.splits;
