@@ -609,7 +609,8 @@ struct Epilogue {
 // groups of pixel blocks with every step of the stage before moving to the
 // next group, so that the output write overlaps the matrix work instead of
 // following it: a finished group's stores are issued a few per step during
-// the next group's steps.  (Issued in one burst they stall the wave, since
+// the next group's steps, behind the step's matrix instructions.  (Issued
+// in one burst they stall the wave, since
 // every workgroup reaches the same group at about the same time and the
 // burst is HBM-write bound.)  Four blocks per group keep four independent
 // accumulator chains in flight; the 4x4x1 tail block, if any, follows group
@@ -666,10 +667,6 @@ __device__ __forceinline__ void compute_stage_streamed(const float *xl, const AS
             const int t = st / C::G4, c4 = st % C::G4;
             if (st + 1 < kSteps) read(grp, st + 1, bv[cur ^ 1]);
             else if (grp + 1 < kGroups) read(grp + 1, 0, bv[cur ^ 1]);
-            if (grp > 0) {
-#pragma unroll
-                for (int k = 0; k < kStoreRate; ++k) store_item(grp - 1, st * kStoreRate + k);
-            }
 #pragma unroll
             for (int m = 0; m < C::MA; ++m)
 #pragma unroll
@@ -678,6 +675,10 @@ __device__ __forceinline__ void compute_stage_streamed(const float *xl, const AS
                     if (n < C::NBM)
                         acc[m][n] = __builtin_amdgcn_mfma_f32_16x16x4f32(A.v[m][c4][t], bv[cur][j], acc[m][n], 0, 0, 0);
                 }
+            if (grp > 0) {
+#pragma unroll
+                for (int k = 0; k < kStoreRate; ++k) store_item(grp - 1, st * kStoreRate + k);
+            }
             __builtin_amdgcn_sched_barrier(0);
             cur ^= 1;
         }
