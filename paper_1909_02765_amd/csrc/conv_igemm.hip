@@ -69,10 +69,23 @@ constexpr int halo_row(int hr, int hc, int s)
 constexpr int round64(int n) { return (n + 63) / 64 * 64; }
 constexpr int cmax(int a, int b) { return a > b ? a : b; }
 
-template <int KS_, int S_, int TH_, int TW_, int NWC_, int NWP_, int NWK_, int MA_, int CC_>
+template <int KS_, int S_, int TH_, int TW_, int NWC_, int NWP_, int NWK_, int MA_, int CC_, int NBUF_ = 2>
 struct Cfg {
     static constexpr int KS = KS_, S = S_, TH = TH_, TW = TW_;
     static constexpr int NWC = NWC_, NWP = NWP_, NWK = NWK_, MA = MA_, CC = CC_;
+    // Stage buffers: 2 = the next stage's loads fly during this stage; 3 =
+    // the loads of the stage after next, for stages shorter than a memory
+    // round trip (small tiles).
+    static constexpr int NBUF = NBUF_;
+    static_assert(NBUF == 2 || NBUF == 3, "two or three stage buffers");
+    // Three buffers: the stage loop is unrolled UNROLL stages deep
+    // (straight-line code keeps the compiler's tracking of the loads in
+    // flight exact).  The compiler drops the weight loads of the last two
+    // unrolled stages (nothing in the unrolled code reads them), which would
+    // leave those stages' waits counting too few loads, so a workgroup takes
+    // at most UNROLL - 2 stages.
+    static constexpr int UNROLL = NBUF == 3 ? 18 : 0;
+    static constexpr int MAXS = NBUF == 3 ? UNROLL - 2 : 0;
     static constexpr int NW = NWC * NWP * NWK;  // wavefronts per workgroup
     static constexpr int NT = 64 * NW;
     static constexpr int NPIX = TH * TW;
@@ -119,7 +132,7 @@ struct Cfg {
     // LDS for the cross-wave sum of the NWK partial accumulators.
     static constexpr int RED = (NWK - 1) * NWC * NWP * MA * NB * 4 * 64;
     static constexpr int BUF0 = cmax(XSZ, RED);
-    static constexpr int LDS_BYTES = (BUF0 + XSZ) * 4;
+    static constexpr int LDS_BYTES = (BUF0 + (NBUF - 1) * XSZ) * 4;
     static_assert(CC % (4 * NWK) == 0, "a stage holds whole groups of 4 channels per wave");
     static_assert(LDS_BYTES <= 160 * 1024, "LDS budget of one compute unit");
     static_assert(NT <= 1024, "workgroup size");
@@ -150,6 +163,8 @@ struct IgArgs {
     int c_in, h, w, c_out, pad, h_out, w_out;
     int nchunks, chunks_per_split;
     FastDiv ntiles, co_tiles, tiles_w;  // workgroup -> (split, output-channel tile, spatial tile)
+    FastDiv sp_tiles;                    // spatial tiles (tiles_h * tiles_w)
+    int sp_fast;  // consecutive workgroups take consecutive spatial tiles (else output-channel tiles)
     int to_part;  // write raw partial sums to slice `split` of the workspace (a finishing kernel follows)
     int relu;     // otherwise: store max(conv + bias, 0)
 };
@@ -345,7 +360,8 @@ __device__ __forceinline__ void dma_halo(float *buf, const float *__restrict__ x
                                          const int (&xo)[C::XPT])
 {
     const unsigned plane = (unsigned)a.h * (unsigned)a.w;
-    const __amdgpu_buffer_rsrc_t rx = make_rsrc(x + (size_t)ci0 * plane, (unsigned)(a.c_in - ci0) * plane * 4u);
+    const __amdgpu_buffer_rsrc_t rx =
+        make_rsrc(x + (size_t)ci0 * plane, ci0 < a.c_in ? (unsigned)(a.c_in - ci0) * plane * 4u : 0u);
     constexpr int kFull = C::NIX / C::NW;  // rounds in which every wave issues one
 #pragma unroll
     for (int j = 0; j < kFull; ++j)
@@ -384,7 +400,9 @@ struct NextStage {
         : buf(buf_), A(&A_), xo(xo_), wave(wave_), ws(wk, a.c_out, ci0)
     {
         const unsigned plane = (unsigned)a.h * (unsigned)a.w;
-        rx = make_rsrc(x + (size_t)ci0 * plane, (unsigned)(a.c_in - ci0) * plane * 4u);
+        // A stage past the last (three-buffer prefetch) gets an empty range:
+        // its loads read zeros and touch no memory.
+        rx = make_rsrc(x + (size_t)ci0 * plane, ci0 < a.c_in ? (unsigned)(a.c_in - ci0) * plane * 4u : 0u);
     }
 
     __device__ __forceinline__ void issue(int i)
@@ -417,6 +435,27 @@ __device__ __forceinline__ void stage_ready()
 {
     __builtin_amdgcn_s_waitcnt(0x0F70);
     __syncthreads();
+}
+
+// The same with the K most recent loads of this wave still in flight (the
+// stage after next).  Vector-memory loads complete in issue order, so the
+// count leaves exactly the older stage's loads landed; K is at most the
+// fewest loads any wave issues for a stage.  vmcnt is split over bits 3:0
+// and 15:14 of the wait's immediate.
+template <int K>
+__device__ __forceinline__ void stage_ready_keep()
+{
+    static_assert(K >= 0 && K < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt(0x0F70 | (K & 15) | ((K >> 4) << 14));
+    // A bare barrier: __syncthreads() also orders this wave's pending LDS
+    // writes -- the DMA of the stage after next -- before it, which would
+    // wait for them.  The data each wave needs next is complete by the count
+    // above, and every LDS read of the stage just computed has been consumed
+    // by its matrix instructions.  The empty asm statements keep the compiler
+    // from moving memory accesses across.
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
 }
 
 // B fragments (input patches) of step st for one wave.
@@ -750,10 +789,11 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
                                                     const float *__restrict__ bias, float *__restrict__ out,
                                                     float *__restrict__ part, IgArgs a)
 {
-    // Two stage buffers in separate LDS objects, so the compiler can tell a
-    // read of one from the DMA filling the other.
+    // Stage buffers in separate LDS objects, so the compiler can tell a read
+    // of one from the DMA filling another.
     __shared__ __attribute__((aligned(16))) float lds0[C::BUF0];
     __shared__ __attribute__((aligned(16))) float lds1[C::XSZ];
+    __shared__ __attribute__((aligned(16))) float lds2[C::NBUF == 3 ? C::XSZ : 1];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -767,16 +807,24 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
 
     // Workgroup -> (split, tile).  Workgroups are dealt round-robin to the 8
     // XCDs (workgroup i to XCD i mod 8), each with its own L2; giving every
-    // XCD a contiguous run of tiles keeps neighbouring tiles -- which share
-    // halo rows and output cache lines -- in one L2.
+    // XCD a contiguous run of tiles keeps tiles that share data in one L2:
+    // neighbouring spatial tiles (halo rows, output cache lines, and with
+    // sp_fast the same weights) or, otherwise, the output-channel tiles of
+    // one spatial tile (the same input).
     const int nwg = (int)gridDim.x;
     const int xcd = (int)blockIdx.x % 8, slot = (int)blockIdx.x / 8;
     const int per = nwg / 8, extra = nwg % 8;
     const int lin = xcd * per + min(xcd, extra) + slot;
     const int split = (int)fast_div((unsigned)lin, a.ntiles);
     const int tile = lin - split * (int)a.ntiles.d;
-    const int sp = (int)fast_div((unsigned)tile, a.co_tiles);
-    const int co_t = tile - sp * (int)a.co_tiles.d;
+    int sp, co_t;
+    if (a.sp_fast) {
+        co_t = (int)fast_div((unsigned)tile, a.sp_tiles);
+        sp = tile - co_t * (int)a.sp_tiles.d;
+    } else {
+        sp = (int)fast_div((unsigned)tile, a.co_tiles);
+        co_t = tile - sp * (int)a.co_tiles.d;
+    }
     const int th_i = (int)fast_div((unsigned)sp, a.tiles_w);
     const int tw_i = sp - th_i * (int)a.tiles_w.d;
     const int co0 = co_t * C::COT;
@@ -835,6 +883,40 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
     // range (< 2^30, checked when the plan is made), and its store is dropped.
     Epilogue<C> ep;
     ep.init(a, out, part, bias, split, co0 + wc * 16 * C::MA + 4 * g, wp, g, l16, oh0, ow0);
+
+    if constexpr (C::NBUF == 3) {
+        // Three buffers: stage ch computes from buffer ch mod 3 while the
+        // loads of stage ch + 2 fill buffer (ch + 2) mod 3, whose last reader
+        // (stage ch - 1) every wave finished before the barrier that ended it.
+        // The prefetch is issued unconditionally: for stages past the last,
+        // every load falls outside its descriptor (zeros into a buffer no
+        // stage reads), which keeps the loop free of branches around loads
+        // -- so that the compiler's own load tracking stays exact across it
+        // and adds no waits of its own.
+        constexpr int kLoads = NextStage<C, WS>::kFull + WS::NA;  // fewest loads any wave issues per stage
+        AStage<C> a2;
+        dma_halo<C>(lds1, x, a, (c_begin + 1) * C::CC, wave, xo);
+        load_a<C>(a1, WS(wctx, a.c_out, (c_begin + 1) * C::CC));
+        stage_ready_keep<kLoads>();
+        // One stage: compute from (xl, A), prefetch stage ch + 2 into (xn, An).
+        auto step = [&](int ch, float *xl, AStage<C> &A, float *xn, AStage<C> &An) -> bool {
+            if (ch + 1 >= c_end) {
+                final_stage<C>(xl, A, b_base, acc, lds0, wave, wk, lane, ep);
+                return true;
+            }
+            NextStage<C, WS> next(xn, An, x, a, wctx, (ch + 2) * C::CC, wave, xo);
+            compute_stage<C>(xl, A, b_base, acc, next);
+            stage_ready_keep<kLoads>();
+            return false;
+        };
+#pragma unroll
+        for (int k = 0; k < C::UNROLL; k += 3) {
+            if (step(c_begin + k, lds0, a0, lds2, a2)) break;
+            if (step(c_begin + k + 1, lds1, a1, lds0, a0)) break;
+            if (step(c_begin + k + 2, lds2, a2, lds1, a1)) break;
+        }
+        return;
+    }
 
     stage_ready();
 
@@ -991,6 +1073,7 @@ struct Variant {
     const char *name;
     int ks, s, th, tw, nwc, nwp, nwk, ma, cc;
     int nt, cot, lds;
+    int max_stages;  // 0: any number of stages per workgroup
     void (*launch)(dim3 grid, hipStream_t st, const float *, const float *, const float *, float *, float *,
                    const IgArgs &, bool packed);
 };
@@ -1007,7 +1090,7 @@ template <class C>
 constexpr Variant make_variant(const char *name)
 {
     return Variant{name, C::KS, C::S, C::TH, C::TW, C::NWC, C::NWP, C::NWK, C::MA, C::CC,
-                   C::NT, C::COT, C::LDS_BYTES, &launch_cfg<C>};
+                   C::NT, C::COT, C::LDS_BYTES, C::MAXS, &launch_cfg<C>};
 }
 
 //                                  KS S  TH  TW NWC NWP NWK MA CC
@@ -1023,13 +1106,19 @@ const Variant kVariants[] = {
     make_variant<Cfg<3, 1, 14, 14, 4, 1, 1, 1, 4>>("k3s1_t14x14_co64_cc4"),
     make_variant<Cfg<3, 1, 7, 7, 4, 1, 1, 1, 4>>("k3s1_t7x7_co64_cc4"),
     make_variant<Cfg<3, 1, 7, 7, 4, 1, 1, 1, 8>>("k3s1_t7x7_co64"),
+    make_variant<Cfg<3, 1, 7, 7, 4, 1, 1, 1, 16>>("k3s1_t7x7_co64_cc16"),
     make_variant<Cfg<3, 1, 7, 7, 4, 1, 4, 1, 16>>("k3s1_t7x7_co64_k4"),
     make_variant<Cfg<3, 1, 8, 32, 2, 2, 1, 2, 8>>("k3s1_t8x32_co64"),
     make_variant<Cfg<3, 1, 4, 4, 1, 1, 4, 1, 64>>("k3s1_t4x4_co16_k4"),
     make_variant<Cfg<3, 1, 4, 4, 1, 1, 4, 1, 32>>("k3s1_t4x4_co16_k4_cc32"),
     make_variant<Cfg<3, 1, 4, 4, 1, 1, 4, 2, 32>>("k3s1_t4x4_co32_k4"),
     make_variant<Cfg<3, 1, 4, 4, 1, 1, 4, 4, 16>>("k3s1_t4x4_co64_k4"),
+    make_variant<Cfg<3, 1, 4, 4, 1, 1, 4, 1, 32, 3>>("k3s1_t4x4_co16_k4_cc32_b3"),
+    make_variant<Cfg<3, 1, 4, 4, 1, 1, 4, 1, 16, 3>>("k3s1_t4x4_co16_k4_cc16_b3"),
+    make_variant<Cfg<3, 1, 4, 4, 1, 1, 4, 2, 32, 3>>("k3s1_t4x4_co32_k4_b3"),
+    make_variant<Cfg<3, 1, 7, 7, 4, 1, 1, 1, 4, 3>>("k3s1_t7x7_co64_cc4_b3"),
     make_variant<Cfg<3, 2, 7, 7, 4, 1, 1, 1, 8>>("k3s2_t7x7_co64"),
+    make_variant<Cfg<3, 2, 7, 7, 4, 1, 1, 1, 16>>("k3s2_t7x7_co64_cc16"),
     make_variant<Cfg<3, 2, 7, 7, 4, 1, 4, 1, 16>>("k3s2_t7x7_co64_k4"),
     make_variant<Cfg<3, 2, 4, 4, 1, 1, 4, 1, 64>>("k3s2_t4x4_co16_k4"),
     make_variant<Cfg<1, 1, 7, 7, 4, 1, 1, 1, 16>>("k1s1_t7x7_co64"),
@@ -1037,6 +1126,7 @@ const Variant kVariants[] = {
     make_variant<Cfg<1, 1, 14, 14, 4, 1, 1, 1, 16>>("k1s1_t14x14_co64"),
     make_variant<Cfg<1, 1, 4, 4, 1, 1, 4, 1, 64>>("k1s1_t4x4_co16_k4"),
     make_variant<Cfg<5, 1, 7, 7, 4, 1, 1, 1, 4>>("k5s1_t7x7_co64"),
+    make_variant<Cfg<5, 1, 7, 7, 4, 1, 1, 1, 8>>("k5s1_t7x7_co64_cc8"),
     make_variant<Cfg<5, 1, 7, 7, 4, 1, 2, 1, 8>>("k5s1_t7x7_co64_k2"),
     make_variant<Cfg<5, 1, 4, 4, 1, 1, 4, 1, 32>>("k5s1_t4x4_co16_k4"),
 };
@@ -1086,9 +1176,11 @@ bool igemm_make_plan(const ConvShape &s, int variant, int splits, ilpm_plan *p)
         splits = 1;
         if (tiles < kCUs) splits = (int)((kCUs + tiles - 1) / tiles);
         if (splits > nchunks) splits = nchunks;
+        if (d.max_stages > 0 && ceil_div(nchunks, splits) > d.max_stages) splits = ceil_div(nchunks, d.max_stages);
     }
     if (splits > nchunks) return false;
     const int cps = ceil_div(nchunks, splits);
+    if (d.max_stages > 0 && cps > d.max_stages) return false;
     splits = ceil_div(nchunks, cps);  // no empty split
     if (splits > 65535) return false;
     if ((int64_t)tiles * splits > 0x7fffffffL) return false;  // workgroup indices are divided as 31-bit values
@@ -1189,6 +1281,11 @@ hipError_t igemm_launch(const ilpm_plan &p, const ConvShape &s, const float *x, 
     a.ntiles = make_fastdiv((unsigned)(p.grid / p.splits));
     a.co_tiles = make_fastdiv((unsigned)ceil_div(s.c_out, d.cot));
     a.tiles_w = make_fastdiv((unsigned)ceil_div(s.w_out, d.tw));
+    a.sp_tiles = make_fastdiv((unsigned)(ceil_div(s.h_out, d.th) * ceil_div(s.w_out, d.tw)));
+    // Each XCD runs a contiguous run of workgroups.  When the weights
+    // outweigh the input, let the run share output-channel tiles (and so
+    // weights) across spatial tiles; otherwise share spatial tiles (input).
+    a.sp_fast = (int64_t)s.c_out * s.c_in * s.k * s.k > (int64_t)s.c_in * s.h * s.w ? 1 : 0;
     a.to_part = (p.splits > 1 || pool) ? 1 : 0;
     a.relu = relu ? 1 : 0;
     const int tiles = p.grid / p.splits;
