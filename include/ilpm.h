@@ -160,6 +160,20 @@ int ilpm_variant_info(int path, int variant, int *K, int *stride, int *tile_h, i
                       int *co_tile);
 
 /*
+ * ilpm_variant_pipeline -- how a compiled variant moves its data: input
+ * channels per stage (`ci_chunk`), the stage count a workgroup is built for
+ * (`stages`, 0 = any), stage buffers (`buffers`; 0 for the direct path) and
+ * ILPM_VARIANT_* `flags`.  A variant with a fixed stage count (more than two
+ * buffers: the loads of later stages fly while earlier ones compute, and
+ * the stage sequence is unrolled at compile time) plans only shapes whose
+ * ceil(C_in / ci_chunk) is a whole multiple of `stages`, with exactly
+ * ceil(C_in / ci_chunk) / stages splits.  Pure host; ILPM_ERR_INVALID_ARG
+ * for an unknown variant.  Any output pointer may be NULL.
+ */
+#define ILPM_VARIANT_WEIGHTS_LDS 1   /* weights staged through LDS from OIHW; prepacked weights are an OIHW copy */
+int ilpm_variant_pipeline(int path, int variant, int *ci_chunk, int *stages, int *buffers, int *flags);
+
+/*
  * ilpm_conv2d_fwd_plan -- ilpm_conv2d_fwd with an explicit plan (from
  * ilpm_conv2d_plan or ilpm_conv2d_plan_variant for the same shape).
  */

@@ -26,6 +26,7 @@ ERR_HIP = -4
 ERR_ARCH = -5
 PATH_DIRECT = 0
 PATH_IGEMM = 1
+VARIANT_WEIGHTS_LDS = 1   # ilpm_variant_pipeline flags
 
 
 class IlpmError(RuntimeError):
@@ -93,6 +94,7 @@ _SIGS = {
     "ilpm_num_variants": ([_i], _i),
     "ilpm_variant_name": ([_i, _i], ctypes.c_char_p),
     "ilpm_variant_info": ([_i, _i] + [ctypes.POINTER(_i)] * 5, _i),
+    "ilpm_variant_pipeline": ([_i, _i] + [ctypes.POINTER(_i)] * 4, _i),
     "ilpm_conv2d_prepacked_size": ([_plan_p, _i, _i, _i, ctypes.POINTER(ctypes.c_size_t)], _i),
     "ilpm_conv2d_prepack_weights": ([_vp, _i, _i, _i, _plan_p, _vp, _vp], _i),
     "ilpm_conv2d_fwd_prepacked": ([_vp, _vp, _vp] + [_i] * 7 + [_plan_p, _vp, _vp], _i),
@@ -172,7 +174,11 @@ def variant_info(path: int, variant: int):
     vals = [ctypes.c_int() for _ in range(5)]
     _check(lib.ilpm_variant_info(path, variant, *[ctypes.byref(v) for v in vals]), "ilpm_variant_info")
     k, s, th, tw, co = (v.value for v in vals)
-    return dict(k=k, stride=s, tile_h=th, tile_w=tw, co_tile=co)
+    cc, ns, nb, fl = (ctypes.c_int() for _ in range(4))
+    _check(lib.ilpm_variant_pipeline(path, variant, *(ctypes.byref(v) for v in (cc, ns, nb, fl))),
+           "ilpm_variant_pipeline")
+    return dict(k=k, stride=s, tile_h=th, tile_w=tw, co_tile=co, ci_chunk=cc.value, stages=ns.value,
+                buffers=nb.value, weights_lds=bool(fl.value & VARIANT_WEIGHTS_LDS))
 
 
 def workspace_size(c_in, h, w, c_out, k, stride=1, pad=0) -> int:

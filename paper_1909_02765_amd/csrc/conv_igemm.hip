@@ -46,6 +46,7 @@
 // read different banks (see Cfg).
 #include <cmath>
 #include <type_traits>
+#include <utility>
 
 #include "internal.h"
 
@@ -69,7 +70,8 @@ constexpr int halo_row(int hr, int hc, int s)
 constexpr int round64(int n) { return (n + 63) / 64 * 64; }
 constexpr int cmax(int a, int b) { return a > b ? a : b; }
 
-template <int KS_, int S_, int TH_, int TW_, int NWC_, int NWP_, int NWK_, int MA_, int CC_, int NBUF_ = 2>
+template <int KS_, int S_, int TH_, int TW_, int NWC_, int NWP_, int NWK_, int MA_, int CC_, int NBUF_ = 2, int NS_ = 0,
+          bool WL_ = false>
 struct Cfg {
     static constexpr int KS = KS_, S = S_, TH = TH_, TW = TW_;
     static constexpr int NWC = NWC_, NWP = NWP_, NWK = NWK_, MA = MA_, CC = CC_;
@@ -77,15 +79,14 @@ struct Cfg {
     // the loads of the stage after next, for stages shorter than a memory
     // round trip (small tiles).
     static constexpr int NBUF = NBUF_;
-    static_assert(NBUF == 2 || NBUF == 3, "two or three stage buffers");
-    // Three buffers: the stage loop is unrolled UNROLL stages deep
-    // (straight-line code keeps the compiler's tracking of the loads in
-    // flight exact).  The compiler drops the weight loads of the last two
-    // unrolled stages (nothing in the unrolled code reads them), which would
-    // leave those stages' waits counting too few loads, so a workgroup takes
-    // at most UNROLL - 2 stages.
-    static constexpr int UNROLL = NBUF == 3 ? 18 : 0;
-    static constexpr int MAXS = NBUF == 3 ? UNROLL - 2 : 0;
+    static_assert(NBUF >= 2 && NBUF <= 6, "two to six stage buffers");
+    // More than two buffers: the kernel is built for exactly NS stages per
+    // workgroup, so its stage sequence is straight-line code with no exits
+    // (which keeps the compiler's own tracking of the loads in flight exact:
+    // a loop or an early exit merges its state and it then waits on loads
+    // the stage does not need).
+    static constexpr int NS = NS_;
+    static_assert(NBUF == 2 ? NS == 0 : NS >= 1, "a deeper pipeline needs a fixed stage count");
     static constexpr int NW = NWC * NWP * NWK;  // wavefronts per workgroup
     static constexpr int NT = 64 * NW;
     static constexpr int NPIX = TH * TW;
@@ -129,10 +130,27 @@ struct Cfg {
     static constexpr int NIX = QUAD ? CC * HR / 4 : XSZ / 64;
     static constexpr int XPT = (NIX + NW - 1) / NW;  // DMA instructions per wave
     __device__ static constexpr int dma_dst(int e) { return QUAD ? (e / (HR / 4)) * PL + (e % (HR / 4)) * 64 : e * 64; }
+    // Weights through LDS (WL): instead of each lane gathering its own
+    // weights from OIHW (16 different rows per load instruction, which with
+    // small tiles leaves every stage waiting on the L1), a stage's weight
+    // block -- COT output channels x CC input channels x KK taps -- is copied
+    // after the halo by 16-byte-per-lane DMA of contiguous OIHW runs: output
+    // channel r at row r*ROW, input channel c at +c*KKP, taps padded to KKP =
+    // KK rounded up to 4, so a 4-tap piece never mixes channels.  The matrix
+    // instructions read their A operands from LDS four taps at a time;
+    // ROW/4 odd puts the eight lanes of each 128-byte pass of such a read on
+    // different banks.
+    static constexpr bool WL = WL_;
+    static_assert(!WL || (NWK > 1 && !TAIL4), "weights through LDS: channel-split tiles");
+    static constexpr int KKP = (KK + 3) / 4 * 4;
+    static constexpr int ROW = (CC * KKP + 4) / 8 * 8 + 4;  // >= CC*KKP, = 4 mod 8
+    static constexpr int WSZ = WL ? (COT * ROW + 255) / 256 * 256 : 0;
+    static constexpr int NIXW = WSZ / 256;  // weight DMA instructions per stage (64 lanes x 4 words)
+    static constexpr int SBUF = XSZ + WSZ;  // one stage buffer: halo, then weights
     // LDS for the cross-wave sum of the NWK partial accumulators.
     static constexpr int RED = (NWK - 1) * NWC * NWP * MA * NB * 4 * 64;
-    static constexpr int BUF0 = cmax(XSZ, RED);
-    static constexpr int LDS_BYTES = (BUF0 + (NBUF - 1) * XSZ) * 4;
+    static constexpr int BUF0 = cmax(SBUF, RED);
+    static constexpr int LDS_BYTES = (BUF0 + (NBUF - 1) * SBUF) * 4;
     static_assert(CC % (4 * NWK) == 0, "a stage holds whole groups of 4 channels per wave");
     static_assert(LDS_BYTES <= 160 * 1024, "LDS budget of one compute unit");
     static_assert(NT <= 1024, "workgroup size");
@@ -190,9 +208,17 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const float *base, u
 }
 
 // Weight registers of one stage for one lane: [m-block][channel group][tap].
-template <class C>
+template <class C, bool WL = C::WL>
 struct AStage {
     float v[C::MA][C::G4][C::KK];
+};
+
+// Weights through LDS: what a lane needs is where its A operands lie, the
+// LDS word of (m-block m, channel group 0, tap 0) relative to the stage
+// buffer (the same for every stage).
+template <class C>
+struct AStage<C, true> {
+    int base[C::MA];
 };
 
 // Where a lane's weights come from.  Every wave holds, per stage, the
@@ -207,6 +233,9 @@ struct WeightCtx {
     int ci_lane;   // 4*wk + g
     int block0;    // prepacked layout: (co_t*nchunks)*NWK*NWC + wk*NWC + wc
     int lane;
+    int c_out, wave;
+    const float *w;     // OIHW weights (weights through LDS)
+    const void *wl;     // weights through LDS: this lane's DMA offsets (WlLanes<C>)
 };
 
 // OIHW weights: lane (g, l) reads its own contiguous run of KK taps per
@@ -215,10 +244,11 @@ template <class C>
 struct OihwWeights {
     static constexpr int kPieces = C::KK / 4 + C::KK % 4;
     static constexpr int NA = C::G4 * C::MA * kPieces;
+    static constexpr int NA_MIN = NA;  // issued by every wave
     __amdgpu_buffer_rsrc_t rw;
     unsigned a_base[C::G4][C::MA];
 
-    __device__ __forceinline__ OihwWeights(const WeightCtx &k, int c_out, int ci0) : rw(k.rw)
+    __device__ __forceinline__ OihwWeights(const WeightCtx &k, int c_out, int ci0, float *) : rw(k.rw)
     {
         // One row product per m-block, then additions: no branches, and only
         // MA full 32-bit multiplies.
@@ -272,10 +302,11 @@ struct PackedWeights {
     static constexpr int EPL = C::MA * C::G4 * C::KK;
     static constexpr int N4 = EPL / 4, REM = EPL % 4;
     static constexpr int NA = N4 + REM;
+    static constexpr int NA_MIN = NA;
     __amdgpu_buffer_rsrc_t rw;
     unsigned base;  // bytes: this wave's block for the stage
 
-    __device__ __forceinline__ PackedWeights(const WeightCtx &k, int, int ci0) : rw(k.rw)
+    __device__ __forceinline__ PackedWeights(const WeightCtx &k, int, int ci0, float *) : rw(k.rw)
     {
         const int block = k.block0 + (ci0 / C::CC) * C::NWK * C::NWC;
         base = (unsigned)block * (64u * EPL * 4u);
@@ -306,6 +337,65 @@ struct PackedWeights {
                 __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
                                               rw, (int)(base + 1024u * N4 + 256u * j + 4u * lane), 0, 0)));
         }
+    }
+};
+
+// Weights through LDS: per lane and weight DMA instruction j of this wave
+// (instruction e = j*NW + wave, 4-word piece 64*e + lane of the weight area),
+// the byte offset of its first OIHW element relative to the stage's first
+// input channel, or 2^31 for row padding and channels past C_out, and its
+// input channel within the stage, which at or past C_in reads nothing.  (A
+// piece's taps past KK read the next OIHW elements into row padding no
+// instruction reads; past the tensor's end the descriptor's per-word range
+// check returns zeros.)
+template <class C>
+struct WlLanes {
+    static constexpr int XPTW = (C::NIXW + C::NW - 1) / C::NW;
+    unsigned off[XPTW];
+    int col[XPTW];
+
+    __device__ __forceinline__ void init(int co0, int c_in, int c_out, int wave, int lane)
+    {
+#pragma unroll
+        for (int j = 0; j < XPTW; ++j) {
+            const int q = (j * C::NW + wave) * 64 + lane;  // 4-word piece of the weight area
+            const int r = q / (C::ROW / 4), rem = q - r * (C::ROW / 4);
+            const int c = rem / (C::KKP / 4), piece = rem - c * (C::KKP / 4);
+            const int co = co0 + r;
+            const bool ok = r < C::COT && c < C::CC && co < c_out;
+            off[j] = ok ? (unsigned)(co * c_in * C::KK + c * C::KK + 4 * piece) * 4u : 0x80000000u;
+            col[j] = ok ? c : C::CC;  // the piece's input channel within the stage
+        }
+    }
+};
+
+template <class C>
+struct LdsWeights {
+    static constexpr int XPTW = WlLanes<C>::XPTW;
+    static constexpr int kFullW = C::NIXW / C::NW;
+    static constexpr int NA = XPTW;
+    static constexpr int NA_MIN = kFullW;
+    __amdgpu_buffer_rsrc_t rw;
+    const WlLanes<C> *lanes;
+    float *dst;  // the stage buffer's weight area
+    int lim;     // C_in - ci0: the stage's input channels that exist
+    int wave;
+
+    __device__ __forceinline__ LdsWeights(const WeightCtx &k, int c_out, int ci0, float *buf)
+        : lanes(static_cast<const WlLanes<C> *>(k.wl)), dst(buf + C::XSZ), wave(k.wave)
+    {
+        const int64_t total = (int64_t)c_out * k.c_in * C::KK;
+        const int64_t first = (int64_t)ci0 * C::KK;
+        rw = make_rsrc(k.w + first, first < total ? (unsigned)(total - first) * 4u : 0u);
+        lim = k.c_in - ci0;
+    }
+
+    __device__ __forceinline__ void load(int q, AStage<C> &) const
+    {
+        if (q >= kFullW && q * C::NW + wave >= C::NIXW) return;  // a last, partial round
+        const unsigned o = lanes->col[q] < lim ? lanes->off[q] : 0x80000000u;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_ptr_t)(dst + (q * C::NW + wave) * 256), 16, (int)o, 0, 0,
+                                                 0);
     }
 };
 
@@ -397,11 +487,11 @@ struct NextStage {
 
     __device__ __forceinline__ NextStage(float *buf_, AStage<C> &A_, const float *__restrict__ x, const IgArgs &a,
                                          const WeightCtx &wk, int ci0, int wave_, const int (&xo_)[C::XPT])
-        : buf(buf_), A(&A_), xo(xo_), wave(wave_), ws(wk, a.c_out, ci0)
+        : buf(buf_), A(&A_), xo(xo_), wave(wave_), ws(wk, a.c_out, ci0, buf_)
     {
         const unsigned plane = (unsigned)a.h * (unsigned)a.w;
-        // A stage past the last (three-buffer prefetch) gets an empty range:
-        // its loads read zeros and touch no memory.
+        // A stage starting at or past C_in gets an empty range: its loads
+        // read zeros and touch no memory.
         rx = make_rsrc(x + (size_t)ci0 * plane, ci0 < a.c_in ? (unsigned)(a.c_in - ci0) * plane * 4u : 0u);
     }
 
@@ -458,6 +548,18 @@ __device__ __forceinline__ void stage_ready_keep()
     asm volatile("" ::: "memory");
 }
 
+// The end of a stage of a pipelined plan: its next stage's loads landed,
+// with K of the latest still in flight.
+template <class C, int K>
+__device__ __forceinline__ void stage_wait()
+{
+    if constexpr (K > 0) {
+        stage_ready_keep<K>();
+    } else {
+        stage_ready();
+    }
+}
+
 // B fragments (input patches) of step st for one wave.
 template <class C>
 __device__ __forceinline__ void read_b(const float *xl, const int (&b_base)[C::NB], int st, float (&bv)[C::NB])
@@ -497,6 +599,22 @@ __device__ __forceinline__ void compute_stage(const float *xl, const AStage<C> &
     constexpr int kRate = P::N == 0 ? 1 : (P::N + kHalf - 1) / kHalf;
     float bv[R][C::NB];
     float tb[C::TAIL4 ? kSteps : 1];
+    // Weights through LDS: the A operands of taps 4j..4j+3 (piece j) for
+    // every m-block and channel group, one 16-byte LDS read each, the next
+    // piece read while the current one is used.
+    constexpr int NJ = C::KKP / 4;
+    floatx4 ach[C::WL ? 2 : 1][C::MA][C::WL ? C::G4 : 1];
+    auto read_a_piece = [&](int j, int slot) {
+        if constexpr (C::WL) {
+#pragma unroll
+            for (int m = 0; m < C::MA; ++m)
+#pragma unroll
+                for (int c4 = 0; c4 < C::G4; ++c4)
+                    ach[slot][m][c4] =
+                        *reinterpret_cast<const floatx4 *>(xl + A.base[m] + c4 * 4 * C::NWK * C::KKP + 4 * j);
+        }
+    };
+    read_a_piece(0, 0);
 #pragma unroll
     for (int s = 0; s < D && s < kSteps; ++s) read_b<C>(xl, b_base, s, bv[s]);
     __builtin_amdgcn_sched_barrier(0);
@@ -504,22 +622,29 @@ __device__ __forceinline__ void compute_stage(const float *xl, const AStage<C> &
     for (int st = 0; st < kSteps; ++st) {
         const int cur = st % R;
         const int t = st / C::G4, c4 = st % C::G4;
+        const int j = t / 4;
+        const bool piece_read = C::WL && c4 == 0 && t % 4 == 0 && j + 1 < NJ;
 #pragma unroll
         for (int r = 0; r < kRate; ++r)
             if (st * kRate + r < P::N) next.issue(st * kRate + r);
+        if (piece_read) read_a_piece(j + 1, (j + 1) & 1);
         if (st + D < kSteps) read_b<C>(xl, b_base, st + D, bv[(st + D) % R]);
 #pragma unroll
-        for (int m = 0; m < C::MA; ++m)
+        for (int m = 0; m < C::MA; ++m) {
+            float a_op;
+            if constexpr (C::WL) a_op = ach[j & 1][m][c4][t % 4];
+            else a_op = A.v[m][c4][t];
 #pragma unroll
             for (int n = 0; n < C::NBM; ++n)
-                acc[m][n] = __builtin_amdgcn_mfma_f32_16x16x4f32(A.v[m][c4][t], bv[cur][n], acc[m][n], 0, 0, 0);
+                acc[m][n] = __builtin_amdgcn_mfma_f32_16x16x4f32(a_op, bv[cur][n], acc[m][n], 0, 0, 0);
+        }
         if constexpr (C::TAIL4) tb[st] = bv[cur][C::NB - 1];
         // Within the step: one matrix instruction, then one read of a later
         // step, so the reads issue while the matrix pipe is busy.
         constexpr int kMf = C::MA * C::NBM;
-        const int n_ds = st + D < kSteps ? C::NB : 0;
+        const int n_ds = (st + D < kSteps ? C::NB : 0) + (piece_read ? C::MA * C::G4 : 0);
 #pragma unroll
-        for (int i = 0; i < (kMf > C::NB ? kMf : C::NB); ++i) {
+        for (int i = 0; i < (kMf > C::NB + C::MA * C::G4 ? kMf : C::NB + C::MA * C::G4); ++i) {
             if (i < kMf) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
             if (i < n_ds) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
         }
@@ -784,6 +909,66 @@ __device__ __forceinline__ void final_stage(const float *xl, const AStage<C> &A,
     }
 }
 
+// The fewest loads any wave issues for one stage: its full rounds of halo
+// DMA (a last, partial round falls to some waves only) and its weight loads.
+template <class C, class WS>
+constexpr int kStageLoads()
+{
+    return NextStage<C, WS>::kFull + WS::NA_MIN;
+}
+
+// f(integral_constant<int, I>) for I = 0, 1, ..., in order.
+template <class F, int... I>
+__device__ __forceinline__ void for_each_index(std::integer_sequence<int, I...>, F &&f)
+{
+    (f(std::integral_constant<int, I>{}), ...);
+}
+
+// Loads a wave may leave in flight at the end of stage s (those of stages
+// s + 2 .. s + NBUF - 1 that exist) while stage s + 1's have all landed.
+template <class C, class WS>
+constexpr int kKeepAfter(int s)
+{
+    const int last = s + C::NBUF - 1 < C::NS - 1 ? s + C::NBUF - 1 : C::NS - 1;
+    const int n = last - (s + 2) + 1;
+    return n > 0 ? n * kStageLoads<C, WS>() : 0;
+}
+
+// The stages of a fixed-stage plan, unrolled at compile time: stage s
+// computes from buffer s mod NBUF and issues the loads of stage s + NBUF - 1
+// (into the buffer stage s - 1 read, which every wave finished before the
+// barrier that ended it), and the last stage is the final one.  Every wait
+// is exact: it leaves in flight only the loads of the stages after next.
+template <class C, class WS, int... S>
+__device__ __forceinline__ void run_stages(std::integer_sequence<int, S...>, float *const (&bufs)[6],
+                                           AStage<C> *const (&regs)[6], const float *__restrict__ x,
+                                           const IgArgs &a, const WeightCtx &wctx, int c_begin, int wave, int wk,
+                                           int lane, const int (&xo)[C::XPT], const int (&b_base)[C::NB],
+                                           floatx4 (&acc)[C::MA][C::NACC], const Epilogue<C> &ep)
+{
+    auto stage = [&](auto sc) {
+        constexpr int s = decltype(sc)::value;
+        constexpr int t = s + C::NBUF - 1;  // the stage whose loads this one issues
+        constexpr int keep = kKeepAfter<C, WS>(s);
+        float *xl = bufs[s % C::NBUF];
+        AStage<C> &A = *regs[s % C::NBUF];
+        if constexpr (s == C::NS - 1) {
+            final_stage<C>(xl, A, b_base, acc, bufs[0], wave, wk, lane, ep);
+        } else {
+            if constexpr (t < C::NS) {
+                NextStage<C, WS> next(bufs[t % C::NBUF], *regs[t % C::NBUF], x, a, wctx, (c_begin + t) * C::CC, wave,
+                                      xo);
+                compute_stage<C>(xl, A, b_base, acc, next);
+            } else {
+                NoNextStage none;
+                compute_stage<C>(xl, A, b_base, acc, none);
+            }
+            stage_wait<C, keep>();
+        }
+    };
+    for_each_index(std::integer_sequence<int, S...>{}, stage);
+}
+
 template <class C, bool PK>
 __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x, const float *__restrict__ w,
                                                     const float *__restrict__ bias, float *__restrict__ out,
@@ -792,8 +977,11 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
     // Stage buffers in separate LDS objects, so the compiler can tell a read
     // of one from the DMA filling another.
     __shared__ __attribute__((aligned(16))) float lds0[C::BUF0];
-    __shared__ __attribute__((aligned(16))) float lds1[C::XSZ];
-    __shared__ __attribute__((aligned(16))) float lds2[C::NBUF == 3 ? C::XSZ : 1];
+    __shared__ __attribute__((aligned(16))) float lds1[C::SBUF];
+    __shared__ __attribute__((aligned(16))) float lds2[C::NBUF > 2 ? C::SBUF : 1];
+    __shared__ __attribute__((aligned(16))) float lds3[C::NBUF > 3 ? C::SBUF : 1];
+    __shared__ __attribute__((aligned(16))) float lds4[C::NBUF > 4 ? C::SBUF : 1];
+    __shared__ __attribute__((aligned(16))) float lds5[C::NBUF > 5 ? C::SBUF : 1];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -835,7 +1023,10 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
 
     // Weight operand: lane (g, l16) of m-block m holds output channel
     // co0 + wc*16*MA + 16*m + l16, from OIHW or from the prepacked layout.
-    using WS = typename std::conditional<PK, PackedWeights<C>, OihwWeights<C>>::type;
+    // (Weights through LDS read OIHW; a variant's prepacked weights are an
+    // OIHW copy.)
+    using WS = typename std::conditional<C::WL, LdsWeights<C>,
+                                         typename std::conditional<PK, PackedWeights<C>, OihwWeights<C>>::type>::type;
     const int ci_lane = 4 * wk + g;
     WeightCtx wctx;
     wctx.rw = make_rsrc(w, PK ? a.co_tiles.d * (unsigned)a.nchunks * (C::COT * C::CC * C::KK * 4u)
@@ -846,6 +1037,12 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
     wctx.ci_lane = ci_lane;
     wctx.block0 = (co_t * a.nchunks * C::NWK + wk) * C::NWC + wc;
     wctx.lane = lane;
+    wctx.wave = wave;
+    wctx.c_out = a.c_out;
+    wctx.w = w;
+    WlLanes<C> wl_lanes;
+    if constexpr (C::WL) wl_lanes.init(co0, a.c_in, a.c_out, wave, lane);
+    wctx.wl = &wl_lanes;
 
     // The first stage's loads go out before the rest of the set-up: with one
     // wave per SIMD every vector instruction of the set-up costs its full
@@ -853,8 +1050,14 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
     int xo[C::XPT];
     halo_offsets<C>(xo, a, wave, lane, ih0, iw0);
     AStage<C> a0, a1;
+    if constexpr (C::WL) {
+#pragma unroll
+        for (int m = 0; m < C::MA; ++m)
+            a0.base[m] = C::XSZ + (wc * 16 * C::MA + 16 * m + l16) * C::ROW + (4 * wk + g) * C::KKP;
+        a1 = a0;
+    }
     dma_halo<C>(lds0, x, a, c_begin * C::CC, wave, xo);
-    load_a<C>(a0, WS(wctx, a.c_out, c_begin * C::CC));
+    load_a<C>(a0, WS(wctx, a.c_out, c_begin * C::CC, lds0));
     __builtin_amdgcn_sched_barrier(0);
 
     // Input operand: LDS base of each pixel block for this lane.
@@ -884,37 +1087,22 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
     Epilogue<C> ep;
     ep.init(a, out, part, bias, split, co0 + wc * 16 * C::MA + 4 * g, wp, g, l16, oh0, ow0);
 
-    if constexpr (C::NBUF == 3) {
-        // Three buffers: stage ch computes from buffer ch mod 3 while the
-        // loads of stage ch + 2 fill buffer (ch + 2) mod 3, whose last reader
-        // (stage ch - 1) every wave finished before the barrier that ended it.
-        // The prefetch is issued unconditionally: for stages past the last,
-        // every load falls outside its descriptor (zeros into a buffer no
-        // stage reads), which keeps the loop free of branches around loads
-        // -- so that the compiler's own load tracking stays exact across it
-        // and adds no waits of its own.
-        constexpr int kLoads = NextStage<C, WS>::kFull + WS::NA;  // fewest loads any wave issues per stage
-        AStage<C> a2;
-        dma_halo<C>(lds1, x, a, (c_begin + 1) * C::CC, wave, xo);
-        load_a<C>(a1, WS(wctx, a.c_out, (c_begin + 1) * C::CC));
-        stage_ready_keep<kLoads>();
-        // One stage: compute from (xl, A), prefetch stage ch + 2 into (xn, An).
-        auto step = [&](int ch, float *xl, AStage<C> &A, float *xn, AStage<C> &An) -> bool {
-            if (ch + 1 >= c_end) {
-                final_stage<C>(xl, A, b_base, acc, lds0, wave, wk, lane, ep);
-                return true;
-            }
-            NextStage<C, WS> next(xn, An, x, a, wctx, (ch + 2) * C::CC, wave, xo);
-            compute_stage<C>(xl, A, b_base, acc, next);
-            stage_ready_keep<kLoads>();
-            return false;
-        };
-#pragma unroll
-        for (int k = 0; k < C::UNROLL; k += 3) {
-            if (step(c_begin + k, lds0, a0, lds2, a2)) break;
-            if (step(c_begin + k + 1, lds1, a1, lds0, a0)) break;
-            if (step(c_begin + k + 2, lds2, a2, lds1, a1)) break;
-        }
+    if constexpr (C::NBUF > 2) {
+        // A deeper pipeline: stages 1 .. NBUF - 2 are issued now, stage s
+        // issues stage s + NBUF - 1 (see run_stages).
+        AStage<C> ax[4];
+        if constexpr (C::WL) ax[0] = ax[1] = ax[2] = ax[3] = a0;
+        float *const bufs[6] = {lds0, lds1, lds2, lds3, lds4, lds5};
+        AStage<C> *const regs[6] = {&a0, &a1, &ax[0], &ax[1], &ax[2], &ax[3]};
+        constexpr int kAhead = C::NBUF - 2 < C::NS - 1 ? C::NBUF - 2 : C::NS - 1;  // stages issued here
+        for_each_index(std::make_integer_sequence<int, kAhead>{}, [&](auto tc) {
+            constexpr int t = decltype(tc)::value + 1;
+            dma_halo<C>(bufs[t], x, a, (c_begin + t) * C::CC, wave, xo);
+            load_a<C>(*regs[t], WS(wctx, a.c_out, (c_begin + t) * C::CC, bufs[t]));
+        });
+        stage_wait<C, kAhead * kStageLoads<C, WS>()>();
+        run_stages<C, WS>(std::make_integer_sequence<int, C::NS>{}, bufs, regs, x, a, wctx, c_begin, wave, wk, lane,
+                          xo, b_base, acc, ep);
         return;
     }
 
@@ -1073,7 +1261,9 @@ struct Variant {
     const char *name;
     int ks, s, th, tw, nwc, nwp, nwk, ma, cc;
     int nt, cot, lds;
-    int max_stages;  // 0: any number of stages per workgroup
+    int stages;  // 0: any number of stages per workgroup; else exactly this many
+    bool wl;     // weights through LDS: reads OIHW, and its prepacked weights are an OIHW copy
+    int nbuf;    // stage buffers
     void (*launch)(dim3 grid, hipStream_t st, const float *, const float *, const float *, float *, float *,
                    const IgArgs &, bool packed);
 };
@@ -1090,7 +1280,7 @@ template <class C>
 constexpr Variant make_variant(const char *name)
 {
     return Variant{name, C::KS, C::S, C::TH, C::TW, C::NWC, C::NWP, C::NWK, C::MA, C::CC,
-                   C::NT, C::COT, C::LDS_BYTES, C::MAXS, &launch_cfg<C>};
+                   C::NT, C::COT, C::LDS_BYTES, C::NS, C::WL, C::NBUF, &launch_cfg<C>};
 }
 
 //                                  KS S  TH  TW NWC NWP NWK MA CC
@@ -1113,14 +1303,18 @@ const Variant kVariants[] = {
     make_variant<Cfg<3, 1, 4, 4, 1, 1, 4, 1, 32>>("k3s1_t4x4_co16_k4_cc32"),
     make_variant<Cfg<3, 1, 4, 4, 1, 1, 4, 2, 32>>("k3s1_t4x4_co32_k4"),
     make_variant<Cfg<3, 1, 4, 4, 1, 1, 4, 4, 16>>("k3s1_t4x4_co64_k4"),
-    make_variant<Cfg<3, 1, 4, 4, 1, 1, 4, 1, 32, 3>>("k3s1_t4x4_co16_k4_cc32_b3"),
-    make_variant<Cfg<3, 1, 4, 4, 1, 1, 4, 1, 16, 3>>("k3s1_t4x4_co16_k4_cc16_b3"),
-    make_variant<Cfg<3, 1, 4, 4, 1, 1, 4, 2, 32, 3>>("k3s1_t4x4_co32_k4_b3"),
-    make_variant<Cfg<3, 1, 7, 7, 4, 1, 1, 1, 4, 3>>("k3s1_t7x7_co64_cc4_b3"),
+    make_variant<Cfg<3, 1, 4, 4, 1, 1, 4, 1, 16, 3, 4, true>>("k3s1_t4x4_co16_k4_cc16_s4_wl"),
+    make_variant<Cfg<3, 1, 4, 4, 1, 1, 4, 1, 16, 3, 8, true>>("k3s1_t4x4_co16_k4_cc16_s8_wl"),
+    make_variant<Cfg<3, 1, 4, 4, 1, 1, 4, 1, 16, 3, 16, true>>("k3s1_t4x4_co16_k4_cc16_s16_wl"),
+    make_variant<Cfg<3, 1, 4, 4, 1, 1, 4, 1, 32, 3, 8, true>>("k3s1_t4x4_co16_k4_cc32_s8_wl"),
+    make_variant<Cfg<3, 1, 4, 4, 1, 1, 4, 2, 16, 3, 8, true>>("k3s1_t4x4_co32_k4_cc16_s8_wl"),
+    make_variant<Cfg<3, 1, 7, 7, 4, 1, 1, 1, 4, 3, 4>>("k3s1_t7x7_co64_cc4_s4"),
+    make_variant<Cfg<3, 1, 7, 7, 4, 1, 1, 1, 4, 3, 8>>("k3s1_t7x7_co64_cc4_s8"),
     make_variant<Cfg<3, 2, 7, 7, 4, 1, 1, 1, 8>>("k3s2_t7x7_co64"),
     make_variant<Cfg<3, 2, 7, 7, 4, 1, 1, 1, 16>>("k3s2_t7x7_co64_cc16"),
     make_variant<Cfg<3, 2, 7, 7, 4, 1, 4, 1, 16>>("k3s2_t7x7_co64_k4"),
     make_variant<Cfg<3, 2, 4, 4, 1, 1, 4, 1, 64>>("k3s2_t4x4_co16_k4"),
+    make_variant<Cfg<3, 2, 4, 4, 1, 1, 4, 1, 16, 3, 8, true>>("k3s2_t4x4_co16_k4_cc16_s8_wl"),
     make_variant<Cfg<1, 1, 7, 7, 4, 1, 1, 1, 16>>("k1s1_t7x7_co64"),
     make_variant<Cfg<1, 1, 7, 7, 4, 1, 4, 1, 32>>("k1s1_t7x7_co64_k4"),
     make_variant<Cfg<1, 1, 14, 14, 4, 1, 1, 1, 16>>("k1s1_t14x14_co64"),
@@ -1129,6 +1323,8 @@ const Variant kVariants[] = {
     make_variant<Cfg<5, 1, 7, 7, 4, 1, 1, 1, 8>>("k5s1_t7x7_co64_cc8"),
     make_variant<Cfg<5, 1, 7, 7, 4, 1, 2, 1, 8>>("k5s1_t7x7_co64_k2"),
     make_variant<Cfg<5, 1, 4, 4, 1, 1, 4, 1, 32>>("k5s1_t4x4_co16_k4"),
+    make_variant<Cfg<5, 1, 4, 4, 1, 1, 4, 1, 16, 3, 8, true>>("k5s1_t4x4_co16_k4_cc16_s8_wl"),
+    make_variant<Cfg<5, 1, 4, 4, 1, 1, 4, 1, 16, 3, 16, true>>("k5s1_t4x4_co16_k4_cc16_s16_wl"),
 };
 constexpr int kNumVariants = sizeof(kVariants) / sizeof(kVariants[0]);
 
@@ -1149,6 +1345,17 @@ bool igemm_variant_info(int v, int *k, int *stride, int *tile_h, int *tile_w, in
     *tile_h = d.th;
     *tile_w = d.tw;
     *co_tile = d.cot;
+    return true;
+}
+
+bool igemm_variant_pipeline(int v, int *ci_chunk, int *stages, int *buffers, int *flags)
+{
+    if (v < 0 || v >= kNumVariants) return false;
+    const Variant &d = kVariants[v];
+    *ci_chunk = d.cc;
+    *stages = d.stages;
+    *buffers = d.nbuf;
+    *flags = d.wl ? ILPM_VARIANT_WEIGHTS_LDS : 0;
     return true;
 }
 
@@ -1176,11 +1383,13 @@ bool igemm_make_plan(const ConvShape &s, int variant, int splits, ilpm_plan *p)
         splits = 1;
         if (tiles < kCUs) splits = (int)((kCUs + tiles - 1) / tiles);
         if (splits > nchunks) splits = nchunks;
-        if (d.max_stages > 0 && ceil_div(nchunks, splits) > d.max_stages) splits = ceil_div(nchunks, d.max_stages);
+        if (d.stages > 0) splits = nchunks / d.stages;
     }
+    // A fixed-stage variant covers the input channels in whole splits of
+    // exactly its stage count.
+    if (d.stages > 0 && (nchunks % d.stages != 0 || splits * d.stages != nchunks)) return false;
     if (splits > nchunks) return false;
     const int cps = ceil_div(nchunks, splits);
-    if (d.max_stages > 0 && cps > d.max_stages) return false;
     splits = ceil_div(nchunks, cps);  // no empty split
     if (splits > 65535) return false;
     if ((int64_t)tiles * splits > 0x7fffffffL) return false;  // workgroup indices are divided as 31-bit values
@@ -1231,12 +1440,16 @@ double igemm_plan_cost(const ConvShape &s, const ilpm_plan &p)
 int64_t igemm_packed_floats(const ilpm_plan &p, int c_in, int c_out)
 {
     const Variant &d = kVariants[p.variant];
+    if (d.wl) return (int64_t)c_out * c_in * d.ks * d.ks;
     return (int64_t)ceil_div(c_out, d.cot) * ceil_div(c_in, d.cc) * d.cot * d.cc * d.ks * d.ks;
 }
 
 hipError_t igemm_pack(const ilpm_plan &p, int c_in, int c_out, const float *w, float *packed, hipStream_t stream)
 {
     const Variant &d = kVariants[p.variant];
+    if (d.wl)
+        return hipMemcpyAsync(packed, w, sizeof(float) * (size_t)igemm_packed_floats(p, c_in, c_out),
+                              hipMemcpyDeviceToDevice, stream);
     PackGeom g;
     g.c_in = c_in;
     g.c_out = c_out;

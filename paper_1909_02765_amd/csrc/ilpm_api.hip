@@ -341,6 +341,21 @@ int ilpm_variant_info(int path, int variant, int *K, int *stride, int *tile_h, i
     return ILPM_OK;
 }
 
+int ilpm_variant_pipeline(int path, int variant, int *ci_chunk, int *stages, int *buffers, int *flags)
+{
+    int cc = 0, ns = 0, nb = 0, fl = 0;
+    if (path == ILPM_PATH_IGEMM) {
+        if (!igemm_variant_pipeline(variant, &cc, &ns, &nb, &fl)) return ILPM_ERR_INVALID_ARG;
+    } else if (path != ILPM_PATH_DIRECT || variant < 0 || variant >= direct_num_variants()) {
+        return ILPM_ERR_INVALID_ARG;
+    }
+    if (ci_chunk) *ci_chunk = cc;
+    if (stages) *stages = ns;
+    if (buffers) *buffers = nb;
+    if (flags) *flags = fl;
+    return ILPM_OK;
+}
+
 int ilpm_conv2d_workspace_size(int C_in, int H, int W, int C_out, int K, int stride, int pad, size_t *bytes)
 {
     if (!bytes) return ILPM_ERR_INVALID_ARG;

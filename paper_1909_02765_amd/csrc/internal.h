@@ -26,6 +26,7 @@ hipError_t direct_launch(const ilpm_plan &p, const ConvShape &s, const float *x,
 // ---- implicit-GEMM (fp32 MFMA) family ----
 int igemm_num_variants();
 bool igemm_variant_info(int v, int *k, int *stride, int *tile_h, int *tile_w, int *co_tile);
+bool igemm_variant_pipeline(int v, int *ci_chunk, int *stages, int *buffers, int *flags);
 const char *igemm_variant_name(int v);
 // splits = 0 lets the family choose.
 bool igemm_make_plan(const ConvShape &s, int variant, int splits, ilpm_plan *p);

@@ -127,6 +127,34 @@ def test_plan_variant_rules():
         ilpm.plan_variant(8, 14, 14, 64, 3, 1, 1, ilpm.PATH_IGEMM, v33, 2)
 
 
+def test_fixed_stage_variants_plan_whole_splits():
+    """A three-buffer variant is built for an exact stage count: it plans a
+    shape only in splits of exactly that many channel chunks."""
+    fixed = [v for v in range(ilpm.num_variants(ilpm.PATH_IGEMM))
+             if ilpm.variant_info(ilpm.PATH_IGEMM, v)["stages"]]
+    assert fixed
+    for v in fixed:
+        info = ilpm.variant_info(ilpm.PATH_IGEMM, v)
+        k, s, ns, cc = info["k"], info["stride"], info["stages"], info["ci_chunk"]
+        for splits in (1, 2, 3):
+            c_in = ns * cc * splits - cc // 2  # the last chunk half full
+            p = ilpm.plan_variant(c_in, 20, 20, 40, k, s, k // 2, ilpm.PATH_IGEMM, v)
+            assert p.splits == splits
+            p = ilpm.plan_variant(c_in, 20, 20, 40, k, s, k // 2, ilpm.PATH_IGEMM, v, splits)
+            assert p.splits == splits
+            with pytest.raises(ilpm.IlpmError):
+                ilpm.plan_variant(c_in, 20, 20, 40, k, s, k // 2, ilpm.PATH_IGEMM, v, splits + 1)
+        with pytest.raises(ilpm.IlpmError):  # one chunk more than a whole number of splits
+            ilpm.plan_variant(ns * cc + 1, 20, 20, 40, k, s, k // 2, ilpm.PATH_IGEMM, v)
+    for v in range(ilpm.num_variants(ilpm.PATH_DIRECT)):
+        info = ilpm.variant_info(ilpm.PATH_DIRECT, v)
+        assert info["stages"] == 0 and info["buffers"] == 0 and not info["weights_lds"]
+    for v in range(ilpm.num_variants(ilpm.PATH_IGEMM)):
+        info = ilpm.variant_info(ilpm.PATH_IGEMM, v)
+        assert (info["buffers"] > 2) == (info["stages"] > 0)
+        assert info["ci_chunk"] > 0 and info["buffers"] >= 2
+
+
 def test_plan_env_override(monkeypatch):
     monkeypatch.setenv("ILPM_FORCE_PATH", "direct")
     p = ilpm.plan(64, 56, 56, 64, 3, 1, 1)
@@ -175,12 +203,17 @@ def test_prepacked_size():
             info = ilpm.variant_info(ilpm.PATH_IGEMM, v)
             if info["k"] != k or info["stride"] != s:
                 continue
-            p = ilpm.plan_variant(c_in, 16, 16, c_out, k, s, k // 2, ilpm.PATH_IGEMM, v, 1)
+            ci = c_in
+            if info["stages"]:  # a fixed-stage variant: a channel count it takes, last chunk partial
+                ci = info["stages"] * info["ci_chunk"] - 3
+            p = ilpm.plan_variant(ci, 16, 16, c_out, k, s, k // 2, ilpm.PATH_IGEMM, v, 0 if info["stages"] else 1)
             cot, cc = p.co_tile, p.ci_chunk
-            want = -(-c_out // cot) * cot * (-(-c_in // cc) * cc) * k * k * 4
-            assert ilpm.prepacked_size(p, c_in, c_out, k) == want
+            want = -(-c_out // cot) * cot * (-(-ci // cc) * cc) * k * k * 4
+            if info["weights_lds"]:  # such a variant reads OIHW; its prepacked weights are a copy
+                want = c_out * ci * k * k * 4
+            assert ilpm.prepacked_size(p, ci, c_out, k) == want
             with pytest.raises(ilpm.IlpmError):
-                ilpm.prepacked_size(p, c_in, c_out, k + 2)
+                ilpm.prepacked_size(p, ci, c_out, k + 2)
     p = ilpm.plan_variant(3, 16, 16, 8, 7, 1, 3, ilpm.PATH_DIRECT, 0)
     assert ilpm.prepacked_size(p, 3, 8, 7) == 8 * 3 * 49 * 4
 

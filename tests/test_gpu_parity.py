@@ -137,14 +137,21 @@ def test_fuzz_matrix_core_ragged(ilpm):
                 assert_matches(got, ref, sab, c_in, k, f"ragged v={v} {describe(plan)}")
 
 
+def split_variant(ilpm):
+    """A 3x3 stride-1 matrix-core variant that takes any split count."""
+    for v in range(ilpm.num_variants(ilpm.PATH_IGEMM)):
+        if ilpm.variant_name(ilpm.PATH_IGEMM, v) == "k3s1_t7x7_co64_cc4":
+            return v
+    raise AssertionError("variant k3s1_t7x7_co64_cc4 missing")
+
+
 def test_split_reduction_repeats_bitwise(ilpm):
     """A split plan run several times gives identical bits (the partial sums
     are added in a fixed order)."""
     case = workloads.RESNET_CONV4
     x, w, b, ref, sab = case_data(case)
-    p = ilpm.plan(case.c_in, case.h, case.w, case.c_out, case.k, case.stride, case.pad)
-    plan = p if p.splits > 1 else ilpm.plan_variant(case.c_in, case.h, case.w, case.c_out, case.k, case.stride,
-                                                    case.pad, ilpm.PATH_IGEMM, p.variant, 8)
+    plan = ilpm.plan_variant(case.c_in, case.h, case.w, case.c_out, case.k, case.stride, case.pad,
+                             ilpm.PATH_IGEMM, split_variant(ilpm), 8)
     assert plan.splits > 1
     note(f"[repeat] {describe(plan)}")
     outs = [run_conv(x, w, b, case.stride, case.pad, plan=plan) for _ in range(3)]
@@ -157,9 +164,9 @@ def test_registered_workspace(ilpm):
     torch = torch_cuda()
     case = workloads.RESNET_CONV4
     x, w, b, ref, sab = case_data(case)
-    v = ilpm.plan(case.c_in, case.h, case.w, case.c_out, case.k, case.stride, case.pad).variant
     plan = ilpm.plan_variant(case.c_in, case.h, case.w, case.c_out, case.k, case.stride, case.pad,
-                             ilpm.PATH_IGEMM, v, 4)
+                             ilpm.PATH_IGEMM, split_variant(ilpm), 4)
+    assert plan.workspace_bytes > 0
     small = torch.empty(1024, dtype=torch.float32, device="cuda")
     big = torch.empty((plan.workspace_bytes + 3) // 4 + 64, dtype=torch.float32, device="cuda")
     try:
@@ -312,3 +319,32 @@ def test_wide_channels_many_splits(ilpm):
                 note(f"[wide {j}] v={v} {describe(plan)}")
                 got = run_conv(x, w, b, s, p, plan=plan)
                 assert_matches(got, ref, sab, c_in, k, f"wide {j} v={v} {describe(plan)}")
+
+
+def test_fixed_stage_variants_ragged(ilpm):
+    """The three-buffer variants (built for an exact stage count, loads of the
+    stage after next in flight): one and two splits, the last channel chunk
+    partly filled, partial output-channel and spatial tiles, with and without
+    bias; against the oracle, and prepacked weights against OIHW bit for bit."""
+    rng = np.random.default_rng(41)
+    for v in range(ilpm.num_variants(ilpm.PATH_IGEMM)):
+        info = ilpm.variant_info(ilpm.PATH_IGEMM, v)
+        if not info["stages"]:
+            continue
+        k, s, ns, cc = info["k"], info["stride"], info["stages"], info["ci_chunk"]
+        for j, splits in enumerate((1, 2)):
+            c_in = ns * cc * splits - int(rng.integers(0, cc))
+            c_out = int(rng.integers(17, 90))
+            h = int(rng.integers(5, 19))
+            w_ = int(rng.integers(5, 19))
+            p = k // 2
+            x = workloads.uniform(8100 + 10 * v + j, (1, c_in, h, w_), 0.0, 1.0)
+            wt = workloads.normal(8101 + 10 * v + j, (c_out, c_in, k, k), 0.0, workloads.he_std(c_in, k))
+            b = workloads.normal(8102 + 10 * v + j, (c_out,), 0.0, 0.01) if j == 0 else None
+            ref, sab = oracle.conv2d_f64(x, wt, b, s, p)
+            plan = ilpm.plan_variant(c_in, h, w_, c_out, k, s, p, ilpm.PATH_IGEMM, v)
+            assert plan.splits == splits
+            note(f"[fixed-stage] v={v} c_in={c_in} h={h} w={w_} c_out={c_out} {describe(plan)}")
+            got = run_conv(x, wt, b, s, p, plan=plan)
+            assert_matches(got, ref, sab, c_in, k, f"fixed-stage v={v} {describe(plan)}")
+            _prepacked_vs_oihw(ilpm, x, wt, b, s, p, plan, f"fixed-stage v={v}")
