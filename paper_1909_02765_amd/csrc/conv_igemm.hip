@@ -1308,6 +1308,8 @@ const Variant kVariants[] = {
     make_variant<Cfg<3, 1, 4, 4, 1, 1, 4, 1, 16, 3, 16, true>>("k3s1_t4x4_co16_k4_cc16_s16_wl"),
     make_variant<Cfg<3, 1, 4, 4, 1, 1, 4, 1, 32, 3, 8, true>>("k3s1_t4x4_co16_k4_cc32_s8_wl"),
     make_variant<Cfg<3, 1, 4, 4, 1, 1, 4, 2, 16, 3, 8, true>>("k3s1_t4x4_co32_k4_cc16_s8_wl"),
+    make_variant<Cfg<3, 1, 8, 8, 1, 1, 4, 1, 16, 3, 4, true>>("k3s1_t8x8_co16_k4_cc16_s4_wl"),
+    make_variant<Cfg<3, 1, 8, 8, 1, 1, 4, 1, 16, 3, 8, true>>("k3s1_t8x8_co16_k4_cc16_s8_wl"),
     make_variant<Cfg<3, 1, 7, 7, 4, 1, 1, 1, 4, 3, 4>>("k3s1_t7x7_co64_cc4_s4"),
     make_variant<Cfg<3, 1, 7, 7, 4, 1, 1, 1, 4, 3, 8>>("k3s1_t7x7_co64_cc4_s8"),
     make_variant<Cfg<3, 2, 7, 7, 4, 1, 1, 1, 8>>("k3s2_t7x7_co64"),
@@ -1324,6 +1326,7 @@ const Variant kVariants[] = {
     make_variant<Cfg<5, 1, 7, 7, 4, 1, 2, 1, 8>>("k5s1_t7x7_co64_k2"),
     make_variant<Cfg<5, 1, 4, 4, 1, 1, 4, 1, 32>>("k5s1_t4x4_co16_k4"),
     make_variant<Cfg<5, 1, 4, 4, 1, 1, 4, 1, 16, 3, 8, true>>("k5s1_t4x4_co16_k4_cc16_s8_wl"),
+    make_variant<Cfg<5, 1, 8, 8, 1, 1, 4, 1, 16, 3, 4, true>>("k5s1_t8x8_co16_k4_cc16_s4_wl"),
     make_variant<Cfg<5, 1, 4, 4, 1, 1, 4, 1, 16, 3, 16, true>>("k5s1_t4x4_co16_k4_cc16_s16_wl"),
 };
 constexpr int kNumVariants = sizeof(kVariants) / sizeof(kVariants[0]);
