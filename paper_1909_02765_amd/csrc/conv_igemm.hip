@@ -141,11 +141,11 @@ struct Cfg {
     // ROW/4 odd puts the eight lanes of each 128-byte pass of such a read on
     // different banks.
     static constexpr bool WL = WL_;
-    static_assert(!WL || (NWK > 1 && !TAIL4), "weights through LDS: channel-split tiles");
+
     static constexpr int KKP = (KK + 3) / 4 * 4;
     static constexpr int ROW = (CC * KKP + 4) / 8 * 8 + 4;  // >= CC*KKP, = 4 mod 8
-    static constexpr int WSZ = WL ? (COT * ROW + 255) / 256 * 256 : 0;
-    static constexpr int NIXW = WSZ / 256;  // weight DMA instructions per stage (64 lanes x 4 words)
+    static constexpr int NIXW = WL ? (COT * ROW + 255) / 256 : 0;  // weight DMA instructions (64 lanes x 4 words)
+    static constexpr int WSZ = WL ? NIXW * 256 : 0;
     static constexpr int SBUF = XSZ + WSZ;  // one stage buffer: halo, then weights
     // LDS for the cross-wave sum of the NWK partial accumulators.
     static constexpr int RED = (NWK - 1) * NWC * NWP * MA * NB * 4 * 64;
@@ -377,7 +377,7 @@ struct LdsWeights {
     static constexpr int NA_MIN = kFullW;
     __amdgpu_buffer_rsrc_t rw;
     const WlLanes<C> *lanes;
-    float *dst;  // the stage buffer's weight area
+    float *dst;  // the stage buffer's weight area, after its halo
     int lim;     // C_in - ci0: the stage's input channels that exist
     int wave;
 
@@ -599,6 +599,7 @@ __device__ __forceinline__ void compute_stage(const float *xl, const AStage<C> &
     constexpr int kRate = P::N == 0 ? 1 : (P::N + kHalf - 1) / kHalf;
     float bv[R][C::NB];
     float tb[C::TAIL4 ? kSteps : 1];
+    float ta[C::WL && C::TAIL4 ? C::MA : 1][C::WL && C::TAIL4 ? kSteps : 1];  // the tail burst's A (WL)
     // Weights through LDS: the A operands of taps 4j..4j+3 (piece j) for
     // every m-block and channel group, one 16-byte LDS read each, the next
     // piece read while the current one is used.
@@ -634,6 +635,7 @@ __device__ __forceinline__ void compute_stage(const float *xl, const AStage<C> &
             float a_op;
             if constexpr (C::WL) a_op = ach[j & 1][m][c4][t % 4];
             else a_op = A.v[m][c4][t];
+            if constexpr (C::WL && C::TAIL4) ta[m][st] = a_op;
 #pragma unroll
             for (int n = 0; n < C::NBM; ++n)
                 acc[m][n] = __builtin_amdgcn_mfma_f32_16x16x4f32(a_op, bv[cur][n], acc[m][n], 0, 0, 0);
@@ -655,12 +657,38 @@ __device__ __forceinline__ void compute_stage(const float *xl, const AStage<C> &
         for (int st = 0; st < kSteps; ++st) {
             const int t = st / C::G4, c4 = st % C::G4;
 #pragma unroll
-            for (int m = 0; m < C::MA; ++m)
+            for (int m = 0; m < C::MA; ++m) {
+                float a_op;
+                if constexpr (C::WL) a_op = ta[m][st];
+                else a_op = A.v[m][c4][t];
                 acc[m][C::NB - 1 + st % 4] =
-                    __builtin_amdgcn_mfma_f32_4x4x1f32(A.v[m][c4][t], tb[st], acc[m][C::NB - 1 + st % 4], 0, 0, 0);
+                    __builtin_amdgcn_mfma_f32_4x4x1f32(a_op, tb[st], acc[m][C::NB - 1 + st % 4], 0, 0, 0);
+            }
         }
         __builtin_amdgcn_sched_barrier(0);
     }
+}
+
+// Weights through LDS: all of a stage's A operands of this lane, from the
+// stage buffer into registers (the last stage of a one-group-per-wave plan
+// walks its steps once per pixel group).
+template <class C>
+__device__ __forceinline__ void load_stage_a(const float *xl, const AStage<C> &A,
+                                             float (&av)[C::MA][C::G4][C::KK])
+{
+#pragma unroll
+    for (int m = 0; m < C::MA; ++m)
+#pragma unroll
+        for (int c4 = 0; c4 < C::G4; ++c4) {
+            const float *src = xl + A.base[m] + c4 * 4 * C::NWK * C::KKP;
+#pragma unroll
+            for (int j = 0; j < C::KKP / 4; ++j) {
+                const floatx4 v = *reinterpret_cast<const floatx4 *>(src + 4 * j);
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (4 * j + e < C::KK) av[m][c4][4 * j + e] = v[e];
+            }
+        }
 }
 
 // acc[m][NB-1] = the sum of the four tail accumulators, in a fixed order.
@@ -794,6 +822,8 @@ __device__ __forceinline__ void compute_stage_streamed(const float *xl, const AS
     constexpr int kDeferred = kGroupStores + kTailStores;
     constexpr int kStoreRate = (kDeferred + kSteps - 1) / kSteps;
     float bv[2][GB];
+    float avs[C::WL ? C::MA : 1][C::WL ? C::G4 : 1][C::WL ? C::KK : 1];
+    if constexpr (C::WL) load_stage_a<C>(xl, A, avs);
     // The tail block's B values, read alongside group 0's (one more LDS read
     // per step) so that its instructions run back to back: a group of its
     // own would wait on an LDS read every ~10-cycle instruction.
@@ -836,8 +866,12 @@ __device__ __forceinline__ void compute_stage_streamed(const float *xl, const AS
 #pragma unroll
                 for (int j = 0; j < GB; ++j) {
                     const int n = grp * GB + j;
-                    if (n < C::NBM)
-                        acc[m][n] = __builtin_amdgcn_mfma_f32_16x16x4f32(A.v[m][c4][t], bv[cur][j], acc[m][n], 0, 0, 0);
+                    if (n < C::NBM) {
+                        float a_op;
+                        if constexpr (C::WL) a_op = avs[m][c4][t];
+                        else a_op = A.v[m][c4][t];
+                        acc[m][n] = __builtin_amdgcn_mfma_f32_16x16x4f32(a_op, bv[cur][j], acc[m][n], 0, 0, 0);
+                    }
                 }
             if (grp > 0) {
 #pragma unroll
@@ -851,9 +885,13 @@ __device__ __forceinline__ void compute_stage_streamed(const float *xl, const AS
             for (int st = 0; st < kSteps; ++st) {
                 const int t = st / C::G4, c4 = st % C::G4;
 #pragma unroll
-                for (int m = 0; m < C::MA; ++m)
+                for (int m = 0; m < C::MA; ++m) {
+                    float a_op;
+                    if constexpr (C::WL) a_op = avs[m][c4][t];
+                    else a_op = A.v[m][c4][t];
                     acc[m][C::NB - 1 + st % 4] =
-                        __builtin_amdgcn_mfma_f32_4x4x1f32(A.v[m][c4][t], tb[st], acc[m][C::NB - 1 + st % 4], 0, 0, 0);
+                        __builtin_amdgcn_mfma_f32_4x4x1f32(a_op, tb[st], acc[m][C::NB - 1 + st % 4], 0, 0, 0);
+                }
             }
             fold_tail<C>(acc);
             __builtin_amdgcn_sched_barrier(0);
@@ -1296,6 +1334,7 @@ const Variant kVariants[] = {
     make_variant<Cfg<3, 1, 14, 14, 4, 1, 1, 1, 4>>("k3s1_t14x14_co64_cc4"),
     make_variant<Cfg<3, 1, 7, 7, 4, 1, 1, 1, 4>>("k3s1_t7x7_co64_cc4"),
     make_variant<Cfg<3, 1, 7, 7, 4, 1, 1, 1, 8>>("k3s1_t7x7_co64"),
+    make_variant<Cfg<3, 1, 7, 7, 4, 1, 1, 1, 8, 2, 0, true>>("k3s1_t7x7_co64_wl"),
     make_variant<Cfg<3, 1, 7, 7, 4, 1, 1, 1, 16>>("k3s1_t7x7_co64_cc16"),
     make_variant<Cfg<3, 1, 7, 7, 4, 1, 4, 1, 16>>("k3s1_t7x7_co64_k4"),
     make_variant<Cfg<3, 1, 8, 32, 2, 2, 1, 2, 8>>("k3s1_t8x32_co64"),
