@@ -167,10 +167,14 @@ int ilpm_variant_info(int path, int variant, int *K, int *stride, int *tile_h, i
  * buffers: the loads of later stages fly while earlier ones compute, and
  * the stage sequence is unrolled at compile time) plans only shapes whose
  * ceil(C_in / ci_chunk) is a whole multiple of `stages`, with exactly
- * ceil(C_in / ci_chunk) / stages splits.  Pure host; ILPM_ERR_INVALID_ARG
- * for an unknown variant.  Any output pointer may be NULL.
+ * ceil(C_in / ci_chunk) / stages splits.  A variant with a progressive
+ * first stage (its first stage's matrix work starts once its first four
+ * input channels have landed) plans only splits of at least two stages each.
+ * Pure host; ILPM_ERR_INVALID_ARG for an unknown variant.  Any output pointer
+ * may be NULL.
  */
-#define ILPM_VARIANT_WEIGHTS_LDS 1   /* weights staged through LDS from OIHW; prepacked weights are an OIHW copy */
+#define ILPM_VARIANT_WEIGHTS_LDS 1       /* weights staged through LDS from OIHW; prepacked weights are an OIHW copy */
+#define ILPM_VARIANT_PROGRESSIVE_FIRST 2 /* progressive first stage: at least two stages per split */
 int ilpm_variant_pipeline(int path, int variant, int *ci_chunk, int *stages, int *buffers, int *flags);
 
 /*

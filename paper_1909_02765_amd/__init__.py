@@ -27,6 +27,7 @@ ERR_ARCH = -5
 PATH_DIRECT = 0
 PATH_IGEMM = 1
 VARIANT_WEIGHTS_LDS = 1   # ilpm_variant_pipeline flags
+VARIANT_PROGRESSIVE_FIRST = 2
 
 
 class IlpmError(RuntimeError):
@@ -178,7 +179,8 @@ def variant_info(path: int, variant: int):
     _check(lib.ilpm_variant_pipeline(path, variant, *(ctypes.byref(v) for v in (cc, ns, nb, fl))),
            "ilpm_variant_pipeline")
     return dict(k=k, stride=s, tile_h=th, tile_w=tw, co_tile=co, ci_chunk=cc.value, stages=ns.value,
-                buffers=nb.value, weights_lds=bool(fl.value & VARIANT_WEIGHTS_LDS))
+                buffers=nb.value, weights_lds=bool(fl.value & VARIANT_WEIGHTS_LDS),
+                progressive_first=bool(fl.value & VARIANT_PROGRESSIVE_FIRST))
 
 
 def workspace_size(c_in, h, w, c_out, k, stride=1, pad=0) -> int:

@@ -71,7 +71,7 @@ constexpr int round64(int n) { return (n + 63) / 64 * 64; }
 constexpr int cmax(int a, int b) { return a > b ? a : b; }
 
 template <int KS_, int S_, int TH_, int TW_, int NWC_, int NWP_, int NWK_, int MA_, int CC_, int NBUF_ = 2, int NS_ = 0,
-          bool WL_ = false>
+          bool WL_ = false, bool PF_ = false>
 struct Cfg {
     static constexpr int KS = KS_, S = S_, TH = TH_, TW = TW_;
     static constexpr int NWC = NWC_, NWP = NWP_, NWK = NWK_, MA = MA_, CC = CC_;
@@ -150,7 +150,17 @@ struct Cfg {
     // LDS for the cross-wave sum of the NWK partial accumulators.
     static constexpr int RED = (NWK - 1) * NWC * NWP * MA * NB * 4 * 64;
     static constexpr int BUF0 = cmax(SBUF, RED);
-    static constexpr int LDS_BYTES = (BUF0 + (NBUF - 1) * SBUF) * 4;
+    // Progressive first stage (PF): the first stage's halo goes to buffers of
+    // its own, one per group of four channels (GSZ words each), and its
+    // weights to registers group by group, so that its matrix work starts
+    // once the first group has landed instead of the whole stage.  Every
+    // workgroup issues its first loads at the same moment, so that first
+    // stage is bound by the memory system's bandwidth, not its latency.
+    static constexpr bool PF = PF_;
+    static_assert(!PF || (QUAD && NW == 4 && NWK == 1 && MA == 1 && !WL && NBUF == 2 && G4 >= 2 && G4 <= 4),
+                  "progressive first stage: four-row halo DMA, one channel group per wave, two buffers");
+    static constexpr int GSZ = 4 * PL;
+    static constexpr int LDS_BYTES = (BUF0 + (NBUF - 1) * SBUF + (PF ? G4 * GSZ : 0)) * 4;
     static_assert(CC % (4 * NWK) == 0, "a stage holds whole groups of 4 channels per wave");
     static_assert(LDS_BYTES <= 160 * 1024, "LDS budget of one compute unit");
     static_assert(NT <= 1024, "workgroup size");
@@ -245,6 +255,8 @@ struct OihwWeights {
     static constexpr int kPieces = C::KK / 4 + C::KK % 4;
     static constexpr int NA = C::G4 * C::MA * kPieces;
     static constexpr int NA_MIN = NA;  // issued by every wave
+    // The last load (in issue order) of channel group c's registers.
+    static constexpr int group_last(int c) { return (c + 1) * C::MA * kPieces - 1; }
     __amdgpu_buffer_rsrc_t rw;
     unsigned a_base[C::G4][C::MA];
 
@@ -303,6 +315,13 @@ struct PackedWeights {
     static constexpr int N4 = EPL / 4, REM = EPL % 4;
     static constexpr int NA = N4 + REM;
     static constexpr int NA_MIN = NA;
+    // The last load (in issue order) of channel group c's registers (one
+    // m-block: group c is elements KK*c .. KK*c + KK - 1).
+    static constexpr int group_last(int c)
+    {
+        const int e = C::KK * (c + 1) - 1;
+        return e < 4 * N4 ? e / 4 : N4 + (e - 4 * N4);
+    }
     __amdgpu_buffer_rsrc_t rw;
     unsigned base;  // bytes: this wave's block for the stage
 
@@ -443,15 +462,19 @@ __device__ __forceinline__ void halo_offsets(int (&xo)[C::XPT], const IgArgs &a,
     }
 }
 
-// Issue the halo DMA of the stage starting at input channel ci0 into `buf`.
-// Channels at or past C_in lie past the descriptor's end and read 0.
-template <class C>
-__device__ __forceinline__ void dma_halo(float *buf, const float *__restrict__ x, const IgArgs &a, int ci0, int wave,
-                                         const int (&xo)[C::XPT])
+// The input from channel ci0 on, as a buffer descriptor: channels at or past
+// C_in lie past its end and read 0.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t halo_rsrc(const float *__restrict__ x, const IgArgs &a, int ci0)
 {
     const unsigned plane = (unsigned)a.h * (unsigned)a.w;
-    const __amdgpu_buffer_rsrc_t rx =
-        make_rsrc(x + (size_t)ci0 * plane, ci0 < a.c_in ? (unsigned)(a.c_in - ci0) * plane * 4u : 0u);
+    return make_rsrc(x + (size_t)ci0 * plane, ci0 < a.c_in ? (unsigned)(a.c_in - ci0) * plane * 4u : 0u);
+}
+
+// Issue the halo DMA of a stage (descriptor rx from halo_rsrc) into `buf`.
+template <class C>
+__device__ __forceinline__ void dma_halo(float *buf, const __amdgpu_buffer_rsrc_t &rx, int wave,
+                                         const int (&xo)[C::XPT])
+{
     constexpr int kFull = C::NIX / C::NW;  // rounds in which every wave issues one
 #pragma unroll
     for (int j = 0; j < kFull; ++j)
@@ -669,6 +692,136 @@ __device__ __forceinline__ void compute_stage(const float *xl, const AStage<C> &
     }
 }
 
+// f(integral_constant<int, I>) for I = 0, 1, ..., in order.
+template <class F, int... I>
+__device__ __forceinline__ void for_each_index(std::integer_sequence<int, I...>, F &&f)
+{
+    (f(std::integral_constant<int, I>{}), ...);
+}
+
+// Progressive first stage (PF): instruction i < 4 of channel group c's halo
+// DMA, channel 4c + i (with four waves, DMA instruction j of a wave is
+// channel j), into group c's own buffer.
+template <class C>
+__device__ __forceinline__ void dma_group(float *gbuf, const __amdgpu_buffer_rsrc_t &rx, int c, int i, int wave,
+                                          const int (&xo)[C::XPT])
+{
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_ptr_t)(gbuf + i * C::PL + 64 * wave), 4, xo[4 * c + i], 0, 0,
+                                             0);
+}
+
+// The first stage of a PF plan.  Group 0's loads (halo DMA, then weights)
+// were issued before the set-up and have landed; the other groups' loads and
+// then the next stage's are issued here, a few per step over the first half
+// of the stage.  The steps run group by group (every tap of channel group 0,
+// then group 1, ...), and before the first LDS read of group c every wave
+// waits for its own loads of that group -- vector-memory loads complete in
+// issue order, so the count of loads issued after them, known at compile
+// time, is the wait -- and then for the other waves at a barrier.
+template <class C, class WS, class P, class GB>
+__device__ __forceinline__ void first_stage(const GB &gb, const __amdgpu_buffer_rsrc_t &rx, const WS &ws,
+                                            AStage<C> &A, const int (&xo)[C::XPT], int wave,
+                                            const int (&b_base)[C::NB], floatx4 (&acc)[C::MA][C::NACC], P &next)
+{
+    constexpr int kSteps = C::KK * C::G4;
+    constexpr int D = BPipe<C>::D, R = BPipe<C>::R;
+    static_assert(D < C::KK, "a group's first reads follow its wait");
+    static_assert(C::NIX % C::NW == 0 && WS::NA == WS::NA_MIN, "every wave issues every load");
+    static_assert(WS::group_last(C::G4 - 1) == WS::NA - 1, "the groups cover the stage's weights");
+    // Group c's loads: its 4 DMA instructions, then weight loads
+    // group_last(c - 1) + 1 .. group_last(c); done(c) = the loads of groups
+    // 0..c (group 0's were issued before the set-up).
+    constexpr auto first_w = [](int c) { return c == 0 ? 0 : WS::group_last(c - 1) + 1; };
+    constexpr auto done = [](int c) { return 4 * (c + 1) + WS::group_last(c) + 1; };
+    constexpr int NG = done(C::G4 - 1) - done(0);
+    constexpr int NI = NG + P::N;
+    constexpr int kIssueSteps = kSteps / 2;
+    constexpr int kRate = (NI + kIssueSteps - 1) / kIssueSteps;
+    auto issue = [&](int k) {
+        if (k < NG) {
+#pragma unroll
+            for (int c = 1; c < C::G4; ++c) {
+                const int u = k + done(0) - done(c - 1);  // index within group c
+                if (u >= 0 && k + done(0) < done(c)) {
+                    if (u < 4) dma_group<C>(gb(c), rx, c, u, wave, xo);
+                    else ws.load(first_w(c) + (u - 4), A);
+                }
+            }
+        } else if (k < NI) {
+            next.issue(k - NG);
+        }
+    };
+    // Loads this wave issued after group c's, at its wait before step
+    // c*KK - D: group 0's and those of the steps before.
+    auto group_wait = [&](auto cc) {
+        constexpr int c = decltype(cc)::value;
+        constexpr int w = c * C::KK - D;
+        constexpr int issued = done(0) + (w * kRate < NI ? w * kRate : NI);
+        static_assert(issued >= done(c), "a group's loads are issued before its wait");
+        stage_ready_keep<issued - done(c)>();
+    };
+    auto read = [&](int st, float(&bv)[C::NB]) {
+        const int c4 = st / C::KK, t = st % C::KK;
+        const int kh = t / C::KS, kw = t % C::KS;
+        const float *xl = gb(c4);
+#pragma unroll
+        for (int n = 0; n < C::NB; ++n) bv[n] = xl[b_base[n] + kh * C::HCP + kw];
+    };
+    float bv[R][C::NB];
+    float tb[C::TAIL4 ? kSteps : 1];
+#pragma unroll
+    for (int st = 0; st < D; ++st) read(st, bv[st]);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int st = 0; st < kSteps; ++st) {
+        const int cur = st % R;
+        const int c4 = st / C::KK, t = st % C::KK;
+        if (st + D < kSteps && (st + D) % C::KK == 0) {
+            for_each_index(std::make_integer_sequence<int, 4>{}, [&](auto cc) {
+                if constexpr (decltype(cc)::value >= 1 && decltype(cc)::value < C::G4)
+                    if ((st + D) / C::KK == decltype(cc)::value) group_wait(cc);
+            });
+        }
+#pragma unroll
+        for (int r = 0; r < kRate; ++r) {
+            const int k = st * kRate + r;
+            issue(k);
+            // The waits count loads in issue order: no load of a later group
+            // (or of the next stage) may be scheduled before a group's last.
+            bool group_end = false;
+#pragma unroll
+            for (int c = 1; c < C::G4; ++c) group_end |= k + done(0) + 1 == done(c);
+            if (group_end) __builtin_amdgcn_sched_barrier(0);
+        }
+        if (st + D < kSteps) read(st + D, bv[(st + D) % R]);
+#pragma unroll
+        for (int m = 0; m < C::MA; ++m)
+#pragma unroll
+            for (int n = 0; n < C::NBM; ++n)
+                acc[m][n] = __builtin_amdgcn_mfma_f32_16x16x4f32(A.v[m][c4][t], bv[cur][n], acc[m][n], 0, 0, 0);
+        if constexpr (C::TAIL4) tb[st] = bv[cur][C::NB - 1];
+        constexpr int kMf = C::MA * C::NBM;
+        const int n_ds = st + D < kSteps ? C::NB : 0;
+#pragma unroll
+        for (int i = 0; i < (kMf > C::NB ? kMf : C::NB); ++i) {
+            if (i < kMf) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            if (i < n_ds) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    if constexpr (C::TAIL4) {
+#pragma unroll
+        for (int st = 0; st < kSteps; ++st) {
+            const int c4 = st / C::KK, t = st % C::KK;
+#pragma unroll
+            for (int m = 0; m < C::MA; ++m)
+                acc[m][C::NB - 1 + st % 4] =
+                    __builtin_amdgcn_mfma_f32_4x4x1f32(A.v[m][c4][t], tb[st], acc[m][C::NB - 1 + st % 4], 0, 0, 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    }
+}
+
 // Weights through LDS: all of a stage's A operands of this lane, from the
 // stage buffer into registers (the last stage of a one-group-per-wave plan
 // walks its steps once per pixel group).
@@ -716,8 +869,26 @@ struct Epilogue {
 
     __device__ __forceinline__ float fin(float v) const { return relu && v < 0.f ? 0.f : v; }
 
+    // Lane channel co_lane + 16*m + r's bias (zero for partial sums).  A
+    // lane's channels past C_out never store, so their bias is read from the
+    // last channel instead of being masked.
+    __device__ __forceinline__ void load_bias(const IgArgs &a, const float *bias, int co_lane)
+    {
+#pragma unroll
+        for (int m = 0; m < C::MA; ++m)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) b[m][r] = 0.f;
+        if (!a.to_part && bias != nullptr) {
+#pragma unroll
+            for (int m = 0; m < C::MA; ++m)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) b[m][r] = bias[min(co_lane + 16 * m + r, a.c_out - 1)];
+        }
+    }
+
+    // with_bias = false: load_bias was called already.
     __device__ __forceinline__ void init(const IgArgs &a, float *out, float *part, const float *bias, int split,
-                                         int co_lane, int wp, int g, int l16, int oh0, int ow0)
+                                         int co_lane, int wp, int g, int l16, int oh0, int ow0, bool with_bias = true)
     {
         constexpr unsigned kFar = 1u << 30;
         plane_b = (unsigned)a.h_out * a.w_out * 4u;
@@ -743,16 +914,8 @@ struct Epilogue {
             for (int r = 0; r < 4; ++r) {
                 const int co = co_lane + 16 * m + r;
                 chan_off[m][r] = co < a.c_out ? (unsigned)co * plane_b : kFar;
-                b[m][r] = 0.f;
             }
-        // A lane's channels past C_out never store, so their bias is read
-        // from the last channel instead of being masked.
-        if (!a.to_part && bias != nullptr) {
-#pragma unroll
-            for (int m = 0; m < C::MA; ++m)
-#pragma unroll
-                for (int r = 0; r < 4; ++r) b[m][r] = bias[min(co_lane + 16 * m + r, a.c_out - 1)];
-        }
+        if (with_bias) load_bias(a, bias, co_lane);
         if constexpr (C::TAIL4) {
             // co_lane = co_base + 4*g; the tail uses co_base + 4*cg, cg = l16/4.
             tail_co = co_lane - 4 * g + 4 * (l16 >> 2);
@@ -955,13 +1118,6 @@ constexpr int kStageLoads()
     return NextStage<C, WS>::kFull + WS::NA_MIN;
 }
 
-// f(integral_constant<int, I>) for I = 0, 1, ..., in order.
-template <class F, int... I>
-__device__ __forceinline__ void for_each_index(std::integer_sequence<int, I...>, F &&f)
-{
-    (f(std::integral_constant<int, I>{}), ...);
-}
-
 // Loads a wave may leave in flight at the end of stage s (those of stages
 // s + 2 .. s + NBUF - 1 that exist) while stage s + 1's have all landed.
 template <class C, class WS>
@@ -1007,6 +1163,38 @@ __device__ __forceinline__ void run_stages(std::integer_sequence<int, S...>, flo
     for_each_index(std::integer_sequence<int, S...>{}, stage);
 }
 
+// The stages of a two-buffer plan from stage ch (in bA / rA, landed) on:
+// stage s computes from one buffer while the loads of stage s + 1 fill the
+// other, then waits for them; the last stage is the final one.
+template <class C, class WS>
+__device__ __forceinline__ void stage_loop(float *bA, AStage<C> &rA, float *bB, AStage<C> &rB, float *park, int ch,
+                                           int c_end, const float *__restrict__ x, const IgArgs &a,
+                                           const WeightCtx &wctx, int wave, int wk, int lane,
+                                           const int (&xo)[C::XPT], const int (&b_base)[C::NB],
+                                           floatx4 (&acc)[C::MA][C::NACC], const Epilogue<C> &ep)
+{
+    for (;; ch += 2) {
+        if (ch + 1 >= c_end) {
+            final_stage<C>(bA, rA, b_base, acc, park, wave, wk, lane, ep);
+            break;
+        }
+        {
+            NextStage<C, WS> next(bB, rB, x, a, wctx, (ch + 1) * C::CC, wave, xo);
+            compute_stage<C>(bA, rA, b_base, acc, next);
+        }
+        stage_ready();
+        if (ch + 2 >= c_end) {
+            final_stage<C>(bB, rB, b_base, acc, park, wave, wk, lane, ep);
+            break;
+        }
+        {
+            NextStage<C, WS> next(bA, rA, x, a, wctx, (ch + 2) * C::CC, wave, xo);
+            compute_stage<C>(bB, rB, b_base, acc, next);
+        }
+        stage_ready();
+    }
+}
+
 template <class C, bool PK>
 __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x, const float *__restrict__ w,
                                                     const float *__restrict__ bias, float *__restrict__ out,
@@ -1020,6 +1208,12 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
     __shared__ __attribute__((aligned(16))) float lds3[C::NBUF > 3 ? C::SBUF : 1];
     __shared__ __attribute__((aligned(16))) float lds4[C::NBUF > 4 ? C::SBUF : 1];
     __shared__ __attribute__((aligned(16))) float lds5[C::NBUF > 5 ? C::SBUF : 1];
+    // The first stage's channel groups (PF).
+    constexpr bool kPF = C::PF;
+    __shared__ __attribute__((aligned(16))) float gb0[kPF ? C::GSZ : 1];
+    __shared__ __attribute__((aligned(16))) float gb1[kPF ? C::GSZ : 1];
+    __shared__ __attribute__((aligned(16))) float gb2[kPF && C::G4 > 2 ? C::GSZ : 1];
+    __shared__ __attribute__((aligned(16))) float gb3[kPF && C::G4 > 3 ? C::GSZ : 1];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -1094,8 +1288,23 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
             a0.base[m] = C::XSZ + (wc * 16 * C::MA + 16 * m + l16) * C::ROW + (4 * wk + g) * C::KKP;
         a1 = a0;
     }
-    dma_halo<C>(lds0, x, a, c_begin * C::CC, wave, xo);
-    load_a<C>(a0, WS(wctx, a.c_out, c_begin * C::CC, lds0));
+    const WS ws0(wctx, a.c_out, c_begin * C::CC, lds0);
+    Epilogue<C> ep;
+    const __amdgpu_buffer_rsrc_t rx0 = halo_rsrc(x, a, c_begin * C::CC);
+    if constexpr (kPF) {
+        // The bias goes first, so that every load after it belongs to the
+        // first stage or the next (their waits count exactly those); then
+        // channel group 0's halo and weights.
+        ep.load_bias(a, bias, co0 + wc * 16 * C::MA + 4 * g);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) dma_group<C>(gb0, rx0, 0, i, wave, xo);
+#pragma unroll
+        for (int q = 0; q <= WS::group_last(0); ++q) ws0.load(q, a0);
+    } else {
+        dma_halo<C>(lds0, rx0, wave, xo);
+        load_a<C>(a0, ws0);
+    }
     __builtin_amdgcn_sched_barrier(0);
 
     // Input operand: LDS base of each pixel block for this lane.
@@ -1122,8 +1331,7 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
     // Stores go through a buffer descriptor: a lane outside the output (pixel
     // or channel) gets an offset of at least 2^30 bytes, past the descriptor's
     // range (< 2^30, checked when the plan is made), and its store is dropped.
-    Epilogue<C> ep;
-    ep.init(a, out, part, bias, split, co0 + wc * 16 * C::MA + 4 * g, wp, g, l16, oh0, ow0);
+    ep.init(a, out, part, bias, split, co0 + wc * 16 * C::MA + 4 * g, wp, g, l16, oh0, ow0, !kPF);
 
     if constexpr (C::NBUF > 2) {
         // A deeper pipeline: stages 1 .. NBUF - 2 are issued now, stage s
@@ -1135,7 +1343,7 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
         constexpr int kAhead = C::NBUF - 2 < C::NS - 1 ? C::NBUF - 2 : C::NS - 1;  // stages issued here
         for_each_index(std::make_integer_sequence<int, kAhead>{}, [&](auto tc) {
             constexpr int t = decltype(tc)::value + 1;
-            dma_halo<C>(bufs[t], x, a, (c_begin + t) * C::CC, wave, xo);
+            dma_halo<C>(bufs[t], halo_rsrc(x, a, (c_begin + t) * C::CC), wave, xo);
             load_a<C>(*regs[t], WS(wctx, a.c_out, (c_begin + t) * C::CC, bufs[t]));
         });
         stage_wait<C, kAhead * kStageLoads<C, WS>()>();
@@ -1145,26 +1353,21 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
     }
 
     stage_ready();
-
-    for (int ch = c_begin;; ch += 2) {
-        if (ch + 1 >= c_end) {
-            final_stage<C>(lds0, a0, b_base, acc, lds0, wave, wk, lane, ep);
-            break;
-        }
+    if constexpr (kPF) {
+        // At least two stages (checked when the plan is made): the first
+        // from the group buffers, the second from lds1, and so on.
+        // Group c's buffer (c is a constant wherever this is called).
+        auto gb = [&](int c) -> float * { return c == 0 ? gb0 : c == 1 ? gb1 : c == 2 ? gb2 : gb3; };
         {
-            NextStage<C, WS> next(lds1, a1, x, a, wctx, (ch + 1) * C::CC, wave, xo);
-            compute_stage<C>(lds0, a0, b_base, acc, next);
+            NextStage<C, WS> next(lds1, a1, x, a, wctx, (c_begin + 1) * C::CC, wave, xo);
+            first_stage<C>(gb, rx0, ws0, a0, xo, wave, b_base, acc, next);
         }
         stage_ready();
-        if (ch + 2 >= c_end) {
-            final_stage<C>(lds1, a1, b_base, acc, lds0, wave, wk, lane, ep);
-            break;
-        }
-        {
-            NextStage<C, WS> next(lds0, a0, x, a, wctx, (ch + 2) * C::CC, wave, xo);
-            compute_stage<C>(lds1, a1, b_base, acc, next);
-        }
-        stage_ready();
+        stage_loop<C, WS>(lds1, a1, lds0, a0, lds0, c_begin + 1, c_end, x, a, wctx, wave, wk, lane, xo, b_base,
+                          acc, ep);
+    } else {
+        stage_loop<C, WS>(lds0, a0, lds1, a1, lds0, c_begin, c_end, x, a, wctx, wave, wk, lane, xo, b_base, acc,
+                          ep);
     }
 }
 
@@ -1302,6 +1505,7 @@ struct Variant {
     int stages;  // 0: any number of stages per workgroup; else exactly this many
     bool wl;     // weights through LDS: reads OIHW, and its prepacked weights are an OIHW copy
     int nbuf;    // stage buffers
+    bool pf;     // progressive first stage: needs at least two stages per workgroup
     void (*launch)(dim3 grid, hipStream_t st, const float *, const float *, const float *, float *, float *,
                    const IgArgs &, bool packed);
 };
@@ -1318,7 +1522,7 @@ template <class C>
 constexpr Variant make_variant(const char *name)
 {
     return Variant{name, C::KS, C::S, C::TH, C::TW, C::NWC, C::NWP, C::NWK, C::MA, C::CC,
-                   C::NT, C::COT, C::LDS_BYTES, C::NS, C::WL, C::NBUF, &launch_cfg<C>};
+                   C::NT, C::COT, C::LDS_BYTES, C::NS, C::WL, C::NBUF, C::PF, &launch_cfg<C>};
 }
 
 //                                  KS S  TH  TW NWC NWP NWK MA CC
@@ -1329,6 +1533,8 @@ const Variant kVariants[] = {
     make_variant<Cfg<3, 1, 14, 14, 4, 1, 2, 1, 8>>("k3s1_t14x14_co64_w8"),
     make_variant<Cfg<3, 1, 14, 14, 4, 1, 2, 1, 16>>("k3s1_t14x14_co64_w8_cc16"),
     make_variant<Cfg<3, 1, 14, 14, 4, 1, 1, 1, 16>>("k3s1_t14x14_co64_cc16"),
+    make_variant<Cfg<3, 1, 14, 14, 4, 1, 1, 1, 16, 2, 0, false, true>>("k3s1_t14x14_co64_cc16_pf"),
+    make_variant<Cfg<3, 1, 14, 14, 4, 1, 1, 1, 8, 2, 0, false, true>>("k3s1_t14x14_co64_pf"),
     make_variant<Cfg<3, 1, 14, 14, 4, 1, 1, 2, 8>>("k3s1_t14x14_co128"),
     make_variant<Cfg<3, 1, 14, 14, 2, 1, 2, 1, 8>>("k3s1_t14x14_co32_k2"),
     make_variant<Cfg<3, 1, 14, 14, 4, 1, 1, 1, 4>>("k3s1_t14x14_co64_cc4"),
@@ -1397,7 +1603,7 @@ bool igemm_variant_pipeline(int v, int *ci_chunk, int *stages, int *buffers, int
     *ci_chunk = d.cc;
     *stages = d.stages;
     *buffers = d.nbuf;
-    *flags = d.wl ? ILPM_VARIANT_WEIGHTS_LDS : 0;
+    *flags = (d.wl ? ILPM_VARIANT_WEIGHTS_LDS : 0) | (d.pf ? ILPM_VARIANT_PROGRESSIVE_FIRST : 0);
     return true;
 }
 
@@ -1426,6 +1632,7 @@ bool igemm_make_plan(const ConvShape &s, int variant, int splits, ilpm_plan *p)
         if (tiles < kCUs) splits = (int)((kCUs + tiles - 1) / tiles);
         if (splits > nchunks) splits = nchunks;
         if (d.stages > 0) splits = nchunks / d.stages;
+        if (d.pf) splits = splits < nchunks / 2 ? splits : (nchunks / 2 > 0 ? nchunks / 2 : 1);
     }
     // A fixed-stage variant covers the input channels in whole splits of
     // exactly its stage count.
@@ -1433,6 +1640,8 @@ bool igemm_make_plan(const ConvShape &s, int variant, int splits, ilpm_plan *p)
     if (splits > nchunks) return false;
     const int cps = ceil_div(nchunks, splits);
     splits = ceil_div(nchunks, cps);  // no empty split
+    // A progressive first stage is followed by at least one more.
+    if (d.pf && (cps < 2 || nchunks - (splits - 1) * cps < 2)) return false;
     if (splits > 65535) return false;
     if ((int64_t)tiles * splits > 0x7fffffffL) return false;  // workgroup indices are divided as 31-bit values
     const size_t out_elems = (size_t)s.c_out * s.h_out * s.w_out;

@@ -155,6 +155,30 @@ def test_fixed_stage_variants_plan_whole_splits():
         assert info["ci_chunk"] > 0 and info["buffers"] >= 2
 
 
+def test_progressive_first_stage_plans_two_stages_per_split():
+    """A variant with a progressive first stage computes that stage from
+    buffers of its own and goes on to a second: it plans only splits of at
+    least two channel chunks, and its automatic split count keeps that."""
+    pf = [v for v in range(ilpm.num_variants(ilpm.PATH_IGEMM))
+          if ilpm.variant_info(ilpm.PATH_IGEMM, v)["progressive_first"]]
+    assert pf
+    for v in pf:
+        info = ilpm.variant_info(ilpm.PATH_IGEMM, v)
+        k, s, cc = info["k"], info["stride"], info["ci_chunk"]
+        assert info["stages"] == 0 and info["buffers"] == 2 and not info["weights_lds"]
+        with pytest.raises(ilpm.IlpmError):  # one chunk
+            ilpm.plan_variant(cc, 20, 20, 40, k, s, k // 2, ilpm.PATH_IGEMM, v, 1)
+        assert ilpm.plan_variant(cc + 1, 20, 20, 40, k, s, k // 2, ilpm.PATH_IGEMM, v, 1).splits == 1
+        with pytest.raises(ilpm.IlpmError):  # 3 chunks in 2 splits leaves a split of one
+            ilpm.plan_variant(3 * cc, 20, 20, 40, k, s, k // 2, ilpm.PATH_IGEMM, v, 2)
+        assert ilpm.plan_variant(4 * cc, 20, 20, 40, k, s, k // 2, ilpm.PATH_IGEMM, v, 2).splits == 2
+        for c_in in (2 * cc, 5 * cc - 1, 16 * cc):  # few output tiles: the automatic count splits
+            p = ilpm.plan_variant(c_in, 14, 14, 40, k, s, k // 2, ilpm.PATH_IGEMM, v)
+            nchunks = -(-c_in // cc)
+            cps = -(-nchunks // p.splits)
+            assert cps >= 2 and nchunks - (p.splits - 1) * cps >= 2
+
+
 def test_plan_env_override(monkeypatch):
     monkeypatch.setenv("ILPM_FORCE_PATH", "direct")
     p = ilpm.plan(64, 56, 56, 64, 3, 1, 1)
@@ -206,6 +230,8 @@ def test_prepacked_size():
             ci = c_in
             if info["stages"]:  # a fixed-stage variant: a channel count it takes, last chunk partial
                 ci = info["stages"] * info["ci_chunk"] - 3
+            if info["progressive_first"]:  # at least two stages, the last partial
+                ci = max(ci, 2 * info["ci_chunk"] - 3)
             p = ilpm.plan_variant(ci, 16, 16, c_out, k, s, k // 2, ilpm.PATH_IGEMM, v, 0 if info["stages"] else 1)
             cot, cc = p.co_tile, p.ci_chunk
             want = -(-c_out // cot) * cot * (-(-ci // cc) * cc) * k * k * 4

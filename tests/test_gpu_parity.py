@@ -348,3 +348,34 @@ def test_fixed_stage_variants_ragged(ilpm):
             got = run_conv(x, wt, b, s, p, plan=plan)
             assert_matches(got, ref, sab, c_in, k, f"fixed-stage v={v} {describe(plan)}")
             _prepacked_vs_oihw(ilpm, x, wt, b, s, p, plan, f"fixed-stage v={v}")
+
+
+def test_progressive_first_stage_ragged(ilpm):
+    """Variants whose first stage starts computing on its first four channels
+    while the rest land (its halo in buffers of its own, waits counted per
+    channel group): two to five stages, the last channel chunk partly filled,
+    one and two splits, partial spatial and output-channel tiles, with and
+    without bias; against the oracle, and prepacked weights against OIHW bit
+    for bit (the prepacked kernel takes the same summation order)."""
+    rng = np.random.default_rng(43)
+    for v in range(ilpm.num_variants(ilpm.PATH_IGEMM)):
+        info = ilpm.variant_info(ilpm.PATH_IGEMM, v)
+        if not info["progressive_first"]:
+            continue
+        k, s, cc = info["k"], info["stride"], info["ci_chunk"]
+        for j, (stages, splits) in enumerate(((2, 1), (5, 1), (4, 2))):
+            c_in = stages * cc - int(rng.integers(0, cc - 1))
+            c_out = int(rng.integers(17, 140))
+            h = int(rng.integers(9, 45))
+            w_ = int(rng.integers(9, 45))
+            p = k // 2
+            x = workloads.uniform(8300 + 10 * v + j, (1, c_in, h, w_), 0.0, 1.0)
+            wt = workloads.normal(8301 + 10 * v + j, (c_out, c_in, k, k), 0.0, workloads.he_std(c_in, k))
+            b = workloads.normal(8302 + 10 * v + j, (c_out,), 0.0, 0.01) if j != 1 else None
+            ref, sab = oracle.conv2d_f64(x, wt, b, s, p)
+            plan = ilpm.plan_variant(c_in, h, w_, c_out, k, s, p, ilpm.PATH_IGEMM, v, splits)
+            assert plan.splits == splits
+            note(f"[progressive] v={v} c_in={c_in} h={h} w={w_} c_out={c_out} {describe(plan)}")
+            got = run_conv(x, wt, b, s, p, plan=plan)
+            assert_matches(got, ref, sab, c_in, k, f"progressive v={v} {describe(plan)}")
+            _prepacked_vs_oihw(ilpm, x, wt, b, s, p, plan, f"progressive v={v}")
