@@ -758,7 +758,10 @@ __device__ __forceinline__ void first_stage(const GB &gb, const __amdgpu_buffer_
         constexpr int w = c * C::KK - D;
         constexpr int issued = done(0) + (w * kRate < NI ? w * kRate : NI);
         static_assert(issued >= done(c), "a group's loads are issued before its wait");
-        stage_ready_keep<issued - done(c)>();
+        // At most 63 loads are ever in flight (the counter's width; issue
+        // stalls beyond), so with more issued after the group's, waiting for
+        // 63 still leaves the group's loads landed.
+        stage_ready_keep<(issued - done(c) < 63 ? issued - done(c) : 63)>();
     };
     auto read = [&](int st, float(&bv)[C::NB]) {
         const int c4 = st / C::KK, t = st % C::KK;
