@@ -987,7 +987,10 @@ __device__ __forceinline__ void compute_stage_streamed(const float *xl, const AS
     constexpr int kTailStores = C::TAIL4 ? C::MA * 4 : 0;
     constexpr int kDeferred = kGroupStores + kTailStores;
     constexpr int kStoreRate = (kDeferred + kSteps - 1) / kSteps;
-    float bv[2][GB];
+    // B reads run DS steps ahead: a step here has only GB matrix
+    // instructions, too few to cover an LDS read issued one step before.
+    constexpr int DS = 2;
+    float bv[DS + 1][GB];
     float avs[C::WL ? C::MA : 1][C::WL ? C::G4 : 1][C::WL ? C::KK : 1];
     if constexpr (C::WL) load_stage_a<C>(xl, A, avs);
     // The tail block's B values, read alongside group 0's (one more LDS read
@@ -1017,16 +1020,16 @@ __device__ __forceinline__ void compute_stage_streamed(const float *xl, const AS
             ep.store_tail_one(m, r, acc[m][C::NB - 1][r]);
         }
     };
-    read(0, 0, bv[0]);
+#pragma unroll
+    for (int i = 0; i < DS && i < kGroups * kSteps; ++i) read(i / kSteps, i % kSteps, bv[i]);
     __builtin_amdgcn_sched_barrier(0);
-    int cur = 0;
 #pragma unroll
     for (int grp = 0; grp < kGroups; ++grp) {
 #pragma unroll
         for (int st = 0; st < kSteps; ++st) {
             const int t = st / C::G4, c4 = st % C::G4;
-            if (st + 1 < kSteps) read(grp, st + 1, bv[cur ^ 1]);
-            else if (grp + 1 < kGroups) read(grp + 1, 0, bv[cur ^ 1]);
+            const int lin = grp * kSteps + st, cur = lin % (DS + 1), ahead = lin + DS;
+            if (ahead < kGroups * kSteps) read(ahead / kSteps, ahead % kSteps, bv[ahead % (DS + 1)]);
 #pragma unroll
             for (int m = 0; m < C::MA; ++m)
 #pragma unroll
@@ -1044,7 +1047,6 @@ __device__ __forceinline__ void compute_stage_streamed(const float *xl, const AS
                 for (int k = 0; k < kStoreRate; ++k) store_item(grp - 1, st * kStoreRate + k);
             }
             __builtin_amdgcn_sched_barrier(0);
-            cur ^= 1;
         }
         if (C::TAIL4 && grp == 0) {
 #pragma unroll
