@@ -870,18 +870,26 @@ struct Epilogue {
     int tail_co, c_out, relu;
     unsigned tail_pix, plane_b;
 
-    __device__ __forceinline__ float fin(float v) const { return relu && v < 0.f ? 0.f : v; }
+    // RELU: 0 = as the launch says (relu), 1 = no ReLU, 2 = ReLU (the last
+    // stage decides once instead of per store).
+    template <int RELU = 0>
+    __device__ __forceinline__ float fin(float v) const
+    {
+        const bool on = RELU == 0 ? relu != 0 : RELU == 2;
+        return on && v < 0.f ? 0.f : v;
+    }
 
-    // Lane channel co_lane + 16*m + r's bias (zero for partial sums).  A
-    // lane's channels past C_out never store, so their bias is read from the
-    // last channel instead of being masked.
-    __device__ __forceinline__ void load_bias(const IgArgs &a, const float *bias, int co_lane)
+    // Lane channel co_lane + 16*m + r's bias (with partial sums, split 0's
+    // carry it and the others none).  A lane's channels past C_out never
+    // store, so their bias is read from the last channel instead of being
+    // masked.
+    __device__ __forceinline__ void load_bias(const IgArgs &a, const float *bias, int co_lane, int split)
     {
 #pragma unroll
         for (int m = 0; m < C::MA; ++m)
 #pragma unroll
             for (int r = 0; r < 4; ++r) b[m][r] = 0.f;
-        if (!a.to_part && bias != nullptr) {
+        if (bias != nullptr && (!a.to_part || split == 0)) {
 #pragma unroll
             for (int m = 0; m < C::MA; ++m)
 #pragma unroll
@@ -918,7 +926,7 @@ struct Epilogue {
                 const int co = co_lane + 16 * m + r;
                 chan_off[m][r] = co < a.c_out ? (unsigned)co * plane_b : kFar;
             }
-        if (with_bias) load_bias(a, bias, co_lane);
+        if (with_bias) load_bias(a, bias, co_lane, split);
         if constexpr (C::TAIL4) {
             // co_lane = co_base + 4*g; the tail uses co_base + 4*cg, cg = l16/4.
             tail_co = co_lane - 4 * g + 4 * (l16 >> 2);
@@ -930,10 +938,11 @@ struct Epilogue {
         }
     }
 
-    // Row r of 16x16 block (m, n).
+    // Row r of 16x16 block (m, n); the accumulator includes the bias.
+    template <int RELU = 0>
     __device__ __forceinline__ void store_one(int m, int n, int r, float v) const
     {
-        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, fin(v + b[m][r])), ro,
+        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, fin<RELU>(v)), ro,
                                               (int)(chan_off[m][r] + pix_off[n]), 0, 0);
     }
 
@@ -941,6 +950,7 @@ struct Epilogue {
     // partials, lane l getting (v[l] + v[l^16]) + (v[l^32] + v[l^48]) for
     // the first 16 lanes; lane 4*cg + j stores the channels that lanes
     // 16*cg.. hold the bias of.
+    template <int RELU = 0>
     __device__ __forceinline__ void store_tail_one(int m, int r, float v) const
     {
         constexpr unsigned kFar = 1u << 30;
@@ -950,7 +960,7 @@ struct Epilogue {
         const float tb = __shfl(b[m][r], src);
         const int co = tail_co + 16 * m + r;
         const unsigned off = (co < c_out && tail_pix < kFar) ? (unsigned)co * plane_b + tail_pix : kFar;
-        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, fin(s + tb)), ro, (int)off, 0, 0);
+        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, fin<RELU>(s + tb)), ro, (int)off, 0, 0);
     }
 
     __device__ __forceinline__ void store(int m, int n, const floatx4 &v) const
@@ -973,7 +983,7 @@ struct Epilogue {
 // burst is HBM-write bound.)  Four blocks per group keep four independent
 // accumulator chains in flight; the 4x4x1 tail block, if any, follows group
 // 0 as one burst on its four accumulators and is stored with group 0.
-template <class C>
+template <class C, int RELU>
 __device__ __forceinline__ void compute_stage_streamed(const float *xl, const AStage<C> &A,
                                                        const int (&b_base)[C::NB], floatx4 (&acc)[C::MA][C::NACC],
                                                        const Epilogue<C> &ep)
@@ -1014,10 +1024,10 @@ __device__ __forceinline__ void compute_stage_streamed(const float *xl, const AS
         if (i < kGroupStores) {
             const int m = i / (GB * 4), j = (i / 4) % GB, r = i % 4;
             const int n = grp * GB + j;
-            if (n < C::NBM) ep.store_one(m, n, r, acc[m][n][r]);
+            if (n < C::NBM) ep.template store_one<RELU>(m, n, r, acc[m][n][r]);
         } else if (C::TAIL4 && grp == 0 && i < kDeferred) {
             const int m = (i - kGroupStores) / 4, r = (i - kGroupStores) % 4;
-            ep.store_tail_one(m, r, acc[m][C::NB - 1][r]);
+            ep.template store_tail_one<RELU>(m, r, acc[m][C::NB - 1][r]);
         }
     };
 #pragma unroll
@@ -1079,7 +1089,11 @@ __device__ __forceinline__ void final_stage(const float *xl, const AStage<C> &A,
                                             int lane, const Epilogue<C> &ep)
 {
     if constexpr (C::NWK == 1) {
-        compute_stage_streamed<C>(xl, A, b_base, acc, ep);
+        // The ReLU choice is made once here: per store it cost a compare, a
+        // mask and a select (with their register hazards) between the
+        // matrix instructions.
+        if (ep.relu) compute_stage_streamed<C, 2>(xl, A, b_base, acc, ep);
+        else compute_stage_streamed<C, 1>(xl, A, b_base, acc, ep);
     } else {
         NoNextStage none;
         compute_stage<C>(xl, A, b_base, acc, none);
@@ -1300,7 +1314,7 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
         // The bias goes first, so that every load after it belongs to the
         // first stage or the next (their waits count exactly those); then
         // channel group 0's halo and weights.
-        ep.load_bias(a, bias, co0 + wc * 16 * C::MA + 4 * g);
+        ep.load_bias(a, bias, co0 + wc * 16 * C::MA + 4 * g, split);
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int i = 0; i < 4; ++i) dma_group<C>(gb0, rx0, 0, i, wave, xo);
@@ -1321,12 +1335,6 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
         b_base[nb] = ci_lane * C::PL + (p / C::TW) * C::S * C::HCP + (p % C::TW) * C::S;
     }
 
-    floatx4 acc[C::MA][C::NACC];
-#pragma unroll
-    for (int m = 0; m < C::MA; ++m)
-#pragma unroll
-        for (int n = 0; n < C::NACC; ++n) acc[m][n] = floatx4{0.f, 0.f, 0.f, 0.f};
-
     // Output side, set up before the last stage so that its stores can stream
     // out while the last blocks are still being computed.  Accumulator block
     // (m, n), register r holds output channel co0 + wc*16*MA + 16*m + 4*g + r
@@ -1337,6 +1345,18 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
     // or channel) gets an offset of at least 2^30 bytes, past the descriptor's
     // range (< 2^30, checked when the plan is made), and its store is dropped.
     ep.init(a, out, part, bias, split, co0 + wc * 16 * C::MA + 4 * g, wp, g, l16, oh0, ow0, !kPF);
+
+    // The 16x16x4 blocks' accumulators start from the bias (zero for splits
+    // other than 0, and for the waves wk > 0 whose partials are added to wave
+    // wk = 0's), so the stores need no addition; the 4x4x1 tail block's four k-slice
+    // accumulators start from zero and get the bias when they are summed.
+    floatx4 acc[C::MA][C::NACC];
+#pragma unroll
+    for (int m = 0; m < C::MA; ++m)
+#pragma unroll
+        for (int n = 0; n < C::NACC; ++n)
+            acc[m][n] = (n < C::NBM && wk == 0) ? floatx4{ep.b[m][0], ep.b[m][1], ep.b[m][2], ep.b[m][3]}
+                                                : floatx4{0.f, 0.f, 0.f, 0.f};
 
     if constexpr (C::NBUF > 2) {
         // A deeper pipeline: stages 1 .. NBUF - 2 are issued now, stage s
@@ -1376,8 +1396,8 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
     }
 }
 
-// out[i] = part[0][i] + part[1][i] + ... + part[splits-1][i] + bias[channel(i)]
-// (then max(., 0) with relu), summed in that order.  Each thread owns V
+// out[i] = part[0][i] + part[1][i] + ... + part[splits-1][i] (then max(., 0)
+// with relu), summed in that order; split 0's partial sums carry the bias.  Each thread owns V
 // consecutive outputs (V = 4 when every split slice is 16-byte aligned) and
 // issues the loads of up to kBatch slices before it adds any of them, so the
 // latency of the partial sums (just written by the conv kernel, mostly still
@@ -1419,9 +1439,8 @@ __device__ __forceinline__ T sum_slices(const T *pv, int64_t stride, int64_t i, 
 }
 
 template <int V>
-__global__ __launch_bounds__(128) void sum_splits(const float *__restrict__ part, const float *__restrict__ bias,
-                                                  float *__restrict__ out, int splits, int plane, int64_t total,
-                                                  int relu)
+__global__ __launch_bounds__(128) void sum_splits(const float *__restrict__ part, float *__restrict__ out,
+                                                  int splits, int64_t total, int relu)
 {
     using T = typename VecF<V>::T;
     const int64_t nvec = total / V;
@@ -1433,16 +1452,15 @@ __global__ __launch_bounds__(128) void sum_splits(const float *__restrict__ part
         const float *sv = reinterpret_cast<const float *>(&s);
 #pragma unroll
         for (int e = 0; e < V; ++e) {
-            const float v = sv[e] + (bias ? bias[(i * V + e) / plane] : 0.f);
+            const float v = sv[e];
             o[e] = relu && v < 0.f ? 0.f : v;
         }
     }
 }
 
-// The same sum for the four outputs of each 2x2 window, each plus its bias
-// (and ReLU), then their maximum: out [c][h_out/2][w_out/2].
-__global__ __launch_bounds__(128) void sum_splits_pool(const float *__restrict__ part,
-                                                       const float *__restrict__ bias, float *__restrict__ out,
+// The same sum for the four outputs of each 2x2 window, their maximum, then
+// ReLU: out [c][h_out/2][w_out/2].
+__global__ __launch_bounds__(128) void sum_splits_pool(const float *__restrict__ part, float *__restrict__ out,
                                                        int splits, int c, int h_out, int w_out, int relu)
 {
     const int hp = h_out / 2, wp = w_out / 2;
@@ -1454,13 +1472,12 @@ __global__ __launch_bounds__(128) void sum_splits_pool(const float *__restrict__
         const int r = (int)((i / wp) % hp);
         const int ch = (int)(i / ((int64_t)wp * hp));
         const int64_t base = ((int64_t)ch * h_out + 2 * r) * w_out + 2 * j;
-        const float b = bias ? bias[ch] : 0.f;
-        float m = sum_slices<float>(part, slice, base, splits) + b;
-        float v = sum_slices<float>(part, slice, base + 1, splits) + b;
+        float m = sum_slices<float>(part, slice, base, splits);
+        float v = sum_slices<float>(part, slice, base + 1, splits);
         m = v > m ? v : m;
-        v = sum_slices<float>(part, slice, base + w_out, splits) + b;
+        v = sum_slices<float>(part, slice, base + w_out, splits);
         m = v > m ? v : m;
-        v = sum_slices<float>(part, slice, base + w_out + 1, splits) + b;
+        v = sum_slices<float>(part, slice, base + w_out + 1, splits);
         m = v > m ? v : m;
         out[i] = relu && m < 0.f ? 0.f : m;
     }
@@ -1766,7 +1783,7 @@ hipError_t igemm_launch(const ilpm_plan &p, const ConvShape &s, const float *x, 
         const int64_t total = (int64_t)s.c_out * (s.h_out / 2) * (s.w_out / 2);
         int64_t blocks = (total + 127) / 128;
         if (blocks > 8192) blocks = 8192;
-        hipLaunchKernelGGL(sum_splits_pool, dim3((unsigned)blocks), dim3(128), 0, stream, part, bias, out, p.splits,
+        hipLaunchKernelGGL(sum_splits_pool, dim3((unsigned)blocks), dim3(128), 0, stream, part, out, p.splits,
                            s.c_out, s.h_out, s.w_out, a.relu);
         return hipGetLastError();
     }
@@ -1776,11 +1793,11 @@ hipError_t igemm_launch(const ilpm_plan &p, const ConvShape &s, const float *x, 
     int64_t blocks = (threads + 127) / 128;
     if (blocks > 8192) blocks = 8192;
     if (vec4)
-        hipLaunchKernelGGL(sum_splits<4>, dim3((unsigned)blocks), dim3(128), 0, stream, part, bias, out, p.splits,
-                           s.h_out * s.w_out, total, a.relu);
+        hipLaunchKernelGGL(sum_splits<4>, dim3((unsigned)blocks), dim3(128), 0, stream, part, out, p.splits, total,
+                           a.relu);
     else
-        hipLaunchKernelGGL(sum_splits<1>, dim3((unsigned)blocks), dim3(128), 0, stream, part, bias, out, p.splits,
-                           s.h_out * s.w_out, total, a.relu);
+        hipLaunchKernelGGL(sum_splits<1>, dim3((unsigned)blocks), dim3(128), 0, stream, part, out, p.splits, total,
+                           a.relu);
     return hipGetLastError();
 }
 
