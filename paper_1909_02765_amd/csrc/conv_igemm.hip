@@ -863,7 +863,7 @@ template <class C>
 struct Epilogue {
     __amdgpu_buffer_rsrc_t ro;
     unsigned pix_off[C::NB];   // byte offset of each pixel block's lane pixel
-    unsigned chan_off[C::MA][4];
+    unsigned chan_off[C::MA];  // byte offset of output channel co_lane + 16*m (row 0 of the m-block)
     float b[C::MA][4];
     // The 4x4x1 tail block (TAIL4): after the k-slice sum, lane 4*cg + j of
     // the first 16 stores channels tail_co + 16*m + r, r = 0..3, at pixel j.
@@ -920,12 +920,10 @@ struct Epilogue {
             pix_off[n] = ok ? obase + (unsigned)(__mul24(q, a.w_out) + r) * 4u : kFar;
         }
 #pragma unroll
-        for (int m = 0; m < C::MA; ++m)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int co = co_lane + 16 * m + r;
-                chan_off[m][r] = co < a.c_out ? (unsigned)co * plane_b : kFar;
-            }
+        for (int m = 0; m < C::MA; ++m) {
+            const int co = co_lane + 16 * m;
+            chan_off[m] = co < a.c_out ? (unsigned)co * plane_b : kFar;
+        }
         if (with_bias) load_bias(a, bias, co_lane, split);
         if constexpr (C::TAIL4) {
             // co_lane = co_base + 4*g; the tail uses co_base + 4*cg, cg = l16/4.
@@ -938,12 +936,15 @@ struct Epilogue {
         }
     }
 
-    // Row r of 16x16 block (m, n); the accumulator includes the bias.
+    // Row r of 16x16 block (m, n); the accumulator includes the bias.  Row r
+    // is channel + r: r planes go into the scalar offset, so the four rows
+    // share one vector offset.  A channel at or past C_out lies at or past
+    // the descriptor's end (C_out planes), so its store is dropped.
     template <int RELU = 0>
     __device__ __forceinline__ void store_one(int m, int n, int r, float v) const
     {
         __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, fin<RELU>(v)), ro,
-                                              (int)(chan_off[m][r] + pix_off[n]), 0, 0);
+                                              (int)(chan_off[m] + pix_off[n]), (int)(r * plane_b), 0);
     }
 
     // Row r of the 4x4x1 tail block of m-block m: sum the four k-slice
