@@ -85,9 +85,12 @@ typedef struct ilpm_plan {
  *   stride >= 1, pad >= 0, all sizes >= 1, H_out >= 1 and W_out >= 1.
  * Picks the kernel with ilpm_conv2d_plan.  Plans with splits > 1 write
  * per-split partial outputs to the device workspace (registered with
- * ilpm_set_workspace, else allocated by the library on first need) and sum
- * them in a second kernel on the same stream; calls that overlap in time on
- * one device and both use split plans must be ordered on one stream.
+ * ilpm_set_workspace, else allocated by the library on first need); the
+ * last workgroup of each output tile sums them in split order (or a second
+ * kernel on the same stream does, see ilpm_set_split_sum).  Such plans also
+ * use a per-device array of tile arrival counts that the library holds; calls
+ * that overlap in time on one device and both use split plans must be
+ * ordered on one stream.
  * Returns ILPM_OK or a negative status.
  */
 int ilpm_conv2d_fwd(const float *in, const float *w, const float *bias,
@@ -110,6 +113,21 @@ int ilpm_conv2d_workspace_size(int C_in, int H, int W, int C_out, int K, int str
  * `stream` is unused (kept for ABI stability).
  */
 int ilpm_set_workspace(void *ptr, size_t bytes, hipStream_t stream);
+
+/*
+ * ilpm_set_split_sum -- how split plans (splits > 1) sum their per-split
+ * partial outputs, for every later call in the process (Section 4's
+ * accumulation over input channels, split across workgroups):
+ *   ILPM_SPLIT_SUM_FUSED  (default) the last of a tile's workgroups to finish
+ *                         sums the tile's slices; one launch per call.
+ *   ILPM_SPLIT_SUM_KERNEL a second kernel sums all slices after the first.
+ * Both add the slices in split order, so their outputs are bit-identical.
+ * The 2x2 max-pool epilogue always uses the second kernel.  Returns
+ * ILPM_ERR_INVALID_ARG for any other mode.  Host only.
+ */
+#define ILPM_SPLIT_SUM_FUSED 0
+#define ILPM_SPLIT_SUM_KERNEL 1
+int ilpm_set_split_sum(int mode);
 
 /* Text for a status code (static storage). */
 const char *ilpm_status_str(int status);

@@ -24,6 +24,8 @@ ERR_UNSUPPORTED = -2
 ERR_WORKSPACE = -3
 ERR_HIP = -4
 ERR_ARCH = -5
+SPLIT_SUM_FUSED = 0
+SPLIT_SUM_KERNEL = 1
 PATH_DIRECT = 0
 PATH_IGEMM = 1
 VARIANT_WEIGHTS_LDS = 1   # ilpm_variant_pipeline flags
@@ -87,6 +89,7 @@ _SIGS = {
     "ilpm_conv2d_fwd_plan": ([_vp, _vp, _vp] + [_i] * 7 + [_vp, _plan_p, _vp], _i),
     "ilpm_conv2d_workspace_size": ([_i] * 7 + [ctypes.POINTER(ctypes.c_size_t)], _i),
     "ilpm_set_workspace": ([_vp, ctypes.c_size_t, _vp], _i),
+    "ilpm_set_split_sum": ([_i], _i),
     "ilpm_status_str": ([_i], ctypes.c_char_p),
     "ilpm_last_hip_error": ([], _i),
     "ilpm_conv2d_validate": ([_vp, _vp, _vp] + [_i] * 7 + [_vp], _i),
@@ -199,6 +202,13 @@ def set_workspace(buf=None, stream=None):
     nbytes = buf.numel() * buf.element_size()
     _check(lib.ilpm_set_workspace(ctypes.c_void_p(buf.data_ptr()), nbytes, _stream_handle(stream)),
            "ilpm_set_workspace")
+
+
+def set_split_sum(mode: int):
+    """How split plans sum their partial outputs from now on: SPLIT_SUM_FUSED (the
+    last workgroup of each output tile, the default) or SPLIT_SUM_KERNEL (a second
+    kernel).  Both give bit-identical outputs."""
+    _check(lib.ilpm_set_split_sum(int(mode)), "ilpm_set_split_sum")
 
 
 def conv2d(x, w, bias=None, stride: int = 1, pad: int = 0, out=None, plan: Optional[ilpm_plan] = None,

@@ -37,13 +37,16 @@
 // Work split across workgroups: output tiles (TH x TW pixels x COT channels)
 // and, optionally, `splits` contiguous ranges of input-channel stages.  With
 // splits > 1 (or a pooled epilogue) each workgroup writes its partial output,
-// in the output's own layout, to slice `split` of the workspace, and a second
-// kernel sums the slices in split order and applies bias, ReLU and the pool,
-// so the result does not depend on the order in which workgroups run.
+// in the output's own layout, to slice `split` of the workspace.  The slices
+// are summed in split order, so the result does not depend on the order in
+// which workgroups run: by the last of a tile's workgroups to finish (fused
+// finish: a per-tile arrival count, no second launch), or by a second kernel
+// (the pooled epilogue, and on request).
 //
 // LDS: two stage buffers of the halo [CC][HR][HCP] -- (TH-1)*S+K rows of
 // (TW-1)*S+K pixels -- laid out so that the four channel groups of a step
 // read different banks (see Cfg).
+#include <atomic>
 #include <cmath>
 #include <type_traits>
 #include <utility>
@@ -164,6 +167,23 @@ struct Cfg {
     static_assert(CC % (4 * NWK) == 0, "a stage holds whole groups of 4 channels per wave");
     static_assert(LDS_BYTES <= 160 * 1024, "LDS budget of one compute unit");
     static_assert(NT <= 1024, "workgroup size");
+    // Cache policy of the output stores, and whether the workgroups of a tile
+    // finish the split sum themselves (see FusedSplit).
+    static constexpr int SPOL = 0;
+    static constexpr bool FUSED = false;
+};
+
+// The same configuration for split plans whose tiles sum their own partial
+// sums (finish_split_tile).  The partial sums are stored at device scope
+// (cache policy SC1: written through to where the XCDs' L2 caches are
+// coherent) and read back at device scope, so the workgroup that sums a tile
+// sees the other XCDs' slices without writing back or invalidating whole L2
+// caches.
+constexpr int kPolicyDeviceScope = 16;  // SC1 in a buffer instruction's cache-policy operand
+template <class C>
+struct FusedSplit : C {
+    static constexpr int SPOL = kPolicyDeviceScope;
+    static constexpr bool FUSED = true;
 };
 
 // Unsigned division by a divisor d >= 1 fixed at launch, for dividends below
@@ -193,8 +213,10 @@ struct IgArgs {
     FastDiv ntiles, co_tiles, tiles_w;  // workgroup -> (split, output-channel tile, spatial tile)
     FastDiv sp_tiles;                    // spatial tiles (tiles_h * tiles_w)
     int sp_fast;  // consecutive workgroups take consecutive spatial tiles (else output-channel tiles)
-    int to_part;  // write raw partial sums to slice `split` of the workspace (a finishing kernel follows)
+    int to_part;  // write raw partial sums to slice `split` of the workspace
     int relu;     // otherwise: store max(conv + bias, 0)
+    int splits;   // input-channel splits (workgroups per output tile)
+    int fuse;     // to_part: the tile's last workgroup sums the slices into out (with ReLU)
 };
 
 // Buffer descriptors give branch-free loads: a lane whose element lies in the
@@ -944,7 +966,7 @@ struct Epilogue {
     __device__ __forceinline__ void store_one(int m, int n, int r, float v) const
     {
         __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, fin<RELU>(v)), ro,
-                                              (int)(chan_off[m] + pix_off[n]), (int)(r * plane_b), 0);
+                                              (int)(chan_off[m] + pix_off[n]), (int)(r * plane_b), C::SPOL);
     }
 
     // Row r of the 4x4x1 tail block of m-block m: sum the four k-slice
@@ -961,7 +983,8 @@ struct Epilogue {
         const float tb = __shfl(b[m][r], src);
         const int co = tail_co + 16 * m + r;
         const unsigned off = (co < c_out && tail_pix < kFar) ? (unsigned)co * plane_b + tail_pix : kFar;
-        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, fin<RELU>(s + tb)), ro, (int)off, 0, 0);
+        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, fin<RELU>(s + tb)), ro, (int)off, 0,
+                                                  C::SPOL);
     }
 
     __device__ __forceinline__ void store(int m, int n, const floatx4 &v) const
@@ -1215,6 +1238,87 @@ __device__ __forceinline__ void stage_loop(float *bA, AStage<C> &rA, float *bB, 
     }
 }
 
+// Arrivals per output tile for the fused split sum.  Zero when the module
+// loads; the workgroup that completes a tile puts its count back to zero, so
+// the array is zero again whenever no call is running.
+constexpr int kMaxFusedTiles = 1 << 16;
+// The fused split sum is used when each thread of the finishing workgroup
+// loads at most kFuseMaxLoads partial sums (outputs per thread x splits).
+// Measured on MI355X: with one output of 4 slices per thread it saves the
+// second launch (1x1 512->512 at 7x7: 6.86 -> 6.46 us per call); with 4
+// outputs of 8 slices it costs more than it saves (5x5 at 7x7: 12.95 ->
+// 14.58 us), and larger tiles leave the sum to sum_splits, which spreads it
+// over the whole GPU instead of the tiles' last workgroups.
+constexpr int kFuseElems = 4;  // outputs per thread and pass of the finishing loop
+constexpr int kFuseMaxLoads = 8;
+__device__ unsigned g_split_arrivals[kMaxFusedTiles];
+
+// Fused split sum.  Every workgroup of a tile has stored its partial sums at
+// device scope to slice `split` of `part`; once those stores have completed it
+// counts itself in, and the last of the tile's `splits` workgroups adds the
+// slices in split order (the order and arithmetic of sum_splits, so the
+// values do not depend on which workgroup is last), applies ReLU and writes
+// the tile's outputs.  Its loads are device-scope loads, which see the other
+// workgroups' stores however the XCDs' L2 caches hold them.
+__device__ __forceinline__ float load_device_scope(const float *p)
+{
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+template <class C>
+__device__ __forceinline__ void finish_split_tile(const IgArgs &a, const float *part, float *out, int tile, int co0,
+                                                  int oh0, int ow0, unsigned *last_lds)
+{
+    __builtin_amdgcn_s_waitcnt(0);  // this thread's partial-sum stores have completed
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const unsigned prev = atomicAdd(&g_split_arrivals[tile], 1u);
+        const unsigned last = prev + 1 == (unsigned)a.splits ? 1u : 0u;
+        if (last) atomicExch(&g_split_arrivals[tile], 0u);
+        *last_lds = last;
+    }
+    __syncthreads();
+    if (*last_lds == 0u) return;
+    // Up to kFuseElems outputs per thread and pass, with the loads of all
+    // their slices (kB at a time) in flight before any is added: a pass costs
+    // about one round trip to the shared cache level.
+    constexpr int kTP = C::TH * C::TW;
+    constexpr int kB = 8;
+    const int64_t slice = (int64_t)a.c_out * a.h_out * a.w_out;
+    for (int e0 = threadIdx.x; e0 < C::COT * kTP; e0 += kFuseElems * C::NT) {
+        int64_t off[kFuseElems];
+        bool ok[kFuseElems];
+        float v[kFuseElems];
+#pragma unroll
+        for (int j = 0; j < kFuseElems; ++j) {
+            const int e = e0 + j * C::NT;
+            const int c = e / kTP;
+            const int p = e - c * kTP;
+            const int q = p / C::TW;
+            const int oh = oh0 + q, ow = ow0 + (p - q * C::TW), co = co0 + c;
+            ok[j] = e < C::COT * kTP && co < a.c_out && oh < a.h_out && ow < a.w_out;
+            off[j] = ok[j] ? ((int64_t)co * a.h_out + oh) * a.w_out + ow : 0;
+            v[j] = ok[j] ? load_device_scope(part + off[j]) : 0.f;
+        }
+        for (int k = 1; k < a.splits; k += kB) {
+            float t[kFuseElems][kB];
+#pragma unroll
+            for (int j = 0; j < kFuseElems; ++j)
+#pragma unroll
+                for (int b = 0; b < kB; ++b)
+                    if (ok[j] && k + b < a.splits) t[j][b] = load_device_scope(part + off[j] + (k + b) * slice);
+#pragma unroll
+            for (int j = 0; j < kFuseElems; ++j)
+#pragma unroll
+                for (int b = 0; b < kB; ++b)
+                    if (ok[j] && k + b < a.splits) v[j] += t[j][b];
+        }
+#pragma unroll
+        for (int j = 0; j < kFuseElems; ++j)
+            if (ok[j]) out[off[j]] = a.relu && v[j] < 0.f ? 0.f : v[j];
+    }
+}
+
 template <class C, bool PK>
 __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x, const float *__restrict__ w,
                                                     const float *__restrict__ bias, float *__restrict__ out,
@@ -1234,6 +1338,7 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
     __shared__ __attribute__((aligned(16))) float gb1[kPF ? C::GSZ : 1];
     __shared__ __attribute__((aligned(16))) float gb2[kPF && C::G4 > 2 ? C::GSZ : 1];
     __shared__ __attribute__((aligned(16))) float gb3[kPF && C::G4 > 3 ? C::GSZ : 1];
+    __shared__ unsigned last_arrival[1];  // fused split sum: this workgroup completes its tile
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -1375,6 +1480,7 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
         stage_wait<C, kAhead * kStageLoads<C, WS>()>();
         run_stages<C, WS>(std::make_integer_sequence<int, C::NS>{}, bufs, regs, x, a, wctx, c_begin, wave, wk, lane,
                           xo, b_base, acc, ep);
+        if constexpr (C::FUSED) finish_split_tile<C>(a, part, out, tile, co0, oh0, ow0, last_arrival);
         return;
     }
 
@@ -1395,6 +1501,7 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
         stage_loop<C, WS>(lds0, a0, lds1, a1, lds0, c_begin, c_end, x, a, wctx, wave, wk, lane, xo, b_base, acc,
                           ep);
     }
+    if constexpr (C::FUSED) finish_split_tile<C>(a, part, out, tile, co0, oh0, ow0, last_arrival);
 }
 
 // out[i] = part[0][i] + part[1][i] + ... + part[splits-1][i] (then max(., 0)
@@ -1537,8 +1644,14 @@ template <class C>
 void launch_cfg(dim3 grid, hipStream_t st, const float *x, const float *w, const float *b, float *o, float *ws,
                 const IgArgs &a, bool packed)
 {
-    if (packed) hipLaunchKernelGGL((conv_igemm<C, true>), grid, dim3(C::NT), 0, st, x, w, b, o, ws, a);
-    else hipLaunchKernelGGL((conv_igemm<C, false>), grid, dim3(C::NT), 0, st, x, w, b, o, ws, a);
+    using F = FusedSplit<C>;
+    if (a.fuse) {
+        if (packed) hipLaunchKernelGGL((conv_igemm<F, true>), grid, dim3(C::NT), 0, st, x, w, b, o, ws, a);
+        else hipLaunchKernelGGL((conv_igemm<F, false>), grid, dim3(C::NT), 0, st, x, w, b, o, ws, a);
+    } else {
+        if (packed) hipLaunchKernelGGL((conv_igemm<C, true>), grid, dim3(C::NT), 0, st, x, w, b, o, ws, a);
+        else hipLaunchKernelGGL((conv_igemm<C, false>), grid, dim3(C::NT), 0, st, x, w, b, o, ws, a);
+    }
 }
 
 template <class C>
@@ -1742,6 +1855,17 @@ hipError_t igemm_pack(const ilpm_plan &p, int c_in, int c_out, const float *w, f
     return hipGetLastError();
 }
 
+namespace {
+std::atomic<int> g_split_sum_mode{ILPM_SPLIT_SUM_FUSED};
+}
+
+bool igemm_set_split_sum(int mode)
+{
+    if (mode != ILPM_SPLIT_SUM_FUSED && mode != ILPM_SPLIT_SUM_KERNEL) return false;
+    g_split_sum_mode.store(mode, std::memory_order_relaxed);
+    return true;
+}
+
 size_t igemm_workspace_bytes(const ilpm_plan &p, const ConvShape &s, int epilogue)
 {
     const bool to_part = p.splits > 1 || (epilogue & ILPM_EPI_MAXPOOL2);
@@ -1776,10 +1900,16 @@ hipError_t igemm_launch(const ilpm_plan &p, const ConvShape &s, const float *x, 
     a.to_part = (p.splits > 1 || pool) ? 1 : 0;
     a.relu = relu ? 1 : 0;
     const int tiles = p.grid / p.splits;
+    a.splits = p.splits;
+    a.fuse = (p.splits > 1 && !pool && tiles <= kMaxFusedTiles &&
+              ceil_div(d.cot * d.th * d.tw, d.nt) * p.splits <= kFuseMaxLoads &&
+              g_split_sum_mode.load(std::memory_order_relaxed) == ILPM_SPLIT_SUM_FUSED)
+                 ? 1
+                 : 0;
     float *part = static_cast<float *>(workspace);
     d.launch(dim3(tiles * p.splits), stream, x, w, bias, out, part, a, packed);
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess || !a.to_part) return e;
+    if (e != hipSuccess || !a.to_part || a.fuse) return e;
     if (pool) {
         const int64_t total = (int64_t)s.c_out * (s.h_out / 2) * (s.w_out / 2);
         int64_t blocks = (total + 127) / 128;

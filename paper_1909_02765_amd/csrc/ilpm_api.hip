@@ -387,6 +387,8 @@ int ilpm_conv2d_epilogue_workspace_size(int C_in, int H, int W, int C_out, int K
 
 int ilpm_last_hip_error(void) { return g_last_hip; }
 
+int ilpm_set_split_sum(int mode) { return igemm_set_split_sum(mode) ? ILPM_OK : ILPM_ERR_INVALID_ARG; }
+
 int ilpm_set_workspace(void *ptr, size_t bytes, hipStream_t stream)
 {
     (void)stream;

@@ -41,6 +41,8 @@ hipError_t igemm_launch(const ilpm_plan &p, const ConvShape &s, const float *x, 
                         const float *bias, float *out, void *workspace, hipStream_t stream, bool packed,
                         int epilogue);
 size_t igemm_workspace_bytes(const ilpm_plan &p, const ConvShape &s, int epilogue);
+// ILPM_SPLIT_SUM_* for every later igemm_launch; false for another value.
+bool igemm_set_split_sum(int mode);
 // Floats of the prepacked weights of a variant for C_in, C_out (zero-padded
 // to whole output-channel tiles and input-channel chunks).
 int64_t igemm_packed_floats(const ilpm_plan &p, int c_in, int c_out);

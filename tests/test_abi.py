@@ -304,3 +304,16 @@ def test_winograd_sizes_and_argument_checks():
     assert lib.ilpm_conv2d_fwd_winograd(0x1002, 0x100000, None, 3, 8, 8, 4, 1, 0x200000, None) == ilpm.ERR_INVALID_ARG
     assert lib.ilpm_conv2d_fwd_winograd(0x1000, 0x100000, None, 3, 1, 8, 4, 0, 0x200000, None) == ilpm.ERR_INVALID_ARG
     assert lib.ilpm_winograd_transform_filter(0x1000, 3, 4, 0x1000 + 64, None) == ilpm.ERR_INVALID_ARG  # overlap
+
+
+def test_split_sum_mode_switch():
+    """The two split-sum modes are accepted (host only, no launch); any other is refused."""
+    try:
+        assert ilpm.lib.ilpm_set_split_sum(ilpm.SPLIT_SUM_KERNEL) == ilpm.OK
+        assert ilpm.lib.ilpm_set_split_sum(ilpm.SPLIT_SUM_FUSED) == ilpm.OK
+        for bad in (-1, 2, 99):
+            assert ilpm.lib.ilpm_set_split_sum(bad) == ilpm.ERR_INVALID_ARG
+            with pytest.raises(ilpm.IlpmError):
+                ilpm.set_split_sum(bad)
+    finally:
+        ilpm.set_split_sum(ilpm.SPLIT_SUM_FUSED)

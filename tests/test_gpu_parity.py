@@ -379,3 +379,68 @@ def test_progressive_first_stage_ragged(ilpm):
             got = run_conv(x, wt, b, s, p, plan=plan)
             assert_matches(got, ref, sab, c_in, k, f"progressive v={v} {describe(plan)}")
             _prepacked_vs_oihw(ilpm, x, wt, b, s, p, plan, f"progressive v={v}")
+
+
+def test_fused_split_sum_matches_kernel_bitwise(ilpm):
+    """The fused split sum (the last workgroup of each tile adds the slices) and
+    the separate split-sum kernel add the same slices in the same order, so
+    every split plan gives the same bits either way.  Shapes alternate between
+    calls, so a tile's arrival count left non-zero by one call would corrupt the
+    next; each fused output is also checked against the oracle, and the ReLU
+    epilogue takes the same path."""
+    torch = torch_cuda()
+    shapes = [(300, 9, 9, 200, 3, 1, 1), (96, 7, 7, 40, 1, 1, 0), (130, 11, 10, 70, 5, 1, 2),
+              (70, 15, 13, 90, 3, 2, 1)]
+    data = []
+    for j, (c_in, h, w_, c_out, k, s, p) in enumerate(shapes):
+        x = workloads.uniform(7100 + 10 * j, (1, c_in, h, w_), 0.0, 1.0)
+        w = workloads.normal(7101 + 10 * j, (c_out, c_in, k, k), 0.0, workloads.he_std(c_in, k))
+        b = workloads.normal(7102 + 10 * j, (c_out,), 0.0, 0.01) if j % 2 == 0 else None
+        ref, sab = oracle.conv2d_f64(x, w, b, s, p)
+        data.append((x, w, b, ref, sab))
+    plans = []
+    for j, (c_in, h, w_, c_out, k, s, p) in enumerate(shapes):
+        for v in range(ilpm.num_variants(ilpm.PATH_IGEMM)):
+            info = ilpm.variant_info(ilpm.PATH_IGEMM, v)
+            if info["k"] != k or info["stride"] != s:
+                continue
+            for splits in (0, 3, 8):
+                try:
+                    plan = ilpm.plan_variant(c_in, h, w_, c_out, k, s, p, ilpm.PATH_IGEMM, v, splits)
+                except ilpm.IlpmError:
+                    continue
+                if plan.splits > 1:
+                    plans.append((j, plan))
+    assert len(plans) >= 8
+    # A registered workspace filled with NaN before every call: a partial sum
+    # read before the workgroup that wrote it has landed shows as NaN.
+    need = max(plan.workspace_bytes for _, plan in plans)
+    ws = torch.empty(need // 4 + 64, device="cuda", dtype=torch.float32)
+    ilpm.set_workspace(ws)
+    try:
+        for mode in (ilpm.SPLIT_SUM_KERNEL, ilpm.SPLIT_SUM_FUSED):
+            ilpm.set_split_sum(mode)
+            outs = []
+            # Interleave shapes: plan i of one shape, then one of another.
+            for j, plan in plans:
+                c_in, h, w_, c_out, k, s, p = shapes[j]
+                x, w, b, ref, sab = data[j]
+                note(f"[split sum mode {mode}] shape {shapes[j]} {describe(plan)}")
+                ws.fill_(float("nan"))
+                got = run_conv(x, w, b, s, p, plan=plan)
+                ws.fill_(float("nan"))
+                relu = ilpm.conv2d_epilogue(dev(x), dev(w), dev(b), s, p, ilpm.EPI_RELU, plan=plan)
+                torch.cuda.synchronize()
+                outs.append((got, relu.cpu().numpy()))
+            if mode == ilpm.SPLIT_SUM_KERNEL:
+                base = outs
+        for (j, plan), (got, relu), (got0, relu0) in zip(plans, outs, base):
+            c_in, _, _, _, k, _, _ = shapes[j]
+            np.testing.assert_array_equal(got, got0, err_msg=f"fused vs kernel {describe(plan)}")
+            np.testing.assert_array_equal(relu, relu0, err_msg=f"fused relu vs kernel {describe(plan)}")
+            np.testing.assert_array_equal(relu, np.maximum(got, 0.0))
+            assert_matches(got, data[j][3], data[j][4], c_in, k, f"fused {describe(plan)}")
+    finally:
+        ilpm.set_split_sum(ilpm.SPLIT_SUM_FUSED)
+        torch.cuda.synchronize()
+        ilpm.set_workspace(None)
