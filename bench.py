@@ -490,10 +490,54 @@ def bench_vgg16_stack(torch, ilpm, workloads, reps):
     t_unfused = timed(launches)
     t_fused = timed(fused)
     same = bool(torch.equal(out_unfused, out_fused))
+    ref = out_fused.clone()
+
+    # The fused stack captured once in a HIP graph and replayed (no host
+    # launch cost between layers); every replay's output is checked against
+    # the eager result.  The eager passes above have sized the workspace, so
+    # the library allocates nothing during capture.
+    stream = torch.cuda.Stream()
+    stream.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(stream):
+        fused_s = []
+        x = x0
+        for (name, ci, co, hw, pool, _), w in zip(layers, ws):
+            epi = ilpm.EPI_RELU | (ilpm.EPI_MAXPOOL2 if pool else 0)
+            y = torch.empty(ilpm.epilogue_out_shape(co, hw, hw, 3, 1, 1, epi), device="cuda", dtype=torch.float32)
+            fused_s.append(ilpm.conv2d_epilogue_launcher(x, w, None, 1, 1, epi, y))
+            x = y
+        out_graph = x
+        for f in fused_s:
+            f()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
+            for f in fused_s:
+                f()
+    torch.cuda.synchronize()
+    graph_same = True
+    for _ in range(3):
+        out_graph.fill_(float("nan"))
+        g.replay()
+        torch.cuda.synchronize()
+        graph_same = graph_same and bool(torch.equal(out_graph, ref))
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        g.replay()
+    b.record()
+    torch.cuda.synchronize()
+    t_graph = a.elapsed_time(b) * 1000.0 / reps
+    out_graph.fill_(float("nan"))
+    g.replay()
+    torch.cuda.synchronize()
+    graph_same = graph_same and bool(torch.equal(out_graph, ref))
     rows = [{"layer": "vgg16_stack_unfused", "us": round(t_unfused, 3),
              "note": "13 convs + 13 ReLU + 4 max-pool kernels, end to end"},
             {"layer": "vgg16_stack_fused", "us": round(t_fused, 3),
-             "note": "13 convs with the fused ReLU / ReLU+max-pool epilogue", "same_output_bits": same}]
+             "note": "13 convs with the fused ReLU / ReLU+max-pool epilogue", "same_output_bits": same},
+            {"layer": "vgg16_stack_fused_graph", "us": round(t_graph, 3),
+             "note": "the fused stack replayed from one captured HIP graph", "same_output_bits": graph_same}]
     for r in rows:
         print(json.dumps(r), file=sys.stderr)
     return rows
