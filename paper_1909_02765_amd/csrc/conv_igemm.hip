@@ -1567,26 +1567,48 @@ __global__ __launch_bounds__(128) void sum_splits(const float *__restrict__ part
 }
 
 // The same sum for the four outputs of each 2x2 window, their maximum, then
-// ReLU: out [c][h_out/2][w_out/2].
-__global__ __launch_bounds__(128) void sum_splits_pool(const float *__restrict__ part, float *__restrict__ out,
-                                                       int splits, int c, int h_out, int w_out, int relu)
+// ReLU: out [c][h_out/2][w_out/2].  One thread per pooled output; its index
+// is split into (channel, row, column) by multiply-and-shift division (a
+// 64-bit divide is a long instruction sequence on the GPU, and three per
+// output made this kernel compute-bound).  With an even w_out each window row
+// is one aligned 8-byte pair (V2).  The values are those of the plain sum
+// and maximum, in the same order.
+template <bool V2>
+__global__ __launch_bounds__(256) void sum_splits_pool(const float *__restrict__ part, float *__restrict__ out,
+                                                       int splits, int c, int h_out, int w_out, FastDiv wp_d,
+                                                       FastDiv hp_d, int relu)
 {
-    const int hp = h_out / 2, wp = w_out / 2;
-    const int64_t total = (int64_t)c * hp * wp;
+    const unsigned hp = (unsigned)h_out / 2, wp = (unsigned)w_out / 2;
+    const unsigned total = (unsigned)c * hp * wp;
     const int64_t slice = (int64_t)c * h_out * w_out;
-    const int64_t step = (int64_t)gridDim.x * 128;
-    for (int64_t i = (int64_t)blockIdx.x * 128 + threadIdx.x; i < total; i += step) {
-        const int j = (int)(i % wp);
-        const int r = (int)((i / wp) % hp);
-        const int ch = (int)(i / ((int64_t)wp * hp));
+    const unsigned step = gridDim.x * 256u;
+    for (unsigned i = blockIdx.x * 256u + threadIdx.x; i < total; i += step) {
+        const unsigned t = fast_div(i, wp_d);
+        const unsigned j = i - t * wp;
+        const unsigned ch = fast_div(t, hp_d);
+        const unsigned r = t - ch * hp;
         const int64_t base = ((int64_t)ch * h_out + 2 * r) * w_out + 2 * j;
-        float m = sum_slices<float>(part, slice, base, splits);
-        float v = sum_slices<float>(part, slice, base + 1, splits);
-        m = v > m ? v : m;
-        v = sum_slices<float>(part, slice, base + w_out, splits);
-        m = v > m ? v : m;
-        v = sum_slices<float>(part, slice, base + w_out + 1, splits);
-        m = v > m ? v : m;
+        float m, v;
+        if constexpr (V2) {
+            const float2 *p2 = reinterpret_cast<const float2 *>(part);
+            const float2 top = sum_slices<float2>(p2, slice / 2, base / 2, splits);
+            const float2 bot = sum_slices<float2>(p2, slice / 2, (base + w_out) / 2, splits);
+            m = top.x;
+            v = top.y;
+            m = v > m ? v : m;
+            v = bot.x;
+            m = v > m ? v : m;
+            v = bot.y;
+            m = v > m ? v : m;
+        } else {
+            m = sum_slices<float>(part, slice, base, splits);
+            v = sum_slices<float>(part, slice, base + 1, splits);
+            m = v > m ? v : m;
+            v = sum_slices<float>(part, slice, base + w_out, splits);
+            m = v > m ? v : m;
+            v = sum_slices<float>(part, slice, base + w_out + 1, splits);
+            m = v > m ? v : m;
+        }
         out[i] = relu && m < 0.f ? 0.f : m;
     }
 }
@@ -1911,11 +1933,17 @@ hipError_t igemm_launch(const ilpm_plan &p, const ConvShape &s, const float *x, 
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || !a.to_part || a.fuse) return e;
     if (pool) {
+        // Pooled outputs number fewer than the output's, which are below 2^31.
         const int64_t total = (int64_t)s.c_out * (s.h_out / 2) * (s.w_out / 2);
-        int64_t blocks = (total + 127) / 128;
+        int64_t blocks = (total + 255) / 256;
         if (blocks > 8192) blocks = 8192;
-        hipLaunchKernelGGL(sum_splits_pool, dim3((unsigned)blocks), dim3(128), 0, stream, part, out, p.splits,
-                           s.c_out, s.h_out, s.w_out, a.relu);
+        const FastDiv wp_d = make_fastdiv((unsigned)(s.w_out / 2)), hp_d = make_fastdiv((unsigned)(s.h_out / 2));
+        if (s.w_out % 2 == 0)
+            hipLaunchKernelGGL(sum_splits_pool<true>, dim3((unsigned)blocks), dim3(256), 0, stream, part, out, p.splits,
+                               s.c_out, s.h_out, s.w_out, wp_d, hp_d, a.relu);
+        else
+            hipLaunchKernelGGL(sum_splits_pool<false>, dim3((unsigned)blocks), dim3(256), 0, stream, part, out,
+                               p.splits, s.c_out, s.h_out, s.w_out, wp_d, hp_d, a.relu);
         return hipGetLastError();
     }
     const int64_t total = (int64_t)s.c_out * s.h_out * s.w_out;
