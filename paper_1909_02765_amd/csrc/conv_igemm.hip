@@ -171,6 +171,12 @@ struct Cfg {
     // finish the split sum themselves (see FusedSplit).
     static constexpr int SPOL = 0;
     static constexpr bool FUSED = false;
+    // A 2x2 max-pool can be applied inside the workgroup (PoolTile) when the
+    // tile's windows do not cross tiles (even TH, TW) and the tile's outputs
+    // fit in LDS beside the stage buffers.
+    static constexpr bool POOL = false;
+    static constexpr int POOL_FLOATS = COT * NPIX;
+    static constexpr bool POOLABLE = TH % 2 == 0 && TW % 2 == 0 && LDS_BYTES + 4 * POOL_FLOATS <= 160 * 1024;
 };
 
 // The same configuration for split plans whose tiles sum their own partial
@@ -184,6 +190,18 @@ template <class C>
 struct FusedSplit : C {
     static constexpr int SPOL = kPolicyDeviceScope;
     static constexpr bool FUSED = true;
+};
+
+// The same configuration with the 2x2 max-pool epilogue done in the
+// workgroup: the last stage writes its results (ReLU applied, when asked) to
+// an LDS copy of the tile instead of the output, in the same order and with
+// the same values, and pool_tile_finish writes the maxima of the tile's 2x2
+// windows.  The result is that of conv -> ReLU -> pool, without writing the
+// full-size output or launching a second kernel.
+template <class C>
+struct PoolTile : C {
+    static_assert(C::POOLABLE, "pooled tiles need even tile sides and LDS room for the tile");
+    static constexpr bool POOL = true;
 };
 
 // Unsigned division by a divisor d >= 1 fixed at launch, for dividends below
@@ -217,6 +235,7 @@ struct IgArgs {
     int relu;     // otherwise: store max(conv + bias, 0)
     int splits;   // input-channel splits (workgroups per output tile)
     int fuse;     // to_part: the tile's last workgroup sums the slices into out (with ReLU)
+    int pool_tile;  // out is the 2x2 max-pooled output, pooled in the workgroup (PoolTile)
 };
 
 // Buffer descriptors give branch-free loads: a lane whose element lies in the
@@ -891,6 +910,10 @@ struct Epilogue {
     // the first 16 stores channels tail_co + 16*m + r, r = 0..3, at pixel j.
     int tail_co, c_out, relu;
     unsigned tail_pix, plane_b;
+    // POOL: results go to the LDS tile pl [COT][NPIX] (channel co0 + c at
+    // row c); the offsets above then address it in bytes.
+    float *pl;
+    int pool_co0;
 
     // RELU: 0 = as the launch says (relu), 1 = no ReLU, 2 = ReLU (the last
     // stage decides once instead of per store).
@@ -958,6 +981,39 @@ struct Epilogue {
         }
     }
 
+    // POOL: address the LDS tile instead of the output (after init): pixel p
+    // of the tile at byte 4*p, channel co0 + c at byte 4*c*NPIX; pixels
+    // outside the image or the tile and channels past C_out keep the
+    // out-of-range offset and are not written.
+    __device__ __forceinline__ void pool_init(float *tile, int co0, int co_lane, int wp, int g, int l16, int oh0,
+                                              int ow0, const IgArgs &a)
+    {
+        constexpr unsigned kFar = 1u << 30;
+        pl = tile;
+        pool_co0 = co0;
+        plane_b = 4u * C::NPIX;
+        const int rows = a.h_out - oh0, cols = a.w_out - ow0;
+#pragma unroll
+        for (int n = 0; n < C::NB; ++n) {
+            const int p = (wp * C::NB + n) * 16 + l16;
+            const int q = p / C::TW, r = p - q * C::TW;
+            const bool ok = p < C::NPIX && q < rows && r < cols;
+            pix_off[n] = ok ? 4u * p : kFar;
+        }
+#pragma unroll
+        for (int m = 0; m < C::MA; ++m) {
+            const int co = co_lane + 16 * m;
+            chan_off[m] = co < a.c_out ? 4u * (co - co0) * C::NPIX : kFar;
+        }
+        if constexpr (C::TAIL4) {
+            const int j = l16 & 3;
+            const int p = (C::NB - 1) * 16 + j;
+            const int q = p / C::TW, r = p - q * C::TW;
+            const bool lane_stores = g == 0 && j < C::TAILP && q < rows && r < cols;
+            tail_pix = lane_stores ? 4u * p : kFar;
+        }
+    }
+
     // Row r of 16x16 block (m, n); the accumulator includes the bias.  Row r
     // is channel + r: r planes go into the scalar offset, so the four rows
     // share one vector offset.  A channel at or past C_out lies at or past
@@ -965,8 +1021,13 @@ struct Epilogue {
     template <int RELU = 0>
     __device__ __forceinline__ void store_one(int m, int n, int r, float v) const
     {
-        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, fin<RELU>(v)), ro,
-                                              (int)(chan_off[m] + pix_off[n]), (int)(r * plane_b), C::SPOL);
+        if constexpr (C::POOL) {
+            constexpr unsigned kFar = 1u << 30;
+            if ((chan_off[m] | pix_off[n]) < kFar) pl[(chan_off[m] + pix_off[n]) / 4 + r * C::NPIX] = fin<RELU>(v);
+        } else {
+            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, fin<RELU>(v)), ro,
+                                                  (int)(chan_off[m] + pix_off[n]), (int)(r * plane_b), C::SPOL);
+        }
     }
 
     // Row r of the 4x4x1 tail block of m-block m: sum the four k-slice
@@ -982,9 +1043,13 @@ struct Epilogue {
         s += __shfl_xor(s, 32);
         const float tb = __shfl(b[m][r], src);
         const int co = tail_co + 16 * m + r;
-        const unsigned off = (co < c_out && tail_pix < kFar) ? (unsigned)co * plane_b + tail_pix : kFar;
-        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, fin<RELU>(s + tb)), ro, (int)off, 0,
+        if constexpr (C::POOL) {
+            if (co < c_out && tail_pix < kFar) pl[(co - pool_co0) * C::NPIX + tail_pix / 4] = fin<RELU>(s + tb);
+        } else {
+            const unsigned off = (co < c_out && tail_pix < kFar) ? (unsigned)co * plane_b + tail_pix : kFar;
+            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, fin<RELU>(s + tb)), ro, (int)off, 0,
                                                   C::SPOL);
+        }
     }
 
     __device__ __forceinline__ void store(int m, int n, const floatx4 &v) const
@@ -1112,12 +1177,23 @@ __device__ __forceinline__ void final_stage(const float *xl, const AStage<C> &A,
                                             floatx4 (&acc)[C::MA][C::NACC], float *park_area, int wave, int wk,
                                             int lane, const Epilogue<C> &ep)
 {
-    if constexpr (C::NWK == 1) {
+    if constexpr (C::NWK == 1 && !C::POOL) {
         // The ReLU choice is made once here: per store it cost a compare, a
         // mask and a select (with their register hazards) between the
         // matrix instructions.
         if (ep.relu) compute_stage_streamed<C, 2>(xl, A, b_base, acc, ep);
         else compute_stage_streamed<C, 1>(xl, A, b_base, acc, ep);
+    } else if constexpr (C::NWK == 1) {
+        // PoolTile: the results go to LDS, whose queue the matrix steps'
+        // operand reads use; written in one burst after the stage instead of
+        // between its steps.
+        NoNextStage none;
+        compute_stage<C>(xl, A, b_base, acc, none);
+        fold_tail<C>(acc);
+#pragma unroll
+        for (int m = 0; m < C::MA; ++m)
+#pragma unroll
+            for (int n = 0; n < C::NB; ++n) ep.store(m, n, acc[m][n]);
     } else {
         NoNextStage none;
         compute_stage<C>(xl, A, b_base, acc, none);
@@ -1319,6 +1395,39 @@ __device__ __forceinline__ void finish_split_tile(const IgArgs &a, const float *
     }
 }
 
+// PoolTile: every wave has written its results to the LDS tile; each output
+// of the pooled tile is the maximum of its 2x2 window, compared in the order
+// (0,0), (0,1), (1,0), (1,1) as the pool kernels do.  Windows lie inside the
+// tile (even sides, tiles start at even coordinates); a window with any pixel
+// outside the image has no pooled output (floor), and channels past C_out
+// are not written.
+template <class C>
+__device__ __forceinline__ void pool_tile_finish(const float *tile, float *out, const IgArgs &a, int co0, int oh0,
+                                                 int ow0)
+{
+    __syncthreads();
+    constexpr int PH = C::TH / 2, PW = C::TW / 2;
+    const int hp = a.h_out / 2, wpo = a.w_out / 2;
+    const int pi0 = oh0 / 2, pj0 = ow0 / 2;
+    for (int e = threadIdx.x; e < C::COT * PH * PW; e += C::NT) {
+        const int c = e / (PH * PW);
+        const int q = e - c * (PH * PW);
+        const int i = q / PW, j = q - (q / PW) * PW;
+        const int co = co0 + c, pi = pi0 + i, pj = pj0 + j;
+        if (co >= a.c_out || pi >= hp || pj >= wpo) continue;
+        // Even NPIX and TW: each window row is an aligned pair.
+        const float2 top = *reinterpret_cast<const float2 *>(tile + c * C::NPIX + 2 * i * C::TW + 2 * j);
+        const float2 bot = *reinterpret_cast<const float2 *>(tile + c * C::NPIX + (2 * i + 1) * C::TW + 2 * j);
+        float m = top.x, v = top.y;
+        m = v > m ? v : m;
+        v = bot.x;
+        m = v > m ? v : m;
+        v = bot.y;
+        m = v > m ? v : m;
+        out[((int64_t)co * hp + pi) * wpo + pj] = m;
+    }
+}
+
 template <class C, bool PK>
 __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x, const float *__restrict__ w,
                                                     const float *__restrict__ bias, float *__restrict__ out,
@@ -1339,6 +1448,7 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
     __shared__ __attribute__((aligned(16))) float gb2[kPF && C::G4 > 2 ? C::GSZ : 1];
     __shared__ __attribute__((aligned(16))) float gb3[kPF && C::G4 > 3 ? C::GSZ : 1];
     __shared__ unsigned last_arrival[1];  // fused split sum: this workgroup completes its tile
+    __shared__ __attribute__((aligned(16))) float pool_lds[C::POOL ? C::POOL_FLOATS : 1];  // PoolTile's tile
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -1451,6 +1561,7 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
     // or channel) gets an offset of at least 2^30 bytes, past the descriptor's
     // range (< 2^30, checked when the plan is made), and its store is dropped.
     ep.init(a, out, part, bias, split, co0 + wc * 16 * C::MA + 4 * g, wp, g, l16, oh0, ow0, !kPF);
+    if constexpr (C::POOL) ep.pool_init(pool_lds, co0, co0 + wc * 16 * C::MA + 4 * g, wp, g, l16, oh0, ow0, a);
 
     // The 16x16x4 blocks' accumulators start from the bias (zero for splits
     // other than 0, and for the waves wk > 0 whose partials are added to wave
@@ -1481,6 +1592,7 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
         run_stages<C, WS>(std::make_integer_sequence<int, C::NS>{}, bufs, regs, x, a, wctx, c_begin, wave, wk, lane,
                           xo, b_base, acc, ep);
         if constexpr (C::FUSED) finish_split_tile<C>(a, part, out, tile, co0, oh0, ow0, last_arrival);
+        if constexpr (C::POOL) pool_tile_finish<C>(pool_lds, out, a, co0, oh0, ow0);
         return;
     }
 
@@ -1502,6 +1614,7 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
                           ep);
     }
     if constexpr (C::FUSED) finish_split_tile<C>(a, part, out, tile, co0, oh0, ow0, last_arrival);
+    if constexpr (C::POOL) pool_tile_finish<C>(pool_lds, out, a, co0, oh0, ow0);
 }
 
 // out[i] = part[0][i] + part[1][i] + ... + part[splits-1][i] (then max(., 0)
@@ -1658,6 +1771,7 @@ struct Variant {
     bool wl;     // weights through LDS: reads OIHW, and its prepacked weights are an OIHW copy
     int nbuf;    // stage buffers
     bool pf;     // progressive first stage: needs at least two stages per workgroup
+    bool poolable;  // has a PoolTile instantiation (2x2 max-pool in the workgroup)
     void (*launch)(dim3 grid, hipStream_t st, const float *, const float *, const float *, float *, float *,
                    const IgArgs &, bool packed);
 };
@@ -1666,6 +1780,12 @@ template <class C>
 void launch_cfg(dim3 grid, hipStream_t st, const float *x, const float *w, const float *b, float *o, float *ws,
                 const IgArgs &a, bool packed)
 {
+    if constexpr (C::POOLABLE) {
+        if (a.pool_tile) {
+            hipLaunchKernelGGL((conv_igemm<PoolTile<C>, false>), grid, dim3(C::NT), 0, st, x, w, b, o, ws, a);
+            return;
+        }
+    }
     using F = FusedSplit<C>;
     if (a.fuse) {
         if (packed) hipLaunchKernelGGL((conv_igemm<F, true>), grid, dim3(C::NT), 0, st, x, w, b, o, ws, a);
@@ -1680,7 +1800,7 @@ template <class C>
 constexpr Variant make_variant(const char *name)
 {
     return Variant{name, C::KS, C::S, C::TH, C::TW, C::NWC, C::NWP, C::NWK, C::MA, C::CC,
-                   C::NT, C::COT, C::LDS_BYTES, C::NS, C::WL, C::NBUF, C::PF, &launch_cfg<C>};
+                   C::NT, C::COT, C::LDS_BYTES, C::NS, C::WL, C::NBUF, C::PF, C::POOLABLE, &launch_cfg<C>};
 }
 
 //                                  KS S  TH  TW NWC NWP NWK MA CC
@@ -1919,7 +2039,11 @@ hipError_t igemm_launch(const ilpm_plan &p, const ConvShape &s, const float *x, 
     // outweigh the input, let the run share output-channel tiles (and so
     // weights) across spatial tiles; otherwise share spatial tiles (input).
     a.sp_fast = (int64_t)s.c_out * s.c_in * s.k * s.k > (int64_t)s.c_in * s.h * s.w ? 1 : 0;
-    a.to_part = (p.splits > 1 || pool) ? 1 : 0;
+    // A pooled epilogue of a one-split plan on OIHW weights is done in the
+    // workgroup when the variant allows it; otherwise the conv writes its
+    // full-size sums to the workspace and sum_splits_pool pools them.
+    a.pool_tile = (pool && p.splits == 1 && !packed && d.poolable) ? 1 : 0;
+    a.to_part = (p.splits > 1 || (pool && !a.pool_tile)) ? 1 : 0;
     a.relu = relu ? 1 : 0;
     const int tiles = p.grid / p.splits;
     a.splits = p.splits;
