@@ -260,10 +260,12 @@ int ilpm_conv2d_fwd_prepacked(const float *in, const float *packed, const float 
  * combination of the ILPM_EPI_* bits (0 = none).  With both bits set the
  * result is max-pool of ReLU, which equals ReLU of max-pool.  `out` has the
  * pooled shape when ILPM_EPI_MAXPOOL2 is set.  plan: NULL for the default
- * plan of the shape, or one made for this exact shape.  Pooling uses
- * workspace for the full-size convolution output (see
- * ilpm_conv2d_epilogue_workspace_size).  The values are exactly those of the
- * unfused sequence conv (same plan) -> ReLU -> max-pool.
+ * plan of the shape, or one made for this exact shape.  One-split
+ * matrix-core plans on OIHW weights whose tiles have even sides pool inside
+ * the kernel; other plans write the full-size convolution output (as
+ * per-split partial sums) to the workspace and pool it in a second kernel
+ * (ilpm_conv2d_epilogue_workspace_size covers that route).  The values are
+ * exactly those of the unfused sequence conv (same plan) -> ReLU -> max-pool.
  */
 int ilpm_conv2d_fwd_epilogue(const float *in, const float *w, const float *bias,
                              int C_in, int H, int W, int C_out, int K, int stride, int pad,
