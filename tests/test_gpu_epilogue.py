@@ -103,3 +103,46 @@ def test_epilogue_against_oracle(ilpm):
         torch.cuda.synchronize()
         err = np.abs(got.cpu().numpy().astype(np.float64) - want)
         assert (err <= tw).all(), f"{case.name}: worst {np.max(err / tw)}"
+
+
+def test_pooled_tile_writes_only_the_pooled_output(ilpm):
+    """One-split plans whose tiles have even sides pool inside the kernel: NaN
+    canaries around the pooled output survive, the values equal conv -> ReLU
+    -> pool of the same plan, and for the 14x14-tile variants (which pool in
+    the workgroup) a NaN-filled registered workspace is left untouched."""
+    torch = torch_cuda()
+    guard = 4096
+    in_kernel = {"k3s1_t14x14_co64_cc16_pf", "k3s1_t14x14_co32_k2", "k3s1_t14x14_co64"}
+    ws = torch.full((1 << 22,), float("nan"), device="cuda", dtype=torch.float32)
+    ilpm.set_workspace(ws)
+    try:
+        for seed, (c_in, h, w_, c_out) in enumerate([(64, 30, 30, 70), (32, 17, 19, 40), (48, 28, 29, 64)]):
+            x, w, b = random_case(8600 + 10 * seed, c_in, h, w_, c_out, 3)
+            xd, wdv, bd = dev(x), dev(w), dev(b)
+            ho, wo = h // 2, w_ // 2
+            n = c_out * ho * wo
+            for v in range(ilpm.num_variants(ilpm.PATH_IGEMM)):
+                info = ilpm.variant_info(ilpm.PATH_IGEMM, v)
+                if info["k"] != 3 or info["stride"] != 1 or info["tile_h"] % 2 or info["tile_w"] % 2:
+                    continue
+                try:
+                    plan = ilpm.plan_variant(c_in, h, w_, c_out, 3, 1, 1, ilpm.PATH_IGEMM, v, 1)
+                except ilpm.IlpmError:
+                    continue
+                name = ilpm.variant_name(ilpm.PATH_IGEMM, v)
+                note(f"[pooled tile] shape {(c_in, h, w_, c_out)} v={v} {name}")
+                base = ilpm.conv2d(xd, wdv, bd, 1, 1, plan=plan)
+                torch.cuda.synchronize()
+                want = pool_relu_np(base.cpu().numpy(), 3)
+                ws.fill_(float("nan"))
+                buf = torch.full((n + 2 * guard,), float("nan"), device="cuda", dtype=torch.float32)
+                out = buf[guard:guard + n].view(1, c_out, ho, wo)
+                ilpm.conv2d_epilogue(xd, wdv, bd, 1, 1, ilpm.EPI_RELU | ilpm.EPI_MAXPOOL2, plan=plan, out=out)
+                torch.cuda.synchronize()
+                assert torch.isnan(buf[:guard]).all() and torch.isnan(buf[guard + n:]).all(), name
+                np.testing.assert_array_equal(out.cpu().numpy(), want, err_msg=name)
+                if name in in_kernel:
+                    assert torch.isnan(ws).all(), f"{name}: the pooled tile went through the workspace"
+    finally:
+        torch.cuda.synchronize()
+        ilpm.set_workspace(None)
