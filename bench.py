@@ -16,6 +16,7 @@ VGG-16's first layer, then the VGG-16 conv stack layer by layer, and writes the
 table to --report (JSON) without changing the line.
 """
 from __future__ import annotations
+--vgg16-stack REPS times only the VGG-16 stack end to end (for kernel traces).
 
 import argparse
 import hashlib
@@ -310,6 +311,8 @@ def main():
     ap.add_argument("--peaks", action="store_true", help="also measure the MI355X ceilings")
     ap.add_argument("--copy-calib", type=int, default=0, metavar="MIB",
                     help="also run a plain copy of MIB MiB (counter calibration under rocprofv3)")
+    ap.add_argument("--vgg16-stack", type=int, default=0, metavar="REPS",
+                    help="only time the VGG-16 stack end to end, REPS passes per timing (kernel traces)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -324,6 +327,10 @@ def main():
     torch.cuda.set_device(0)
     import paper_1909_02765_amd as ilpm
     import workloads
+
+    if args.vgg16_stack:
+        print(json.dumps(bench_vgg16_stack(torch, ilpm, workloads, args.vgg16_stack)))
+        return
 
     case = workloads.case_by_name(args.workload)
     if case is None:
