@@ -14,9 +14,10 @@ layer, the next 400 32.1 us, every later batch 31.1-31.3 us).
 --all also times every other workload, the rest of ResNet's 3x3 layer set and
 VGG-16's first layer, then the VGG-16 conv stack layer by layer, and writes the
 table to --report (JSON) without changing the line.
+
+--vgg16-stack REPS times only the VGG-16 stack end to end (for kernel traces).
 """
 from __future__ import annotations
---vgg16-stack REPS times only the VGG-16 stack end to end (for kernel traces).
 
 import argparse
 import hashlib
