@@ -95,7 +95,7 @@ def test_epilogue_against_oracle(ilpm):
     for case in (workloads.VGG_EARLY, workloads.RESNET_CONV2, workloads.RESNET_CONV5):
         x, w, b = case.inputs()
         ref, sab = oracle.conv2d_f64(x, w, b, case.stride, case.pad)
-        tol = 1e-4 * (1.0 + sab / (case.c_in * case.k * case.k))
+        tol = oracle.tolerance(sab, case.c_in, case.k)
         want = pool_relu_np(ref, 3)
         tw = pool_relu_np(tol, 2)  # largest tolerance per window
         note(f"[epilogue-oracle] {case.name}")

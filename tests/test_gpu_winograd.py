@@ -35,7 +35,7 @@ def run_and_check(ilpm, name, x, w, b, pad):
     g = got.cpu().numpy().astype(np.float64)
     np.testing.assert_array_equal(got.cpu().numpy(), again.cpu().numpy())
     err = np.abs(g - ref)
-    tol = 1e-4 * (1 + sab / (c_in * 9))
+    tol = oracle.tolerance(sab, c_in, 3)
     assert (err <= tol).all(), f"{name}: tolerance ratio {np.max(err / tol)}"
     assert (err <= error_bound(x, w, pad) + 1e-30).all(), f"{name}: outside the rounding bound"
     return u

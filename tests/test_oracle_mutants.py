@@ -1,7 +1,10 @@
-"""Plant plausible mistakes in the oracle's C source, build each broken copy on
-the CPU, and check that the pin suite rejects every one of them.
+"""Plant plausible mistakes in the oracle -- its C source, and the acceptance
+rule in its Python module -- and check that the pin suites reject every one.
 
-Each mutant runs in a child process (a broken index may read out of bounds)."""
+Each C mutant is built on the CPU and runs in a child process (a broken index
+may read out of bounds).  Each Python mutant is the module's source with one
+change, loaded under another name."""
+import importlib.util
 import json
 import os
 import subprocess
@@ -65,3 +68,42 @@ def test_mutant_is_caught(tmp_path, name, old, new):
         return  # the mutant crashed the pin run: caught
     failed = json.loads(r.stdout.strip().splitlines()[-1])
     assert failed, f"mutant {name} passed every pin"
+
+
+# (name, text in oracle/__init__.py, replacement): mistakes in the acceptance
+# rule that every parity verdict goes through.
+PY_SOURCE = os.path.join(ROOT, "oracle", "__init__.py")
+PY_MUTANTS = [
+    ("divisor_c_in_only", "float(c_in * k * k)", "float(c_in)"),
+    ("divisor_k_squared_only", "float(c_in * k * k)", "float(k * k)"),
+    ("absolute_floor_dropped", "1e-4 * (1.0 + np.asarray(sumabs, dtype=np.float64) / float(c_in * k * k))",
+     "1e-4 * (np.asarray(sumabs, dtype=np.float64) / float(c_in * k * k))"),
+    ("scale_1e-3", "return 1e-4 * (1.0 +", "return 1e-3 * (1.0 +"),
+    ("sumabs_ignored", "np.asarray(sumabs, dtype=np.float64) / float", "0.0 * np.asarray(sumabs, dtype=np.float64) / float"),
+    ("comparison_inverted", "ratio[i] <= 1.0", "ratio[i] >= 1.0"),
+    ("comparison_strict", "ratio[i] <= 1.0", "ratio[i] < 1.0"),
+    ("abs_dropped", "ratio = np.abs(r - ref) / tol", "ratio = (r - ref) / tol"),
+    ("non_finite_accepted", "return False, float(\"inf\"), i", "return True, float(\"inf\"), i"),
+    ("non_finite_guard_dropped", "if bad.any():", "if False:"),
+    ("worst_is_best", "i = int(np.argmax(ratio))", "i = int(np.argmin(ratio))"),
+    ("shape_check_dropped", "if r.shape != ref.shape:", "if False:"),
+]
+
+
+@pytest.mark.parametrize("name,old,new", PY_MUTANTS, ids=[m[0] for m in PY_MUTANTS])
+def test_acceptance_mutant_is_caught(tmp_path, name, old, new):
+    from acceptance_pins import ALL_ACCEPTANCE_PINS
+    src = open(PY_SOURCE).read()
+    assert src.count(old) == 1, f"mutation site for {name} not found exactly once"
+    path = tmp_path / f"oracle_{name}.py"
+    path.write_text(src.replace(old, new))
+    spec = importlib.util.spec_from_file_location(f"oracle_mutant_{name}", path)
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    failed = []
+    for pin in ALL_ACCEPTANCE_PINS:
+        try:
+            pin(mod)
+        except Exception:
+            failed.append(pin.__name__)
+    assert failed, f"acceptance-rule mutant {name} passed every pin"

@@ -38,5 +38,5 @@ def test_winograd_fp32_within_bound_and_tolerance():
         got = winograd_conv(x, w, b, case.pad, dtype=np.float32).astype(np.float64)
         err = np.abs(got - ref)
         assert (err <= error_bound(x, w, case.pad) + 1e-30).all(), case.name
-        tol = 1e-4 * (1 + sab / (case.c_in * 9))
+        tol = oracle.tolerance(sab, case.c_in, 3)
         assert (err <= tol).all(), f"{case.name}: worst {np.max(err / tol)}"
