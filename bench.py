@@ -7,9 +7,19 @@ pad 1), with every tensor already resident in HBM.  Prints ONE JSON line.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--all]
 
-The default warm-up is 1000 calls: in a fresh process the first few hundred
-calls of a layer run slower (the first 400 averaged 46 us on the VGG-early
-layer, the next 400 32.1 us, every later batch 31.1-31.3 us).
+Before the counted warm-up (--warmup) every timed layer gets an untimed
+spin-up of the same launch, bounded by wall-clock time (--spinup-ms, default
+300 ms; its calls and milliseconds are in the line): in a fresh process, and
+after the GPU has idled while the host drew the next layer's inputs, the first
+few hundred calls run slower (on the VGG-early layer, 400-call batches from
+process start averaged 46, 32.1, then 31.1-31.3 us).  The timed region itself
+is exactly --steps back-to-back calls.
+
+Besides the headline layer, the line carries a compact row per other workload
+("configs": the tiny layer, ResNet conv4.x, the strided layer, the 1x1 and
+5x5 deep layers, and the VGG-16 stack end to end with its per-layer times):
+us per call, GFLOP/s, the roofline bound and fraction, and cold us (HBM-bound
+rows, each call after a 512 MiB cache scrub).
 
 --all also times every other workload, the rest of ResNet's 3x3 layer set and
 VGG-16's first layer, then the VGG-16 conv stack layer by layer, and writes the
@@ -79,10 +89,34 @@ def measured_traffic(workload, digest):
     return e.get("hbm_bytes_per_launch")
 
 
-def time_layer(torch, ilpm, x, w, b, s, p, out, steps, warmup):
+SPINUP = {"ms": 300.0}  # set from --spinup-ms
+
+
+def spin_up(torch, launch, ms=None):
+    """Untimed back-to-back calls of `launch` until `ms` milliseconds of wall
+    clock have passed (checked every 50 calls, after a synchronisation), so
+    that the GPU is at its steady state when the counted warm-up starts.
+    Returns (calls, ms spent)."""
+    ms = SPINUP["ms"] if ms is None else ms
+    t0 = time.perf_counter()
+    calls = 0
+    while (time.perf_counter() - t0) * 1e3 < ms:
+        for _ in range(50):
+            launch()
+        calls += 50
+        torch.cuda.synchronize()
+    return calls, (time.perf_counter() - t0) * 1e3
+
+
+def time_layer(torch, ilpm, x, w, b, s, p, out, steps, warmup, spin=None):
     """Mean µs per call over `steps` back-to-back ilpm_conv2d_fwd calls on the
-    current stream, bracketed by events recorded on that same stream."""
+    current stream, bracketed by events recorded on that same stream (after
+    the untimed spin-up and `warmup` counted warm-up calls).  `spin`, a dict,
+    receives the spin-up's calls and milliseconds."""
     launch = ilpm.conv2d_launcher(x, w, b, s, p, out)
+    calls, ms = spin_up(torch, launch)
+    if spin is not None:
+        spin.update(calls=calls, ms=round(ms, 1))
     for _ in range(warmup):
         launch()
     torch.cuda.synchronize()
@@ -114,6 +148,7 @@ def time_layer_graph(torch, ilpm, x, w, b, s, p, out, steps, per_graph=20):
                 launch()
     torch.cuda.synchronize()
     reps = max(1, steps // per_graph)
+    spin_up(torch, g.replay)
     for _ in range(max(1, reps // 10)):
         g.replay()
     torch.cuda.synchronize()
@@ -133,6 +168,7 @@ def time_prepacked(torch, ilpm, x, w, b, s, p, out, plan, steps, warmup):
     c_out, _, k, _ = w.shape
     packed = ilpm.prepack_weights(w, plan)
     launch = ilpm.conv2d_prepacked_launcher(x, packed, c_out, k, b, s, p, out, plan)
+    spin_up(torch, launch)
     for _ in range(warmup):
         launch()
     torch.cuda.synchronize()
@@ -287,8 +323,9 @@ def bench_case(torch, ilpm, case, steps, warmup, graph=False):
     flops, nbytes, ho, wo = layer_work(case.c_in, case.h, case.w, case.c_out, case.k, case.stride, case.pad,
                                        b is not None)
     out = torch.empty((1, case.c_out, ho, wo), device="cuda", dtype=torch.float32)
-    us = time_layer(torch, ilpm, xd, wd, bd, case.stride, case.pad, out, steps, warmup)
-    res = dict(x=x, w=w, b=b, out=out, plan=plan, flops=flops, nbytes=nbytes, us=us)
+    spin = {}
+    us = time_layer(torch, ilpm, xd, wd, bd, case.stride, case.pad, out, steps, warmup, spin)
+    res = dict(x=x, w=w, b=b, out=out, plan=plan, flops=flops, nbytes=nbytes, us=us, spin=spin)
     if graph:
         res["graph_us"] = time_layer_graph(torch, ilpm, xd, wd, bd, case.stride, case.pad, out, steps)
         res["prepacked_us"] = time_prepacked(torch, ilpm, xd, wd, bd, case.stride, case.pad, out, plan, steps,
@@ -307,6 +344,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=1000)
     ap.add_argument("--workload", default="vgg_early_64to64_224x224")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--spinup-ms", type=float, default=300.0,
+                    help="untimed, wall-clock-bounded spin-up of each timed launch before its warm-up")
+    ap.add_argument("--no-configs", action="store_true", help="only the headline layer (no per-config rows)")
     ap.add_argument("--all", action="store_true", help="also time every workload and the VGG-16 stack")
     ap.add_argument("--report", default=None, help="JSON file for the --all table")
     ap.add_argument("--peaks", action="store_true", help="also measure the MI355X ceilings")
@@ -328,9 +368,14 @@ def main():
     torch.cuda.set_device(0)
     import paper_1909_02765_amd as ilpm
     import workloads
+    SPINUP["ms"] = max(0.0, args.spinup_ms)
 
     if args.vgg16_stack:
-        print(json.dumps(bench_vgg16_stack(torch, ilpm, workloads, args.vgg16_stack)))
+        rows = bench_vgg16_stack(torch, ilpm, workloads, args.vgg16_stack)
+        print(json.dumps(rows))
+        if any(r.get("same_output_bits") is False for r in rows):
+            print("bench.py: the fused VGG-16 stack's output differs from the unfused one", file=sys.stderr)
+            sys.exit(1)
         return
 
     case = workloads.case_by_name(args.workload)
@@ -358,7 +403,8 @@ def main():
     line = {
         "metric": METRIC, "value": round(gflops, 2), "unit": "GFLOP/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(us / 1000.0, 6),
-        "us_per_layer": round(us, 3), "graph_replay_us_per_layer": round(r["graph_us"], 3),
+        "us_per_layer": round(us, 3), "spinup_calls": r["spin"]["calls"], "spinup_ms": r["spin"]["ms"],
+        "graph_replay_us_per_layer": round(r["graph_us"], 3),
         "prepacked_weights_us_per_layer": round(r["prepacked_us"], 3),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "f32", "data": "synthetic (seeded SplitMix64 inputs, He-normal weights)",
@@ -371,6 +417,10 @@ def main():
     if not args.no_cpu_baseline:
         y = r["out"].cpu().numpy()
         line["cpu_baseline"] = cpu_baseline(case, r["x"], r["w"], r["b"], y)
+
+    failures = []
+    if not args.no_configs:
+        line["configs"] = config_rows(torch, ilpm, workloads, case.name, failures)
 
     if args.copy_calib:
         import ctypes
@@ -412,6 +462,78 @@ def main():
                 json.dump(rows, f, indent=1)
 
     print(json.dumps(line), flush=True)
+    if failures:
+        print("bench.py: " + "; ".join(failures), file=sys.stderr)
+        sys.exit(1)
+
+
+CONFIG_ROWS = ["tiny_3to16_32x32", "resnet_conv4_256to256_14x14", "resnet_strided_128to256_28x28_s2",
+               "deep_1x1_512to512_7x7", "deep_5x5_512to512_7x7"]
+
+
+def config_rows(torch, ilpm, workloads, headline, failures, steps=500, warmup=200):
+    """One compact row per other workload: µs per call (after the spin-up and
+    warm-up), graph-replay µs, GFLOP/s, roofline bound / floor / fraction,
+    and for HBM-bound rows the cold µs and its fraction; then the VGG-16 stack
+    end to end and layer by layer."""
+    rows = []
+    for name in CONFIG_ROWS:
+        if name == headline:
+            continue
+        c = workloads.case_by_name(name)
+        x, w, b = c.inputs()
+        xd, wd, bd = (workloads.to_device(torch, t) for t in (x, w, b))
+        flops, nbytes, ho, wo = layer_work(c.c_in, c.h, c.w, c.c_out, c.k, c.stride, c.pad, b is not None)
+        out = torch.empty((1, c.c_out, ho, wo), device="cuda", dtype=torch.float32)
+        us = time_layer(torch, ilpm, xd, wd, bd, c.stride, c.pad, out, steps, warmup)
+        gus = time_layer_graph(torch, ilpm, xd, wd, bd, c.stride, c.pad, out, steps)
+        fl, kind = roofline_floor_us(flops, nbytes)
+        plan = ilpm.plan(c.c_in, c.h, c.w, c.c_out, c.k, c.stride, c.pad)
+        row = {"workload": name, "us": round(us, 3), "graph_us": round(gus, 3),
+               "gflops": round(flops / us / 1e3, 1), "bound": kind, "floor_us": round(fl, 3),
+               "frac": round(fl / us, 4), "plan": ilpm.variant_name(plan.path, plan.variant) + f" x{plan.splits}"}
+        if kind == "hbm":
+            cus = time_cold(torch, ilpm, xd, wd, bd, c.stride, c.pad, out)
+            row["cold_us"] = round(cus, 3)
+            row["cold_frac"] = round(fl / cus, 4)
+        rows.append(row)
+        print(json.dumps(row), file=sys.stderr)
+    st = bench_vgg16_stack(torch, ilpm, workloads, 20)
+    by = {r["layer"]: r for r in st}
+    for r in st:
+        if r.get("same_output_bits") is False:
+            failures.append(f"{r['layer']}: output differs from the unfused stack's bits")
+    layers = bench_vgg16_layers(torch, ilpm, workloads, 200)
+    floor_total = sum(l["floor_us"] for l in layers)
+    flops_total = sum(l["gflop"] for l in layers) * 1e9
+    us_f = by["vgg16_stack_fused"]["us"]
+    rows.append({"workload": "vgg16_stack_13conv_224", "us": us_f,
+                 "graph_us": by["vgg16_stack_fused_graph"]["us"], "unfused_us": by["vgg16_stack_unfused"]["us"],
+                 "gflops": round(flops_total / us_f / 1e3, 1), "bound": "mfma (conv1_1 hbm)",
+                 "floor_us": round(floor_total, 3), "frac": round(floor_total / us_f, 4),
+                 "note": "end to end, fused ReLU / ReLU+2x2 max-pool epilogue, one call per conv",
+                 "layers": [{k: l[k] for k in ("layer", "us", "frac")} for l in layers]})
+    print(json.dumps(rows[-1]), file=sys.stderr)
+    return rows
+
+
+def bench_vgg16_layers(torch, ilpm, workloads, steps):
+    """Each VGG-16 conv timed by itself (default plan, no epilogue) on the
+    stack's own input to it."""
+    from workloads import to_device
+    out_rows = []
+    x = to_device(torch, workloads.vgg16_input())
+    for name, ci, co, hw, pool, seed in workloads.vgg16_layers():
+        w = to_device(torch, workloads.vgg16_weights(ci, co, seed))
+        out = torch.empty((1, co, hw, hw), device="cuda", dtype=torch.float32)
+        us = time_layer(torch, ilpm, x, w, None, 1, 1, out, steps, 200)
+        flops, nbytes, _, _ = layer_work(ci, hw, hw, co, 3, 1, 1, False)
+        fl, kind = roofline_floor_us(flops, nbytes)
+        out_rows.append({"layer": name, "us": round(us, 3), "frac": round(fl / us, 4), "floor_us": fl,
+                         "gflop": flops / 1e9, "bound": kind})
+        ilpm.relu_(out)
+        x = ilpm.maxpool2x2(out) if pool else out
+    return out_rows
 
 
 def bench_vgg16(torch, ilpm, workloads, steps):
@@ -482,9 +604,10 @@ def bench_vgg16_stack(torch, ilpm, workloads, reps):
     out_fused = x
 
     def timed(fns):
-        for _ in range(3):
+        def one_pass():
             for f in fns:
                 f()
+        spin_up(torch, one_pass)
         torch.cuda.synchronize()
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         a.record()
@@ -523,6 +646,7 @@ def bench_vgg16_stack(torch, ilpm, workloads, reps):
             for f in fused_s:
                 f()
     torch.cuda.synchronize()
+    spin_up(torch, g.replay)
     graph_same = True
     for _ in range(3):
         out_graph.fill_(float("nan"))

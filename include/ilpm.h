@@ -25,7 +25,9 @@
  *     frees) them; the library keeps no tensor pointer after a call returns.
  *   - Work is only enqueued on `stream` (NULL = the default stream); no call
  *     synchronises the host.  A device-side fault shows up at the caller's
- *     next synchronisation.
+ *     next synchronisation.  The one exception to "only enqueued" is the
+ *     library-owned workspace (see ilpm_conv2d_fwd): the first call that
+ *     needs a larger one allocates it with hipMalloc.
  *   - Arguments are checked before anything is launched; on an error the
  *     call returns a negative status and writes nothing.
  *   - K in this library is the filter size; output channels are C_out.  (The
@@ -48,7 +50,8 @@ enum {
     ILPM_ERR_INVALID_ARG = -1, /* null pointer, dimension <= 0, stride <= 0, pad < 0,
                                   no output pixel, out overlapping an input, bad plan */
     ILPM_ERR_UNSUPPORTED = -2, /* a tensor above 2^31-1 elements */
-    ILPM_ERR_WORKSPACE = -3,   /* registered workspace smaller than the plan needs */
+    ILPM_ERR_WORKSPACE = -3,   /* registered workspace smaller than the plan needs, or the
+                                  library's own would have to grow during graph capture */
     ILPM_ERR_HIP = -4,         /* a HIP runtime call or kernel launch failed */
     ILPM_ERR_ARCH = -5         /* the current device is not gfx950 */
 };
@@ -84,13 +87,20 @@ typedef struct ilpm_plan {
  *   out  [1, C_out, H_out, W_out]   NCHW, fully written; must not overlap the inputs
  *   stride >= 1, pad >= 0, all sizes >= 1, H_out >= 1 and W_out >= 1.
  * Picks the kernel with ilpm_conv2d_plan.  Plans with splits > 1 write
- * per-split partial outputs to the device workspace (registered with
- * ilpm_set_workspace, else allocated by the library on first need); the
- * last workgroup of each output tile sums them in split order (or a second
- * kernel on the same stream does, see ilpm_set_split_sum).  Such plans also
- * use a per-device array of tile arrival counts that the library holds; calls
- * that overlap in time on one device and both use split plans must be
- * ordered on one stream.
+ * per-split partial outputs to the device workspace; the last workgroup of
+ * each output tile sums them in split order (or a second kernel on the same
+ * stream does, see ilpm_set_split_sum).  Such plans also use a per-device
+ * array of tile arrival counts that the library holds; calls that overlap in
+ * time on one device and both use split plans must be ordered on one stream.
+ * Workspace: the one registered with ilpm_set_workspace (ILPM_ERR_WORKSPACE
+ * if it is too small), else the library's own for the current device.  A
+ * call that needs more than the library's own holds allocates a larger one
+ * (hipMalloc: no synchronisation, no free -- the smaller buffer is kept
+ * until the process ends, because work already enqueued or a HIP graph
+ * captured earlier may still use it).  While `stream` is being captured
+ * into a graph nothing can be allocated, and such a call returns
+ * ILPM_ERR_WORKSPACE instead: size the workspace before capturing (one
+ * uncaptured call of the same shape, or ilpm_set_workspace).
  * Returns ILPM_OK or a negative status.
  */
 int ilpm_conv2d_fwd(const float *in, const float *w, const float *bias,
@@ -132,6 +142,15 @@ int ilpm_set_split_sum(int mode);
 /* Text for a status code (static storage). */
 const char *ilpm_status_str(int status);
 
+/*
+ * ilpm_arch_supported -- the architecture check every launching call makes
+ * on the current device: ILPM_OK when `gcn_arch_name` (a device's
+ * hipDeviceProp_t::gcnArchName, e.g. "gfx950:sramecc+:xnack-") names gfx950,
+ * ILPM_ERR_ARCH for any other architecture, ILPM_ERR_INVALID_ARG for NULL.
+ * Pure host.
+ */
+int ilpm_arch_supported(const char *gcn_arch_name);
+
 /* The hipError_t value behind the calling thread's most recent ILPM_ERR_HIP
  * (0 if there was none). */
 int ilpm_last_hip_error(void);
@@ -149,8 +168,18 @@ int ilpm_conv2d_validate(const void *in, const void *w, const void *bias,
  * ilpm_conv2d_plan -- the plan ilpm_conv2d_fwd uses for this shape (path,
  * tile, split count, grid, workspace): the fastest plan measured on MI355X
  * for this exact shape when the compiled-in tuning table lists it, else the
- * best by a cost model.  Pure host.  The environment variables
- * ILPM_FORCE_PATH=direct|igemm and ILPM_SPLIT=n override the choice.
+ * best by a cost model.  Pure host.  A shape's plan is chosen once and kept
+ * (a table in the library), so later calls cost a lookup.
+ * Environment overrides, read once, the first time the library plans a call
+ * (for sweeps and ablations; any of them bypasses the tuning table):
+ *   ILPM_FORCE_PATH=direct|igemm  only that kernel family (igemm: the
+ *                                 call fails with ILPM_ERR_UNSUPPORTED if
+ *                                 no matrix-core variant takes the shape);
+ *   ILPM_SPLIT=n                  matrix-core plans with n input-channel
+ *                                 splits;
+ *   ILPM_TILE=<h>x<w>             only variants whose output tile is h x w
+ *                                 (ILPM_ERR_UNSUPPORTED if none takes the
+ *                                 shape).
  */
 int ilpm_conv2d_plan(int C_in, int H, int W, int C_out, int K, int stride, int pad,
                      ilpm_plan *plan);

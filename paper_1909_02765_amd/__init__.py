@@ -91,6 +91,7 @@ _SIGS = {
     "ilpm_set_workspace": ([_vp, ctypes.c_size_t, _vp], _i),
     "ilpm_set_split_sum": ([_i], _i),
     "ilpm_status_str": ([_i], ctypes.c_char_p),
+    "ilpm_arch_supported": ([ctypes.c_char_p], _i),
     "ilpm_last_hip_error": ([], _i),
     "ilpm_conv2d_validate": ([_vp, _vp, _vp] + [_i] * 7 + [_vp], _i),
     "ilpm_conv2d_plan": ([_i] * 7 + [_plan_p], _i),

@@ -42,23 +42,39 @@ def hipcc() -> str:
     return p
 
 
-def build(output: str = LIBRARY, isa_dir: str | None = None, verbose: bool = False) -> str:
-    cmd = [hipcc()] + FLAGS + ["-I", INCLUDE, "-I", CSRC] + sources()
-    tmp = output + ".tmp"
-    cmd += ["-o", tmp]
-    if isa_dir:
-        os.makedirs(isa_dir, exist_ok=True)
-        cmd += ["-save-temps=obj"]
-        cmd[-1:-1] = []
+def _compile(src: str, obj: str, extra=(), cwd=None, verbose=False):
+    cmd = [hipcc()] + [f for f in FLAGS if f != "-shared"] + ["-I", INCLUDE, "-I", CSRC] + list(extra)
+    cmd += ["-c", src, "-o", obj]
     if verbose:
         print(" ".join(cmd), file=sys.stderr)
-    cwd = isa_dir if isa_dir else None
-    if isa_dir:
-        # -save-temps=obj writes next to the output object; build inside isa_dir.
-        cmd[cmd.index("-o") + 1] = os.path.join(isa_dir, "libilpm.so")
-        subprocess.run(cmd, check=True, cwd=cwd)
-        shutil.copyfile(os.path.join(isa_dir, "libilpm.so"), tmp)
-    else:
+    subprocess.run(cmd, check=True, cwd=cwd)
+    return obj
+
+
+def build(output: str = LIBRARY, isa_dir: str | None = None, verbose: bool = False, jobs: int = 0) -> str:
+    """Compile every csrc/*.hip to an object (in parallel: the matrix-core
+    variants are spread over several files for this), then link the shared
+    library.  With isa_dir, the intermediate files (gfx950 assembly) are kept
+    there."""
+    import tempfile
+    from concurrent.futures import ThreadPoolExecutor
+    srcs = sources()
+    jobs = jobs or min(len(srcs), os.cpu_count() or 1, 16)
+    with tempfile.TemporaryDirectory(prefix="ilpm_build_") as tmpdir:
+        objdir = isa_dir or tmpdir
+        if isa_dir:
+            os.makedirs(isa_dir, exist_ok=True)
+        extra = ["-save-temps=obj"] if isa_dir else []
+        objs = [os.path.join(objdir, os.path.basename(sp) + ".o") for sp in srcs]
+        with ThreadPoolExecutor(max_workers=jobs) as ex:
+            futs = [ex.submit(_compile, sp, ob, extra, objdir if isa_dir else None, verbose)
+                    for sp, ob in zip(srcs, objs)]
+            for f in futs:
+                f.result()
+        tmp = output + ".tmp"
+        cmd = [hipcc()] + FLAGS + objs + ["-o", tmp]
+        if verbose:
+            print(" ".join(cmd), file=sys.stderr)
         subprocess.run(cmd, check=True)
     os.replace(tmp, output)
     return output

@@ -1,10 +1,12 @@
 // C-ABI layer: argument checks, plan choice, workspace, device check and
 // launch.  Declarations and contracts are in include/ilpm.h.
 #include <algorithm>
+#include <atomic>
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
 #include <mutex>
+#include <vector>
 
 #include "internal.h"
 
@@ -15,7 +17,7 @@ constexpr int kMaxDevices = 64;
 constexpr int64_t kMaxElems = 0x7fffffffLL;
 
 std::mutex g_mu;
-int g_arch[kMaxDevices];  // 0 unknown, 1 gfx950, -1 other
+std::atomic<int> g_arch[kMaxDevices];  // 0 unknown, 1 gfx950, -1 other
 thread_local int g_last_hip = 0;  // hipError_t behind the last ILPM_ERR_HIP of this thread
 
 int hip_fail(hipError_t e)
@@ -29,8 +31,43 @@ struct Workspace {
     size_t user_bytes = 0;
     void *own = nullptr;
     size_t own_bytes = 0;
+    // Smaller library-owned buffers that a larger one replaced.  They are
+    // never freed: a call still running, or a graph captured earlier, may use
+    // them, and freeing would need a synchronisation.
+    std::vector<void *> retired;
 };
 Workspace g_ws[kMaxDevices];
+
+// Environment overrides, read once when the library first plans a call.
+struct Overrides {
+    int path = -1;          // ILPM_FORCE_PATH: -1 any, ILPM_PATH_DIRECT or ILPM_PATH_IGEMM
+    int splits = 0;         // ILPM_SPLIT: input-channel splits of matrix-core plans (0 = choose)
+    int tile_h = 0, tile_w = 0;  // ILPM_TILE=<h>x<w>: only variants with this output tile
+};
+
+Overrides read_overrides()
+{
+    Overrides o;
+    if (const char *f = std::getenv("ILPM_FORCE_PATH")) {
+        if (std::strcmp(f, "direct") == 0) o.path = ILPM_PATH_DIRECT;
+        else if (std::strcmp(f, "igemm") == 0 || std::strcmp(f, "gemm") == 0) o.path = ILPM_PATH_IGEMM;
+    }
+    if (const char *e = std::getenv("ILPM_SPLIT")) o.splits = std::max(0, std::atoi(e));
+    if (const char *t = std::getenv("ILPM_TILE")) {
+        int h = 0, w = 0;
+        if (std::sscanf(t, "%dx%d", &h, &w) == 2 && h > 0 && w > 0) {
+            o.tile_h = h;
+            o.tile_w = w;
+        }
+    }
+    return o;
+}
+
+const Overrides &overrides()
+{
+    static const Overrides o = read_overrides();
+    return o;
+}
 
 bool overlaps(const void *a, size_t an, const void *b, size_t bn)
 {
@@ -88,22 +125,20 @@ int validate(const void *in, const void *w, const void *bias, const ConvShape &s
 // The default plan: the measured best for this exact shape when the tuning
 // table has it, else the cheapest matrix-core variant for this filter size
 // and stride by the cost model, else the LDS direct kernel, else the plain
-// one.
-int choose_plan(const ConvShape &s, ilpm_plan *p)
+// one.  The environment overrides (read once) narrow the candidates.
+int compute_plan(const ConvShape &s, ilpm_plan *p)
 {
-    const char *force = std::getenv("ILPM_FORCE_PATH");
-    const char *split_env = std::getenv("ILPM_SPLIT");
-    const int forced_splits = split_env ? std::atoi(split_env) : 0;
-    const bool want_direct = force && std::strcmp(force, "direct") == 0;
-    const bool want_igemm = force && std::strcmp(force, "igemm") == 0;
-    if (!force && forced_splits <= 0 && tuned_plan(s, p)) return ILPM_OK;
-    if (want_igemm || !want_direct) {
+    const Overrides &o = overrides();
+    const bool any = o.path < 0 && o.splits == 0 && o.tile_h == 0;
+    if (any && tuned_plan(s, p)) return ILPM_OK;
+    auto tile_ok = [&](const ilpm_plan &q) { return o.tile_h == 0 || (q.tile_h == o.tile_h && q.tile_w == o.tile_w); };
+    if (o.path != ILPM_PATH_DIRECT) {
         bool found = false;
         double best = 0;
         ilpm_plan bp = {};
         for (int v = 0; v < igemm_num_variants(); ++v) {
             ilpm_plan q;
-            if (!igemm_make_plan(s, v, forced_splits > 0 ? forced_splits : 0, &q)) continue;
+            if (!igemm_make_plan(s, v, o.splits, &q) || !tile_ok(q)) continue;
             const double c = igemm_plan_cost(s, q);
             if (!found || c < best) {
                 found = true;
@@ -116,9 +151,56 @@ int choose_plan(const ConvShape &s, ilpm_plan *p)
             return ILPM_OK;
         }
     }
-    if (direct_make_plan(s, 0, p)) return ILPM_OK;
-    if (direct_make_plan(s, 1, p)) return ILPM_OK;
+    if (o.path == ILPM_PATH_IGEMM) return ILPM_ERR_UNSUPPORTED;
+    for (int v = 0; v < direct_num_variants(); ++v) {
+        ilpm_plan q;
+        if (direct_make_plan(s, v, &q) && tile_ok(q)) {
+            *p = q;
+            return ILPM_OK;
+        }
+    }
     return ILPM_ERR_UNSUPPORTED;
+}
+
+// Plans already chosen, by shape: a direct-mapped table, so a call on a shape
+// seen before costs one hash and one comparison instead of the table scan and
+// the cost-model sweep.
+struct PlanSlot {
+    bool used = false;
+    ConvShape s;
+    int rc;
+    ilpm_plan p;
+};
+constexpr int kPlanSlots = 512;
+PlanSlot g_plan_cache[kPlanSlots];
+
+bool same_shape(const ConvShape &a, const ConvShape &b)
+{
+    return a.c_in == b.c_in && a.h == b.h && a.w == b.w && a.c_out == b.c_out && a.k == b.k &&
+           a.stride == b.stride && a.pad == b.pad;
+}
+
+int choose_plan(const ConvShape &s, ilpm_plan *p)
+{
+    uint64_t h = 1469598103934665603ull;  // FNV-1a over the seven sizes
+    for (int v : {s.c_in, s.h, s.w, s.c_out, s.k, s.stride, s.pad}) h = (h ^ (uint32_t)v) * 1099511628211ull;
+    PlanSlot &slot = g_plan_cache[h % kPlanSlots];
+    {
+        std::lock_guard<std::mutex> lk(g_mu);
+        if (slot.used && same_shape(slot.s, s)) {
+            *p = slot.p;
+            return slot.rc;
+        }
+    }
+    ilpm_plan q = {};
+    const int rc = compute_plan(s, &q);
+    std::lock_guard<std::mutex> lk(g_mu);
+    slot.used = true;
+    slot.s = s;
+    slot.rc = rc;
+    slot.p = q;
+    *p = q;
+    return rc;
 }
 
 bool same_plan_shape(const ilpm_plan &a, const ilpm_plan &b)
@@ -141,24 +223,38 @@ int check_plan(const ConvShape &s, const ilpm_plan &p)
     return ILPM_OK;
 }
 
+// gcnArchName is "gfx950" followed by optional ":feature+/-" settings.
+int arch_status(const char *name)
+{
+    if (!name) return ILPM_ERR_INVALID_ARG;
+    return (std::strncmp(name, "gfx950", 6) == 0 && (name[6] == '\0' || name[6] == ':')) ? ILPM_OK : ILPM_ERR_ARCH;
+}
+
 int device_check(int *dev_out)
 {
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return hip_fail(e);
     if (dev < 0 || dev >= kMaxDevices) return hip_fail(hipErrorInvalidDevice);
-    std::lock_guard<std::mutex> lk(g_mu);
-    if (g_arch[dev] == 0) {
+    int known = g_arch[dev].load(std::memory_order_acquire);
+    if (known == 0) {
         hipDeviceProp_t prop;
         e = hipGetDeviceProperties(&prop, dev);
         if (e != hipSuccess) return hip_fail(e);
-        g_arch[dev] = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0 ? 1 : -1;
+        known = arch_status(prop.gcnArchName) == ILPM_OK ? 1 : -1;
+        g_arch[dev].store(known, std::memory_order_release);
     }
     *dev_out = dev;
-    return g_arch[dev] == 1 ? ILPM_OK : ILPM_ERR_ARCH;
+    return known == 1 ? ILPM_OK : ILPM_ERR_ARCH;
 }
 
-int get_workspace(int dev, size_t need, void **ws)
+// The workspace of a call on `stream`: the registered one, else the
+// library's own, grown when too small.  Growing allocates (hipMalloc) but
+// neither synchronises nor frees: the smaller buffer is retired, not freed,
+// since work already enqueued or a graph captured earlier may still use it.
+// While `stream` is being captured nothing is allocated (an allocation is not
+// allowed there): a call that would need to grow returns ILPM_ERR_WORKSPACE.
+int get_workspace(int dev, size_t need, hipStream_t stream, void **ws)
 {
     *ws = nullptr;
     if (need == 0) return ILPM_OK;
@@ -170,17 +266,16 @@ int get_workspace(int dev, size_t need, void **ws)
         return ILPM_OK;
     }
     if (w.own_bytes < need) {
-        hipError_t e;
-        if (w.own) {
-            // Earlier calls may still use the old buffer.
-            if ((e = hipDeviceSynchronize()) != hipSuccess) return hip_fail(e);
-            if ((e = hipFree(w.own)) != hipSuccess) return hip_fail(e);
-            w.own = nullptr;
-            w.own_bytes = 0;
-        }
-        const size_t bytes = ((need + (1u << 20) - 1) >> 20) << 20;
+        hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+        hipError_t e = hipStreamIsCapturing(stream, &cs);
+        if (e != hipSuccess) return hip_fail(e);
+        if (cs != hipStreamCaptureStatusNone) return ILPM_ERR_WORKSPACE;
+        // Geometric growth keeps the retired total below the live buffer.
+        size_t bytes = std::max(need, 2 * w.own_bytes);
+        bytes = ((bytes + (1u << 20) - 1) >> 20) << 20;
         void *p = nullptr;
         if ((e = hipMalloc(&p, bytes)) != hipSuccess) return hip_fail(e);
+        if (w.own) w.retired.push_back(w.own);
         w.own = p;
         w.own_bytes = bytes;
     }
@@ -219,7 +314,7 @@ int run(const float *in, const float *w, const float *bias, const ConvShape &s, 
     int rc = device_check(&dev);
     if (rc != ILPM_OK) return rc;
     void *ws = nullptr;
-    rc = get_workspace(dev, workspace_need(p, s, epilogue), &ws);
+    rc = get_workspace(dev, workspace_need(p, s, epilogue), stream, &ws);
     if (rc != ILPM_OK) return rc;
     log_plan(s, p);
     // Launch errors are read back with hipGetLastError; drop any error an
@@ -417,6 +512,8 @@ int ilpm_conv2d_fwd(const float *in, const float *w, const float *bias, int C_in
     return run(in, w, bias, s, out, p, stream);
 }
 
+int ilpm_arch_supported(const char *gcn_arch_name) { return arch_status(gcn_arch_name); }
+
 int ilpm_conv2d_fwd_plan(const float *in, const float *w, const float *bias, int C_in, int H, int W, int C_out,
                          int K, int stride, int pad, float *out, const ilpm_plan *plan, hipStream_t stream)
 {
@@ -554,7 +651,7 @@ int ilpm_conv2d_fwd_winograd(const float *in, const float *u, const float *bias,
     rc = device_check(&dev);
     if (rc != ILPM_OK) return rc;
     void *ws = nullptr;
-    rc = get_workspace(dev, winograd_workspace_bytes(s), &ws);
+    rc = get_workspace(dev, winograd_workspace_bytes(s), stream, &ws);
     if (rc != ILPM_OK) return rc;
     (void)hipGetLastError();
     hipError_t e;

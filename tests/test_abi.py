@@ -179,13 +179,84 @@ def test_progressive_first_stage_plans_two_stages_per_split():
             assert cps >= 2 and nchunks - (p.splits - 1) * cps >= 2
 
 
-def test_plan_env_override(monkeypatch):
-    monkeypatch.setenv("ILPM_FORCE_PATH", "direct")
-    p = ilpm.plan(64, 56, 56, 64, 3, 1, 1)
-    assert p.path == ilpm.PATH_DIRECT
-    monkeypatch.delenv("ILPM_FORCE_PATH")
-    p = ilpm.plan(64, 56, 56, 64, 3, 1, 1)
-    assert p.path == ilpm.PATH_IGEMM
+_PLAN_IN_CHILD = r"""
+import json, sys
+sys.path.insert(0, {root!r})
+import paper_1909_02765_amd as ilpm
+out = []
+for shape in {shapes!r}:
+    try:
+        p = ilpm.plan(*shape)
+        out.append(dict(path=p.path, tile=[p.tile_h, p.tile_w], splits=p.splits,
+                        name=ilpm.variant_name(p.path, p.variant)))
+    except ilpm.IlpmError as e:
+        out.append(dict(status=e.status))
+print(json.dumps(out))
+"""
+
+
+def plans_with_env(env_extra, shapes):
+    """The default plans of `shapes` in a fresh process whose environment has
+    env_extra (the library reads its overrides once, at its first plan)."""
+    import json
+    import subprocess
+    import sys
+    env = {k: v for k, v in os.environ.items() if not k.startswith("ILPM_")}
+    env.update(env_extra)
+    r = subprocess.run([sys.executable, "-c", _PLAN_IN_CHILD.format(root=ROOT, shapes=shapes)],
+                       capture_output=True, text=True, env=env, timeout=300)
+    assert r.returncode == 0, r.stderr
+    return json.loads(r.stdout.strip().splitlines()[-1])
+
+
+CONV2X = (64, 56, 56, 64, 3, 1, 1)
+CONV4X = (256, 14, 14, 256, 3, 1, 1)
+
+
+def test_plan_env_force_path():
+    base, forced = plans_with_env({}, [CONV2X]), plans_with_env({"ILPM_FORCE_PATH": "direct"}, [CONV2X])
+    assert base[0]["path"] == ilpm.PATH_IGEMM
+    assert forced[0]["path"] == ilpm.PATH_DIRECT
+    assert plans_with_env({"ILPM_FORCE_PATH": "gemm"}, [CONV2X])[0]["path"] == ilpm.PATH_IGEMM
+
+
+def test_plan_env_tile_override():
+    """ILPM_TILE=<h>x<w> keeps only variants with that output tile; a tile no
+    variant has makes planning fail with ILPM_ERR_UNSUPPORTED."""
+    got = plans_with_env({"ILPM_TILE": "7x7"}, [CONV4X, CONV2X])
+    assert all(g["tile"] == [7, 7] for g in got), got
+    got = plans_with_env({"ILPM_TILE": "4x4"}, [CONV4X])
+    assert got[0]["tile"] == [4, 4], got
+    got = plans_with_env({"ILPM_TILE": "1x1"}, [CONV4X])  # only the global-memory direct kernel
+    assert got[0]["path"] == ilpm.PATH_DIRECT and got[0]["tile"] == [1, 1], got
+    got = plans_with_env({"ILPM_TILE": "3x5"}, [CONV4X])
+    assert got[0] == {"status": ilpm.ERR_UNSUPPORTED}, got
+    got = plans_with_env({"ILPM_TILE": "1x1", "ILPM_FORCE_PATH": "igemm"}, [CONV4X])
+    assert got[0] == {"status": ilpm.ERR_UNSUPPORTED}, got
+
+
+def test_plan_env_split_override():
+    got = plans_with_env({"ILPM_SPLIT": "2", "ILPM_TILE": "7x7"}, [CONV4X])
+    assert got[0]["splits"] == 2 and got[0]["tile"] == [7, 7], got
+
+
+def test_plan_is_stable_across_calls():
+    a, b = ilpm.plan(*CONV4X), ilpm.plan(*CONV4X)
+    assert a.as_dict() == b.as_dict()
+
+
+@pytest.mark.parametrize("name,want", [
+    (b"gfx950", ilpm.OK), (b"gfx950:sramecc+:xnack-", ilpm.OK), (b"gfx950:xnack+", ilpm.OK),
+    (b"gfx942", ilpm.ERR_ARCH), (b"gfx942:sramecc+:xnack-", ilpm.ERR_ARCH), (b"gfx90a", ilpm.ERR_ARCH),
+    (b"gfx9501", ilpm.ERR_ARCH), (b"gfx95", ilpm.ERR_ARCH), (b"", ilpm.ERR_ARCH), (b"gfx1201", ilpm.ERR_ARCH),
+    (None, ilpm.ERR_INVALID_ARG)])
+def test_arch_check(name, want):
+    """The architecture check behind ILPM_ERR_ARCH: gfx950 with any feature
+    suffix passes, every other name (including a longer one that starts with
+    gfx950) is refused."""
+    assert ilpm.lib.ilpm_arch_supported(name) == want
+    if want == ilpm.ERR_ARCH:
+        assert ilpm.status_str(want) == "device is not gfx950"
 
 
 def test_fwd_plan_rejects_foreign_plan():
