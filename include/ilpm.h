@@ -108,6 +108,27 @@ int ilpm_conv2d_fwd(const float *in, const float *w, const float *bias,
                     float *out, hipStream_t stream);
 
 /*
+ * ilpm_conv2d_fwd_noalloc -- ilpm_conv2d_fwd for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc): same arguments, same plan and the same
+ * output bits as ilpm_conv2d_fwd, but its split plans keep their partial
+ * sums in a fixed array the library holds on each device (created when the
+ * library's code loads on that device and held until the process ends) of
+ * ILPM_NOALLOC_SCRATCH_BYTES, instead of the registered or library-owned
+ * workspace.  It calls no hipMalloc, hipFree or other allocating routine.
+ * A shape whose plan needs more than that returns ILPM_ERR_WORKSPACE before
+ * anything is launched (ilpm_conv2d_workspace_size tells the need).  Every
+ * call on a device shares that device's array and leaves its contents
+ * behind (each call writes every partial sum it reads, so nothing needs
+ * clearing): calls that overlap in time on one device race, so order them
+ * on one stream.
+ */
+#define ILPM_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
+int ilpm_conv2d_fwd_noalloc(const float *in, const float *w, const float *bias,
+                            int C_in, int H, int W, int C_out, int K, int stride, int pad,
+                            float *out, hipStream_t stream);
+
+/*
  * ilpm_conv2d_workspace_size -- bytes of device workspace the default plan
  * for this shape needs (0 when it needs none).  Pure host; no device access.
  */

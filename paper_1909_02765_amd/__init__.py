@@ -87,6 +87,7 @@ _plan_p = ctypes.POINTER(ilpm_plan)
 _SIGS = {
     "ilpm_conv2d_fwd": ([_vp, _vp, _vp] + [_i] * 7 + [_vp, _vp], _i),
     "ilpm_conv2d_fwd_plan": ([_vp, _vp, _vp] + [_i] * 7 + [_vp, _plan_p, _vp], _i),
+    "ilpm_conv2d_fwd_noalloc": ([_vp, _vp, _vp] + [_i] * 7 + [_vp, _vp], _i),
     "ilpm_conv2d_workspace_size": ([_i] * 7 + [ctypes.POINTER(ctypes.c_size_t)], _i),
     "ilpm_set_workspace": ([_vp, ctypes.c_size_t, _vp], _i),
     "ilpm_set_split_sum": ([_i], _i),
@@ -238,6 +239,25 @@ def conv2d(x, w, bias=None, stride: int = 1, pad: int = 0, out=None, plan: Optio
     else:
         rc = lib.ilpm_conv2d_fwd_plan(*args, ctypes.byref(plan), _stream_handle(stream))
         _check(rc, "ilpm_conv2d_fwd_plan")
+    return out
+
+
+NOALLOC_SCRATCH_BYTES = 16 << 20  # ILPM_NOALLOC_SCRATCH_BYTES
+
+
+def conv2d_noalloc(x, w, bias=None, stride: int = 1, pad: int = 0, *, out, stream=None):
+    """conv2d through ilpm_conv2d_fwd_noalloc (no device allocation: split
+    plans use the library's fixed per-device array).  `out` must be given."""
+    if x.dim() != 4 or x.shape[0] != 1 or w.dim() != 4 or w.shape[2] != w.shape[3] or w.shape[1] != x.shape[1]:
+        raise ValueError("x must be [1, C_in, H, W] and w [C_out, C_in, K, K]")
+    _, c_in, h, wd = x.shape
+    c_out, _, k, _ = w.shape
+    if tuple(out.shape) != (1, c_out, out_size(h, k, stride, pad), out_size(wd, k, stride, pad)):
+        raise ValueError("out has the wrong shape")
+    _check(lib.ilpm_conv2d_fwd_noalloc(_dev_f32(x, "x"), _dev_f32(w, "w"),
+                                       _dev_f32(bias, "bias") if bias is not None else None,
+                                       c_in, h, wd, c_out, k, stride, pad, _dev_f32(out, "out"),
+                                       _stream_handle(stream)), "ilpm_conv2d_fwd_noalloc")
     return out
 
 

@@ -10,6 +10,11 @@
 
 #include "internal.h"
 
+// The no-alloc entry point's workspace: one fixed array per device, created
+// when the code object loads and kept until the process ends (host code uses
+// the address hipGetSymbolAddress returns for it, never this name).
+static __device__ __align__(256) float scratch[ILPM_NOALLOC_SCRATCH_BYTES / sizeof(float)];
+
 namespace ilpm {
 namespace {
 
@@ -18,6 +23,7 @@ constexpr int64_t kMaxElems = 0x7fffffffLL;
 
 std::mutex g_mu;
 std::atomic<int> g_arch[kMaxDevices];  // 0 unknown, 1 gfx950, -1 other
+void *g_scratch[kMaxDevices];          // device address of `scratch` per device (under g_mu)
 thread_local int g_last_hip = 0;  // hipError_t behind the last ILPM_ERR_HIP of this thread
 
 int hip_fail(hipError_t e)
@@ -283,6 +289,22 @@ int get_workspace(int dev, size_t need, hipStream_t stream, void **ws)
     return ILPM_OK;
 }
 
+// The no-alloc entry point's workspace on device `dev`: the address of that
+// device's copy of `scratch`, looked up once per device with the device
+// current (the caller's call runs on it).
+int scratch_address(int dev, void **ptr)
+{
+    std::lock_guard<std::mutex> lk(g_mu);
+    if (!g_scratch[dev]) {
+        void *p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return hip_fail(e);
+        g_scratch[dev] = p;
+    }
+    *ptr = g_scratch[dev];
+    return ILPM_OK;
+}
+
 void log_plan(const ConvShape &s, const ilpm_plan &p)
 {
     static const int on = [] {
@@ -307,14 +329,19 @@ size_t workspace_need(const ilpm_plan &p, const ConvShape &s, int epilogue)
     return (epilogue & ILPM_EPI_MAXPOOL2) ? sizeof(float) * (size_t)s.c_out * s.h_out * s.w_out : 0;
 }
 
+// The workspace comes from get_workspace, or with use_scratch from the
+// device's fixed `scratch` array (the caller has checked that it is large
+// enough).
 int run(const float *in, const float *w, const float *bias, const ConvShape &s, float *out, const ilpm_plan &p,
-        hipStream_t stream, bool packed = false, int epilogue = 0)
+        hipStream_t stream, bool packed = false, int epilogue = 0, bool use_scratch = false)
 {
     int dev = 0;
     int rc = device_check(&dev);
     if (rc != ILPM_OK) return rc;
     void *ws = nullptr;
-    rc = get_workspace(dev, workspace_need(p, s, epilogue), stream, &ws);
+    const size_t need = workspace_need(p, s, epilogue);
+    if (use_scratch) rc = need > 0 ? scratch_address(dev, &ws) : ILPM_OK;
+    else rc = get_workspace(dev, need, stream, &ws);
     if (rc != ILPM_OK) return rc;
     log_plan(s, p);
     // Launch errors are read back with hipGetLastError; drop any error an
@@ -513,6 +540,21 @@ int ilpm_conv2d_fwd(const float *in, const float *w, const float *bias, int C_in
 }
 
 int ilpm_arch_supported(const char *gcn_arch_name) { return arch_status(gcn_arch_name); }
+
+int ilpm_conv2d_fwd_noalloc(const float *in, const float *w, const float *bias, int C_in, int H, int W, int C_out,
+                            int K, int stride, int pad, float *out, hipStream_t stream)
+{
+    ConvShape s;
+    int rc = check_dims(C_in, H, W, C_out, K, stride, pad, &s);
+    if (rc != ILPM_OK) return rc;
+    rc = validate(in, w, bias, s, out);
+    if (rc != ILPM_OK) return rc;
+    ilpm_plan p;
+    rc = choose_plan(s, &p);
+    if (rc != ILPM_OK) return rc;
+    if (workspace_need(p, s, 0) > ILPM_NOALLOC_SCRATCH_BYTES) return ILPM_ERR_WORKSPACE;
+    return run(in, w, bias, s, out, p, stream, false, 0, true);
+}
 
 int ilpm_conv2d_fwd_plan(const float *in, const float *w, const float *bias, int C_in, int H, int W, int C_out,
                          int K, int stride, int pad, float *out, const ilpm_plan *plan, hipStream_t stream)
