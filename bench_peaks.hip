@@ -58,6 +58,50 @@ __global__ __launch_bounds__(256) void copy_f4(const float4 *__restrict__ src, f
     for (; i < n; i += step) dst[i] = src[i];
 }
 
+// Store-only bandwidth: 16 bytes per lane, consecutive lanes consecutive.
+__global__ __launch_bounds__(256) void fill_f4(float4 *__restrict__ dst, size_t n, float v)
+{
+    size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+    const size_t step = (size_t)gridDim.x * 256;
+    for (; i < n; i += step) dst[i] = float4{v, v, v, v};
+}
+
+// Store-only bandwidth with the layout of a 16x16 matrix-core result written
+// to NCHW: each store instruction puts 4 bytes per lane, lanes 16g..16g+15 on
+// 16 consecutive floats of row (plane) 4*blk + g, i.e. four 64-byte segments
+// `plane` floats apart; a wave writes 16 rows x 16 floats per tile, 4
+// instructions.  dst holds rows x plane floats, rows a multiple of 16 and
+// plane of 16.
+__global__ __launch_bounds__(256) void fill_tiles(float *__restrict__ dst, int rows, int plane, float v)
+{
+    const int lane = threadIdx.x & 63, g = lane >> 4, l = lane & 15;
+    const int tiles_p = plane / 16, tiles = (rows / 16) * tiles_p;
+    for (int t = blockIdx.x * 4 + (threadIdx.x >> 6); t < tiles; t += gridDim.x * 4) {
+        const int rb = t / tiles_p, pb = t - rb * tiles_p;
+        float *o = dst + (size_t)(16 * rb + 4 * g) * plane + 16 * pb + l;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) o[(size_t)r * plane] = v;
+    }
+}
+
+// fill_tiles with a cache policy on every store (buffer store, policy bits
+// as the store instruction takes them: 2 non-temporal, 16 SC1, 17 SC0+SC1).
+template <int POL>
+__global__ __launch_bounds__(256) void fill_tiles_pol(float *__restrict__ dst, int rows, int plane, float v)
+{
+    const int lane = threadIdx.x & 63, g = lane >> 4, l = lane & 15;
+    const int tiles_p = plane / 16, tiles = (rows / 16) * tiles_p;
+    const __amdgpu_buffer_rsrc_t ro =
+        __builtin_amdgcn_make_buffer_rsrc(dst, (short)0, rows * plane * 4, 0x00020000);
+    for (int t = blockIdx.x * 4 + (threadIdx.x >> 6); t < tiles; t += gridDim.x * 4) {
+        const int rb = t / tiles_p, pb = t - rb * tiles_p;
+        const int o = (16 * rb + 4 * g) * plane + 16 * pb + l;
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v), ro, (o + r * plane) * 4, 0, POL);
+    }
+}
+
 __global__ void empty_kernel() {}
 
 extern "C" {
@@ -78,6 +122,36 @@ int peak_valu_launch(float *out, int iters, int grid, hipStream_t s)
 int copy_launch(const void *src, void *dst, size_t n16, int grid, hipStream_t s)
 {
     hipLaunchKernelGGL(copy_f4, dim3(grid), dim3(256), 0, s, (const float4 *)src, (float4 *)dst, n16);
+    return (int)hipGetLastError();
+}
+
+// n16: number of 16-byte elements of dst (16-byte aligned).
+int fill_launch(void *dst, size_t n16, int grid, hipStream_t s)
+{
+    hipLaunchKernelGGL(fill_f4, dim3(grid), dim3(256), 0, s, (float4 *)dst, n16, 1.0f);
+    return (int)hipGetLastError();
+}
+
+// dst: rows x plane floats, rows and plane multiples of 16.
+int fill_tiles_launch(void *dst, int rows, int plane, int grid, hipStream_t s)
+{
+    if (rows % 16 || plane % 16) return -1;
+    hipLaunchKernelGGL(fill_tiles, dim3(grid), dim3(256), 0, s, (float *)dst, rows, plane, 1.0f);
+    return (int)hipGetLastError();
+}
+
+// The same with store cache policy pol in {0, 2, 16, 17}; rows * plane * 4 < 2^31.
+int fill_tiles_pol_launch(void *dst, int rows, int plane, int grid, int pol, hipStream_t s)
+{
+    if (rows % 16 || plane % 16 || (long long)rows * plane * 4 >= (1LL << 31)) return -1;
+    float *d = (float *)dst;
+    switch (pol) {
+    case 0: hipLaunchKernelGGL(fill_tiles_pol<0>, dim3(grid), dim3(256), 0, s, d, rows, plane, 1.0f); break;
+    case 2: hipLaunchKernelGGL(fill_tiles_pol<2>, dim3(grid), dim3(256), 0, s, d, rows, plane, 1.0f); break;
+    case 16: hipLaunchKernelGGL(fill_tiles_pol<16>, dim3(grid), dim3(256), 0, s, d, rows, plane, 1.0f); break;
+    case 17: hipLaunchKernelGGL(fill_tiles_pol<17>, dim3(grid), dim3(256), 0, s, d, rows, plane, 1.0f); break;
+    default: return -1;
+    }
     return (int)hipGetLastError();
 }
 

@@ -15,10 +15,14 @@
 //            channels staged in LDS.
 // Variant 1: no LDS, one thread per output element reading global memory;
 //            the fallback for shapes whose halo does not fit LDS.
+// Variants 2..: low-channel layers (C_in*K*K at most 28 or 64), see
+//            conv_direct_mfma below.
 #include "internal.h"
 
 namespace ilpm {
 namespace {
+
+typedef float floatx4 __attribute__((ext_vector_type(4)));
 
 constexpr int kTileH = 8;
 constexpr int kTileW = 32;
@@ -145,6 +149,179 @@ __global__ __launch_bounds__(kThreads) void conv_direct_global(const float *__re
     out[i] = a.relu && v < 0.f ? 0.f : v;
 }
 
+// ---- Low-channel layers on the matrix cores ----
+//
+// When C_in*K*K is small (the network's first layer: 3 input channels, 27
+// products per output) the whole contraction is one short run of matrix
+// instructions, and the layer's time is its output write (VGG-16's first
+// layer writes 12.85 MB and reads 0.6 MB).  What matters is that stores start
+// early and keep streaming, so the work is cut into many small independent
+// wave tiles -- no LDS, no barrier, several waves per SIMD -- each of which
+// gathers its own inputs, runs its matrix instructions and stores its
+// results straight from the accumulators.
+//
+// A wave owns 16*MB output channels x 16*NPB consecutive output pixels (in
+// the row-major order of the output plane, so a block may span two rows).
+// The contraction index is k = (ci*K + kh)*K + kw, i.e. an OIHW weight row
+// read as it is; step s of the v_mfma_f32_16x16x4_f32 chain covers k = 4s..
+// 4s+3, lane (g, l) supplying A = w[co0 + 16m + l][4s + g] (loaded once) and
+// B = the input tap of k = 4s + g for pixel 16n + l of the tile, gathered
+// with buffer loads whose offset is pushed past the range for padding taps
+// and for k >= C_in*K*K (a buffer load out of range returns 0).
+//
+// Divisions by sizes fixed at launch are multiply-shifts with multipliers
+// from the host: k / d = (k * ceil(2^16 / d)) >> 16, exact for k < 64 and
+// d <= 64 (the error k*(ceil(2^16/d) - 2^16/d)/2^16 < 2^-10 stays below the
+// 1/d gap to the next integer), and p / W_out = mulhi(p, ceil(2^32 / W_out)),
+// exact while p * W_out < 2^32 (checked when the plan is made) -- for W_out
+// >= 2; the multiplier for W_out = 1 would be 2^32, so that case is p itself.
+struct LowcArgs {
+    int c_in, h, w, c_out, k, stride, pad, h_out, w_out;
+    int kt;          // C_in*K*K
+    int units;       // wave tiles
+    int co_groups;   // output-channel groups of 16*MB
+    int relu;
+    unsigned m_kk, m_k;  // ceil(2^16 / (K*K)), ceil(2^16 / K)
+    unsigned m_w;        // ceil(2^32 / W_out) for W_out >= 2 (unused for W_out = 1)
+};
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t lowc_rsrc(const float *base, unsigned bytes)
+{
+    const uint64_t b = reinterpret_cast<uint64_t>(base);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)b);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(b >> 32));
+    float *q = reinterpret_cast<float *>(((uint64_t)hi << 32) | lo);
+    return __builtin_amdgcn_make_buffer_rsrc(q, (short)0, (int)__builtin_amdgcn_readfirstlane(bytes), 0x00020000);
+}
+
+template <int MB, int NPB, int STEPS>
+__global__ __launch_bounds__(256) void conv_direct_mfma(const float *__restrict__ x, const float *__restrict__ wt,
+                                                        const float *__restrict__ bias, float *__restrict__ out,
+                                                        LowcArgs a)
+{
+    constexpr unsigned kFar = 0x80000000u;  // past every descriptor's range
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int g = lane >> 4, l = lane & 15;
+    // Workgroups are dealt to the 8 XCDs round-robin; give each XCD a
+    // contiguous run of tiles so that neighbouring pixels (shared input rows)
+    // meet in one L2.
+    const int nwg = (int)gridDim.x;
+    const int xcd = (int)blockIdx.x % 8, slot = (int)blockIdx.x / 8;
+    const int per = nwg / 8, extra = nwg % 8;
+    const int lin = xcd * per + min(xcd, extra) + slot;
+    const int unit = lin * 4 + wave;
+    if (unit >= a.units) return;  // whole waves only; the kernel has no barrier
+    const int cg = unit % a.co_groups;
+    const int pg = unit / a.co_groups;
+    const int co0 = cg * 16 * MB;
+    const int plane = a.h_out * a.w_out;
+
+    const __amdgpu_buffer_rsrc_t rw = lowc_rsrc(wt, (unsigned)a.c_out * a.kt * 4u);
+    const __amdgpu_buffer_rsrc_t rx = lowc_rsrc(x, (unsigned)a.c_in * a.h * a.w * 4u);
+    const __amdgpu_buffer_rsrc_t ro = lowc_rsrc(out, (unsigned)a.c_out * plane * 4u);
+
+    // Input pixel of each of this lane's blocks: top-left tap (ih0, iw0).
+    int ih0[NPB], iw0[NPB];
+    bool pix_ok[NPB];
+#pragma unroll
+    for (int n = 0; n < NPB; ++n) {
+        const int p = (pg * NPB + n) * 16 + l;
+        const int oh = a.w_out == 1 ? p : (int)__umulhi((unsigned)p, a.m_w), ow = p - oh * a.w_out;
+        pix_ok[n] = p < plane;
+        ih0[n] = oh * a.stride - a.pad;
+        iw0[n] = ow * a.stride - a.pad;
+    }
+    // B gathers, all issued before the first matrix instruction.
+    float bv[STEPS][NPB];
+#pragma unroll
+    for (int s = 0; s < STEPS; ++s) {
+        const int k = 4 * s + g;
+        const int ci = (int)(((unsigned)k * a.m_kk) >> 16), t = k - ci * a.k * a.k;
+        const int kh = (int)(((unsigned)t * a.m_k) >> 16), kw = t - kh * a.k;
+#pragma unroll
+        for (int n = 0; n < NPB; ++n) {
+            const int ih = ih0[n] + kh, iw = iw0[n] + kw;
+            const bool ok = k < a.kt && pix_ok[n] && (unsigned)ih < (unsigned)a.h && (unsigned)iw < (unsigned)a.w;
+            const unsigned off = ok ? (unsigned)((ci * a.h + ih) * a.w + iw) * 4u : kFar;
+            bv[s][n] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rx, (int)off, 0, 0));
+        }
+    }
+    // A: this lane's weights, w[co0 + 16m + l][4s + g].
+    float av[MB][STEPS];
+#pragma unroll
+    for (int m = 0; m < MB; ++m) {
+        const int co = co0 + 16 * m + l;
+#pragma unroll
+        for (int s = 0; s < STEPS; ++s) {
+            const int k = 4 * s + g;
+            const unsigned off = (co < a.c_out && k < a.kt) ? (unsigned)(co * a.kt + k) * 4u : kFar;
+            av[m][s] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rw, (int)off, 0, 0));
+        }
+    }
+    // Accumulators start from the bias: register r of block (m, n) is output
+    // channel co0 + 16m + 4g + r at pixel 16n + l.
+    floatx4 acc[MB][NPB];
+#pragma unroll
+    for (int m = 0; m < MB; ++m) {
+        float b4[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int co = co0 + 16 * m + 4 * g + r;
+            b4[r] = (bias != nullptr && co < a.c_out) ? bias[co] : 0.f;
+        }
+#pragma unroll
+        for (int n = 0; n < NPB; ++n) acc[m][n] = floatx4{b4[0], b4[1], b4[2], b4[3]};
+    }
+#pragma unroll
+    for (int s = 0; s < STEPS; ++s)
+#pragma unroll
+        for (int n = 0; n < NPB; ++n)
+#pragma unroll
+            for (int m = 0; m < MB; ++m)
+                acc[m][n] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[m][s], bv[s][n], acc[m][n], 0, 0, 0);
+    // Stores: lanes along pixels (16 consecutive pixels of one channel per
+    // lane group); channels past C_out and pixels past the plane go out of
+    // range and are dropped.
+#pragma unroll
+    for (int m = 0; m < MB; ++m) {
+        const int co = co0 + 16 * m + 4 * g;
+#pragma unroll
+        for (int n = 0; n < NPB; ++n) {
+            const int p = (pg * NPB + n) * 16 + l;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const bool ok = pix_ok[n] && co + r < a.c_out;
+                const unsigned off = ok ? (unsigned)((co + r) * plane + p) * 4u : kFar;
+                float v = acc[m][n][r];
+                if (a.relu && v < 0.f) v = 0.f;
+                __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v), ro, (int)off, 0, 0);
+            }
+        }
+    }
+}
+
+struct LowcVariant {
+    const char *name;
+    int mb, npb, steps;
+    void (*launch)(dim3, hipStream_t, const float *, const float *, const float *, float *, const LowcArgs &);
+};
+
+template <int MB, int NPB, int STEPS>
+void lowc_launch(dim3 grid, hipStream_t st, const float *x, const float *w, const float *b, float *o,
+                 const LowcArgs &a)
+{
+    hipLaunchKernelGGL((conv_direct_mfma<MB, NPB, STEPS>), grid, dim3(256), 0, st, x, w, b, o, a);
+}
+
+const LowcVariant kLowc[] = {
+    {"direct_mfma_k28_co16_px16", 1, 1, 7, &lowc_launch<1, 1, 7>},
+    {"direct_mfma_k28_co64_px32", 4, 2, 7, &lowc_launch<4, 2, 7>},
+    {"direct_mfma_k64_co16_px32", 1, 2, 16, &lowc_launch<1, 2, 16>},
+};
+constexpr int kNumLowc = sizeof(kLowc) / sizeof(kLowc[0]);
+constexpr int kFirstLowc = 2;  // direct variants 0 and 1 are the VALU kernels
+
 DirectArgs make_args(const ConvShape &s)
 {
     DirectArgs a;
@@ -171,25 +348,38 @@ int lds_chunk(const ConvShape &s)
 
 }  // namespace
 
-int direct_num_variants() { return 2; }
+int direct_num_variants() { return kFirstLowc + kNumLowc; }
 
 const char *direct_variant_name(int v)
 {
     if (v == 0) return "direct_lds_t8x32_co16";
     if (v == 1) return "direct_global";
+    if (v >= kFirstLowc && v < kFirstLowc + kNumLowc) return kLowc[v - kFirstLowc].name;
     return nullptr;
 }
 
 bool direct_variant_info(int v, int *k, int *stride, int *tile_h, int *tile_w, int *co_tile)
 {
-    if (v < 0 || v >= 2) return false;
+    if (v < 0 || v >= direct_num_variants()) return false;
     *k = 0;
     *stride = 0;
+    if (v >= kFirstLowc) {
+        // A wave's tile: 16*NPB consecutive pixels of the output plane.
+        const LowcVariant &d = kLowc[v - kFirstLowc];
+        *tile_h = 1;
+        *tile_w = 16 * d.npb;
+        *co_tile = 16 * d.mb;
+        return true;
+    }
     *tile_h = v == 0 ? kTileH : 1;
     *tile_w = v == 0 ? kTileW : 1;
     *co_tile = v == 0 ? kCoGroup : 1;
     return true;
 }
+
+bool direct_is_lowc(int v) { return v >= kFirstLowc && v < kFirstLowc + kNumLowc; }
+
+int direct_lowc_max_kt(int v) { return direct_is_lowc(v) ? 4 * kLowc[v - kFirstLowc].steps : 0; }
 
 bool direct_make_plan(const ConvShape &s, int variant, ilpm_plan *p)
 {
@@ -215,6 +405,27 @@ bool direct_make_plan(const ConvShape &s, int variant, ilpm_plan *p)
         q.grid = (int)(tiles * groups);
         const long halo = ((long)cc * a.halo_h * a.halo_w + 3) & ~3L;
         q.lds_bytes = (int)(sizeof(float) * (halo + (long)cc * s.k * s.k * kCoGroup));
+    } else if (variant >= kFirstLowc && variant < kFirstLowc + kNumLowc) {
+        const LowcVariant &d = kLowc[variant - kFirstLowc];
+        const int64_t kt = (int64_t)s.c_in * s.k * s.k;
+        const int64_t plane = (int64_t)s.h_out * s.w_out;
+        // The whole contraction in one run of matrix instructions; byte
+        // offsets of 31 bits (input, weights) and 30 bits (output).
+        if (kt > 4 * d.steps) return false;
+        // p / W_out by multiply-shift (see LowcArgs): exact while p * W_out < 2^32.
+        if ((plane + 16 * d.npb) * (int64_t)s.w_out >= (1LL << 32)) return false;
+        if ((int64_t)s.c_in * s.h * s.w * 4 >= (1LL << 31) || (int64_t)s.c_out * kt * 4 >= (1LL << 31) ||
+            (int64_t)s.c_out * plane * 4 >= (1LL << 30))
+            return false;
+        const int64_t co_groups = (s.c_out + 16 * d.mb - 1) / (16 * d.mb);
+        const int64_t units = co_groups * ((plane + 16 * d.npb - 1) / (16 * d.npb));
+        if (units > 0x7fffffffLL - 3) return false;
+        q.tile_h = 1;
+        q.tile_w = 16 * d.npb;
+        q.co_tile = 16 * d.mb;
+        q.ci_chunk = s.c_in;
+        q.grid = (int)((units + 3) / 4);
+        q.lds_bytes = 0;
     } else if (variant == 1) {
         const int64_t total = (int64_t)s.c_out * s.h_out * s.w_out;
         const int64_t blocks = (total + kThreads - 1) / kThreads;
@@ -237,6 +448,21 @@ hipError_t direct_launch(const ilpm_plan &p, const ConvShape &s, const float *x,
 {
     DirectArgs a = make_args(s);
     a.relu = relu ? 1 : 0;
+    if (direct_is_lowc(p.variant)) {
+        const LowcVariant &d = kLowc[p.variant - kFirstLowc];
+        LowcArgs la;
+        la.c_in = s.c_in; la.h = s.h; la.w = s.w; la.c_out = s.c_out; la.k = s.k;
+        la.stride = s.stride; la.pad = s.pad; la.h_out = s.h_out; la.w_out = s.w_out;
+        la.kt = s.c_in * s.k * s.k;
+        la.co_groups = ceil_div(s.c_out, 16 * d.mb);
+        la.units = la.co_groups * ceil_div(s.h_out * s.w_out, 16 * d.npb);
+        la.relu = relu ? 1 : 0;
+        la.m_kk = (65536u + (unsigned)(s.k * s.k) - 1) / (unsigned)(s.k * s.k);
+        la.m_k = (65536u + (unsigned)s.k - 1) / (unsigned)s.k;
+        la.m_w = s.w_out >= 2 ? (unsigned)(((1ull << 32) + (uint64_t)s.w_out - 1) / (uint64_t)s.w_out) : 0u;
+        d.launch(dim3(p.grid), stream, x, w, bias, out, la);
+        return hipGetLastError();
+    }
     if (p.variant == 0) {
         a.chunk = p.ci_chunk;
         const int tiles = ceil_div(s.h_out, kTileH) * ceil_div(s.w_out, kTileW);

@@ -19,6 +19,10 @@ int direct_num_variants();
 bool direct_variant_info(int v, int *k, int *stride, int *tile_h, int *tile_w, int *co_tile);
 const char *direct_variant_name(int v);
 bool direct_make_plan(const ConvShape &s, int variant, ilpm_plan *p);
+// The low-channel matrix-core variants (the whole C_in*K*K contraction in one
+// chain of matrix instructions) and the largest C_in*K*K each takes.
+bool direct_is_lowc(int v);
+int direct_lowc_max_kt(int v);
 // relu: store max(conv + bias, 0).
 hipError_t direct_launch(const ilpm_plan &p, const ConvShape &s, const float *x, const float *w,
                          const float *bias, float *out, hipStream_t stream, bool relu);

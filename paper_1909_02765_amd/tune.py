@@ -79,10 +79,59 @@ def time_plan(torch, ilpm, bufs, shape, plan, reps):
     return e0.elapsed_time(e1) * 1000.0 / reps
 
 
-def sweep(shapes, reps=100):
+def time_plan_graph(torch, ilpm, bufs, shape, plan, reps, per_graph=20):
+    """Mean us per call with the calls replayed from a captured HIP graph:
+    the kernels' own rate, without the host's launch cost between calls
+    (which bounds eager timing of the smallest layers)."""
+    c_in, h, w, c_out, k, s, p = shape
+    x, wt, out = bufs
+    stream = torch.cuda.Stream()
+    stream.wait_stream(torch.cuda.current_stream())
+    args = (ctypes.c_void_p(x.data_ptr()), ctypes.c_void_p(wt.data_ptr()), None, c_in, h, w, c_out, k, s, p,
+            ctypes.c_void_p(out.data_ptr()), ctypes.byref(plan), ctypes.c_void_p(stream.cuda_stream))
+    f = ilpm.lib.ilpm_conv2d_fwd_plan
+    with torch.cuda.stream(stream):
+        for _ in range(3):
+            rc = f(*args)
+            if rc != 0:
+                raise ilpm.IlpmError(rc, "ilpm_conv2d_fwd_plan")
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
+            for _ in range(per_graph):
+                f(*args)
+    torch.cuda.synchronize()
+    n = max(1, reps // per_graph)
+    for _ in range(max(1, n // 4)):
+        g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(n):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) * 1000.0 / (n * per_graph)
+
+
+def spin_up(torch, ms=300.0):
+    """Untimed matrix work for `ms` milliseconds of wall clock, so that the
+    first shape is not timed while the GPU is still ramping up."""
+    import time
+    a = torch.randn((2048, 2048), device="cuda")
+    t0 = time.perf_counter()
+    while (time.perf_counter() - t0) * 1e3 < ms:
+        for _ in range(10):
+            a = a @ a * 1e-3
+        torch.cuda.synchronize()
+
+
+def sweep(shapes, reps=100, graph=False):
     import torch
     import paper_1909_02765_amd as ilpm
     torch.cuda.set_device(0)
+    spin_up(torch)
+    timer = time_plan_graph if graph else time_plan
     result = {}
     for shape in shapes:
         c_in, h, w, c_out, k, s, p = shape
@@ -94,7 +143,7 @@ def sweep(shapes, reps=100):
         for plan in candidate_plans(ilpm, shape):
             if plan.path == ilpm.PATH_DIRECT and plan.variant == 1 and c_in * c_out * ho * wo * k * k > 3e8:
                 continue  # the plain fallback is far too slow to matter here
-            us = time_plan(torch, ilpm, (x, wt, out), shape, plan, reps)
+            us = timer(torch, ilpm, (x, wt, out), shape, plan, reps)
             rows.append(({"variant": ilpm.variant_name(plan.path, plan.variant), "path": plan.path,
                           "splits": plan.splits, "us": round(us, 3)}, plan))
         rows.sort(key=lambda r: r[0]["us"])
@@ -106,7 +155,7 @@ def sweep(shapes, reps=100):
             row["us_refined"] = float("inf")
         for _ in range(3):
             for row, plan in finalists:
-                us = time_plan(torch, ilpm, (x, wt, out), shape, plan, reps * 10)
+                us = timer(torch, ilpm, (x, wt, out), shape, plan, reps * 10)
                 row["us_refined"] = round(min(row["us_refined"], us), 3)
         finalists.sort(key=lambda r: r[0]["us_refined"])
         ranked = [row for row, _ in finalists + rows[FINALISTS:]]
@@ -147,14 +196,35 @@ def choose(entry, incumbent):
     return best
 
 
+def read_comments(path=INC):
+    """The timing comment of each table line, by shape key."""
+    out = {}
+    if not os.path.exists(path):
+        return out
+    for line in open(path):
+        line = line.strip()
+        if line.startswith("{") and "//" in line:
+            body = line[1:line.index("}")]
+            out[",".join(t.strip() for t in body.split(",")[:7])] = line[line.index("//"):]
+    return out
+
+
 def emit(table, path=INC):
+    """Rewrite the table: shapes in `table` (a sweep) get their chosen plan;
+    every other shape keeps its current line."""
     current = read_table(path)
-    lines = ["// {C_in, H, W, C_out, K, stride, pad, \"variant\", splits}",
-             "// Fastest measured plan per shape on one MI355X (written by tune.py --emit)."]
-    for key, v in sorted(table.items(), key=lambda kv: [int(t) for t in kv[0].split(",")]):
+    comments = read_comments(path)
+    rows = {}
+    for key, (variant, splits) in current.items():
+        rows[key] = "{%s, \"%s\", %d},  %s" % (key.replace(",", ", "), variant, splits, comments.get(key, ""))
+    for key, v in table.items():
         b = choose(v, current.get(key))
         us = b.get("us_refined", b["us"])
-        lines.append("{%s, \"%s\", %d},  // %.2f us" % (key.replace(",", ", "), b["variant"], b["splits"], us))
+        rows[key] = "{%s, \"%s\", %d},  // %.2f us" % (key.replace(",", ", "), b["variant"], b["splits"], us)
+    lines = ["// {C_in, H, W, C_out, K, stride, pad, \"variant\", splits}",
+             "// Fastest measured plan per shape on one MI355X (written by tune.py --emit)."]
+    for key in sorted(rows, key=lambda k: [int(t) for t in k.split(",")]):
+        lines.append(rows[key].rstrip())
     with open(path, "w") as f:
         f.write("\n".join(lines) + "\n")
 
@@ -164,12 +234,18 @@ def main():
     ap.add_argument("--out", default=None, help="write the sweep as JSON")
     ap.add_argument("--emit", default=None, help="JSON from a sweep -> csrc/tuned_plans.inc")
     ap.add_argument("--reps", type=int, default=100)
+    ap.add_argument("--shapes", nargs="*", default=None, metavar="C_in,H,W,C_out,K,stride,pad",
+                    help="sweep only these shapes (default: every workload and VGG-16 / ResNet layer)")
+    ap.add_argument("--graph", action="store_true",
+                    help="time calls replayed from a HIP graph (for launch-bound layers)")
     args = ap.parse_args()
     if args.emit:
         with open(args.emit) as f:
             emit(json.load(f))
         return
-    table = sweep(default_shapes(), args.reps)
+    shapes = ([tuple(int(t) for t in sh.split(",")) for sh in args.shapes] if args.shapes
+              else default_shapes())
+    table = sweep(shapes, args.reps, args.graph)
     if args.out:
         with open(args.out, "w") as f:
             json.dump(table, f, indent=1)

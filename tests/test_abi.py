@@ -83,7 +83,9 @@ def test_set_workspace_rejects_misaligned():
 
 
 def test_variants_table():
-    assert ilpm.num_variants(ilpm.PATH_DIRECT) == 2
+    nd = ilpm.num_variants(ilpm.PATH_DIRECT)
+    assert nd >= 3
+    assert [ilpm.variant_name(ilpm.PATH_DIRECT, v) for v in (0, 1)] == ["direct_lds_t8x32_co16", "direct_global"]
     n = ilpm.num_variants(ilpm.PATH_IGEMM)
     assert n >= 4
     assert ilpm.num_variants(7) == 0
@@ -388,3 +390,24 @@ def test_split_sum_mode_switch():
                 ilpm.set_split_sum(bad)
     finally:
         ilpm.set_split_sum(ilpm.SPLIT_SUM_FUSED)
+
+
+def test_low_channel_direct_variants_plan_only_short_contractions():
+    """The low-channel matrix-core direct kernels take a shape only when the
+    whole C_in*K*K contraction fits their one chain of matrix instructions."""
+    lowc = [v for v in range(ilpm.num_variants(ilpm.PATH_DIRECT))
+            if ilpm.variant_name(ilpm.PATH_DIRECT, v).startswith("direct_mfma_k28")]
+    assert lowc
+    for v in lowc:
+        p = ilpm.plan_variant(3, 224, 224, 64, 3, 1, 1, ilpm.PATH_DIRECT, v)   # 27 products
+        info = ilpm.variant_info(ilpm.PATH_DIRECT, v)
+        units = -(-64 // info["co_tile"]) * -(-224 * 224 // info["tile_w"])
+        assert p.grid == -(-units // 4) and p.block == 256 and p.lds_bytes == 0 and p.workspace_bytes == 0
+        with pytest.raises(ilpm.IlpmError):
+            ilpm.plan_variant(4, 224, 224, 64, 3, 1, 1, ilpm.PATH_DIRECT, v)  # 36 > 28
+    big = [v for v in range(ilpm.num_variants(ilpm.PATH_DIRECT))
+           if ilpm.variant_name(ilpm.PATH_DIRECT, v).startswith("direct_mfma_k64")]
+    for v in big:
+        ilpm.plan_variant(7, 30, 30, 20, 3, 2, 1, ilpm.PATH_DIRECT, v)        # 63
+        with pytest.raises(ilpm.IlpmError):
+            ilpm.plan_variant(8, 30, 30, 20, 3, 1, 1, ilpm.PATH_DIRECT, v)    # 72 > 64

@@ -38,3 +38,13 @@ def test_emit_round_trips(tmp_path):
              "64,56,56,64,3,1,1": _entry([{"variant": "y", "path": 1, "splits": 3, "us": 9.0}])}
     tune.emit(table, path)
     assert tune.read_table(path) == {"3,32,32,16,3,1,1": ("x", 1), "64,56,56,64,3,1,1": ("y", 3)}
+
+
+def test_emit_merges_a_partial_sweep(tmp_path):
+    """Shapes the sweep did not time keep their current line."""
+    path = os.path.join(tmp_path, "plans.inc")
+    tune.emit({"3,32,32,16,3,1,1": _entry([{"variant": "x", "path": 1, "splits": 1, "us": 4.0}]),
+               "64,56,56,64,3,1,1": _entry([{"variant": "y", "path": 1, "splits": 3, "us": 9.0}])}, path)
+    tune.emit({"64,56,56,64,3,1,1": _entry([{"variant": "z", "path": 1, "splits": 2, "us": 5.0,
+                                            "us_refined": 5.0}])}, path)
+    assert tune.read_table(path) == {"3,32,32,16,3,1,1": ("x", 1), "64,56,56,64,3,1,1": ("z", 2)}
