@@ -352,6 +352,8 @@ def main():
     ap.add_argument("--peaks", action="store_true", help="also measure the MI355X ceilings")
     ap.add_argument("--copy-calib", type=int, default=0, metavar="MIB",
                     help="also run a plain copy of MIB MiB (counter calibration under rocprofv3)")
+    ap.add_argument("--lds-probe", action="store_true",
+                    help="only run the LDS bank probe over lds_banks.probe_patterns() (for rocprofv3 --pmc)")
     ap.add_argument("--vgg16-stack", type=int, default=0, metavar="REPS",
                     help="only time the VGG-16 stack end to end, REPS passes per timing (kernel traces)")
     args = ap.parse_args()
@@ -369,6 +371,10 @@ def main():
     import paper_1909_02765_amd as ilpm
     import workloads
     SPINUP["ms"] = max(0.0, args.spinup_ms)
+
+    if args.lds_probe:
+        print(json.dumps(run_lds_probe(torch)))
+        return
 
     if args.vgg16_stack:
         rows = bench_vgg16_stack(torch, ilpm, workloads, args.vgg16_stack)
@@ -534,6 +540,28 @@ def bench_vgg16_layers(torch, ilpm, workloads, steps):
         ilpm.relu_(out)
         x = ilpm.maxpool2x2(out) if pool else out
     return out_rows
+
+
+def run_lds_probe(torch, iters=1000):
+    """One lds_probe dispatch per address pattern of lds_banks.probe_patterns(),
+    in order; returns the pattern names (the dispatch order, for matching the
+    counter rows of a rocprofv3 run)."""
+    import ctypes
+    from paper_1909_02765_amd import lds_banks
+    lib = ctypes.CDLL(os.path.join(ROOT, "bench_peaks.so"))
+    out = torch.empty(64, device="cuda")
+    names = []
+    for name, width, table in lds_banks.probe_patterns():
+        if len(table) != 64 or any(a < 0 or a + width > 16384 or a % width for a in table):
+            raise ValueError(f"probe pattern {name} out of range")
+        t = torch.tensor(table, dtype=torch.int32, device="cuda")
+        rc = lib.lds_probe_launch(ctypes.c_void_p(t.data_ptr()), ctypes.c_void_p(out.data_ptr()), iters, width,
+                                  ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+        if rc != 0:
+            raise RuntimeError(f"lds_probe_launch: {rc}")
+        torch.cuda.synchronize()
+        names.append(name)
+    return {"lds_probe_iters": iters, "patterns": names}
 
 
 def bench_vgg16(torch, ilpm, workloads, steps):

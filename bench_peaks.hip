@@ -102,6 +102,36 @@ __global__ __launch_bounds__(256) void fill_tiles_pol(float *__restrict__ dst, i
     }
 }
 
+// LDS bank probe: one 64-thread workgroup reads LDS `iters` times, each lane
+// at its own word address table[lane] (WIDTH dwords per lane: ds_read_b32,
+// b64 or b128), so that SQ_LDS_BANK_CONFLICT / SQ_INSTS_LDS of the dispatch
+// give the cost of that address pattern.  Addresses lie in [0, 16384 - WIDTH].
+template <int WIDTH>
+__global__ __launch_bounds__(64) void lds_probe(const int *__restrict__ table, float *__restrict__ out, int iters)
+{
+    __shared__ __attribute__((aligned(16))) float buf[16384];
+    for (int i = threadIdx.x; i < 16384; i += 64) buf[i] = (float)i;
+    __syncthreads();
+    const unsigned addr = (unsigned)table[threadIdx.x] * 4u;
+    float s = 0.f;
+    for (int it = 0; it < iters; ++it) {
+        if constexpr (WIDTH == 1) {
+            float v;
+            asm volatile("ds_read_b32 %0, %1\n s_waitcnt lgkmcnt(0)" : "=v"(v) : "v"(addr) : "memory");
+            s += v;
+        } else if constexpr (WIDTH == 2) {
+            float2 v;
+            asm volatile("ds_read_b64 %0, %1\n s_waitcnt lgkmcnt(0)" : "=v"(v) : "v"(addr) : "memory");
+            s += v.x + v.y;
+        } else {
+            float4 v;
+            asm volatile("ds_read_b128 %0, %1\n s_waitcnt lgkmcnt(0)" : "=v"(v) : "v"(addr) : "memory");
+            s += v.x + v.y + v.z + v.w;
+        }
+    }
+    out[threadIdx.x] = s;
+}
+
 __global__ void empty_kernel() {}
 
 extern "C" {
@@ -152,6 +182,16 @@ int fill_tiles_pol_launch(void *dst, int rows, int plane, int grid, int pol, hip
     case 17: hipLaunchKernelGGL(fill_tiles_pol<17>, dim3(grid), dim3(256), 0, s, d, rows, plane, 1.0f); break;
     default: return -1;
     }
+    return (int)hipGetLastError();
+}
+
+// table: 64 word addresses in [0, 16384 - width], multiples of width; width 1, 2 or 4.
+int lds_probe_launch(const int *table, float *out, int iters, int width, hipStream_t s)
+{
+    if (width == 1) hipLaunchKernelGGL(lds_probe<1>, dim3(1), dim3(64), 0, s, table, out, iters);
+    else if (width == 2) hipLaunchKernelGGL(lds_probe<2>, dim3(1), dim3(64), 0, s, table, out, iters);
+    else if (width == 4) hipLaunchKernelGGL(lds_probe<4>, dim3(1), dim3(64), 0, s, table, out, iters);
+    else return -1;
     return (int)hipGetLastError();
 }
 

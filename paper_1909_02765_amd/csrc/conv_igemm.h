@@ -135,17 +135,6 @@ using ig::Variant;
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void *lds_ptr_t;
 
-// Halo row length in LDS: the smallest r >= hc that puts successive channel
-// planes (hr * r words) on different bank halves.
-constexpr int halo_row(int hr, int hc, int s)
-{
-    for (int r = hc; r < hc + 64; ++r) {
-        if (s % 2 == 1 && (hr * r) % 32 == 16) return r;
-        if (s % 2 == 0 && (hr * r) % 2 == 1) return r;
-    }
-    return hc;
-}
-
 constexpr int round64(int n) { return (n + 63) / 64 * 64; }
 constexpr int cmax(int a, int b) { return a > b ? a : b; }
 
@@ -181,8 +170,21 @@ struct Cfg {
     // MFMA step on different LDS banks (with 256-word planes they share
     // banks, and the stages run ~25% slower).  Other halos pad the rows.
     static constexpr bool QUAD = S == 1 && HC == 16 && HR == 16 && NW % 4 == 0;
-    static constexpr int HCP = QUAD ? 16 : halo_row(HR, HC, S);
-    static constexpr int PL = HR * HCP + (QUAD ? 16 : 0);  // channel plane stride
+    // Other halos are stored unpadded (HCP = HC, PL = HR*HC).  Against a bank
+    // model of gfx950's LDS fitted to hardware counters (32 banks of 4 bytes,
+    // a ds_read_b32 served as two half-waves of 32 lanes, one pass per
+    // distinct word a bank holds in a half), these tight layouts cost at most
+    // two extra passes per B read, and layouts padded to make the reads
+    // conflict-free measured slower (ResNet conv4.x 7.25 us padded, 6.75 us
+    // tight; the strided layer 5.95 / 5.31; the 5x5 layer 13.08 / 12.57): the
+    // padding is halo DMA the small-tile kernels wait on, while a conflict
+    // adds a pass to reads issued steps ahead.  The 16x16 halo (14x14 tiles)
+    // keeps 16-word rows for its four-rows-per-instruction DMA, and with
+    // 14-pixel rows in them every 16-pixel block spans two rows: two of its
+    // banks hold a word of each of the half-wave's two channels whatever the
+    // plane pitch, one extra pass per half on 12 of the 13 blocks.
+    static constexpr int HCP = QUAD ? 16 : HC;
+    static constexpr int PL = QUAD ? HR * HCP + 16 : HR * HC;  // channel plane stride
     static constexpr int COT = NWC * 16 * MA;
     // A tile of 16*q + t pixels, t in 1..4, computes its last pixel block with
     // the 4x4x1 matrix instruction (16 blocks of 4 channels x 4 pixels, one k
@@ -213,12 +215,16 @@ struct Cfg {
     // weights from OIHW (16 different rows per load instruction, which with
     // small tiles leaves every stage waiting on the L1), a stage's weight
     // block -- COT output channels x CC input channels x KK taps -- is copied
-    // after the halo by 16-byte-per-lane DMA of contiguous OIHW runs: output
-    // channel r at row r*ROW, input channel c at +c*KKP, taps padded to KKP =
-    // KK rounded up to 4, so a 4-tap piece never mixes channels.  The matrix
-    // instructions read their A operands from LDS four taps at a time;
-    // ROW/4 odd puts the eight lanes of each 128-byte pass of such a read on
-    // different banks.  Piece j of a run holds taps 4j..4j+3, except the last
+    // after the halo by 16-byte-per-lane DMA of contiguous OIHW runs: input
+    // channel c at plane c*CPL, output channel r at row r*KKP within it, taps
+    // padded to KKP = KK rounded up to 4, so a 4-tap piece never mixes
+    // channels.  The matrix instructions read their A operands from LDS four
+    // taps at a time (ds_read_b128), lane (g, l) at plane g, row l: a KKP-word
+    // row pitch and a plane pitch COT*KKP, a multiple of 64 words, measured
+    // conflict-free on gfx950 (a 12- or 28-word pitch puts the 16 lanes of a
+    // plane on 16 disjoint 4-bank groups); the earlier layout, rows of
+    // CC*KKP+4 words with channels 12 words apart, took 4 extra passes per
+    // read.  Piece j of a run holds taps 4j..4j+3, except the last
     // one (j = NJ-1), which holds the run's last four taps KK-4..KK-1: every
     // 16-byte load then lies inside its own (output, input) channel pair's
     // run, so no load reaches past the run, let alone past the tensor.
@@ -230,8 +236,8 @@ struct Cfg {
     // First tap of piece j, and where tap t lies within its piece t / 4.
     __host__ __device__ static constexpr int piece_tap0(int j) { return j < NJ - 1 ? 4 * j : KK - 4; }
     __host__ __device__ static constexpr int piece_pos(int t) { return t - piece_tap0(t / 4); }
-    static constexpr int ROW = (CC * KKP + 4) / 8 * 8 + 4;  // >= CC*KKP, = 4 mod 8
-    static constexpr int NIXW = WL ? (COT * ROW + 255) / 256 : 0;  // weight DMA instructions (64 lanes x 4 words)
+    static constexpr int CPL = COT * KKP;  // weight plane per input channel: a multiple of 64 words
+    static constexpr int NIXW = WL ? (CC * CPL + 255) / 256 : 0;  // weight DMA instructions (64 lanes x 4 words)
     static constexpr int WSZ = WL ? NIXW * 256 : 0;
     static constexpr int SBUF = XSZ + WSZ;  // one stage buffer: halo, then weights
     // LDS for the cross-wave sum of the NWK partial accumulators.
@@ -471,8 +477,8 @@ struct WlLanes {
 #pragma unroll
         for (int j = 0; j < XPTW; ++j) {
             const int q = (j * C::NW + wave) * 64 + lane;  // 4-word piece of the weight area
-            const int r = q / (C::ROW / 4), rem = q - r * (C::ROW / 4);
-            const int c = rem / (C::KKP / 4), piece = rem - c * (C::KKP / 4);
+            const int c = q / (C::CPL / 4), rem = q - c * (C::CPL / 4);
+            const int r = rem / (C::KKP / 4), piece = rem - r * (C::KKP / 4);
             const int co = co0 + r;
             const bool ok = r < C::COT && c < C::CC && co < c_out;
             off[j] = ok ? (unsigned)(co * c_in * C::KK + c * C::KK + C::piece_tap0(piece)) * 4u : 0x80000000u;
@@ -728,7 +734,7 @@ __device__ __forceinline__ void compute_stage(const float *xl, const AStage<C> &
 #pragma unroll
                 for (int c4 = 0; c4 < C::G4; ++c4)
                     ach[slot][m][c4] =
-                        *reinterpret_cast<const floatx4 *>(xl + A.base[m] + c4 * 4 * C::NWK * C::KKP + 4 * j);
+                        *reinterpret_cast<const floatx4 *>(xl + A.base[m] + c4 * 4 * C::NWK * C::CPL + 4 * j);
         }
     };
     read_a_piece(0, 0);
@@ -929,7 +935,7 @@ __device__ __forceinline__ void load_stage_a(const float *xl, const AStage<C> &A
     for (int m = 0; m < C::MA; ++m)
 #pragma unroll
         for (int c4 = 0; c4 < C::G4; ++c4) {
-            const float *src = xl + A.base[m] + c4 * 4 * C::NWK * C::KKP;
+            const float *src = xl + A.base[m] + c4 * 4 * C::NWK * C::CPL;
 #pragma unroll
             for (int j = 0; j < C::NJ; ++j) {
                 const floatx4 v = *reinterpret_cast<const floatx4 *>(src + 4 * j);
@@ -1597,7 +1603,7 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
     if constexpr (C::WL) {
 #pragma unroll
         for (int m = 0; m < C::MA; ++m)
-            a0.base[m] = C::XSZ + (wc * 16 * C::MA + 16 * m + l16) * C::ROW + (4 * wk + g) * C::KKP;
+            a0.base[m] = C::XSZ + (4 * wk + g) * C::CPL + (wc * 16 * C::MA + 16 * m + l16) * C::KKP;
         a1 = a0;
     }
     const WS ws0(wctx, a.c_out, c_begin * C::CC, lds0);
