@@ -352,6 +352,9 @@ def main():
     ap.add_argument("--peaks", action="store_true", help="also measure the MI355X ceilings")
     ap.add_argument("--copy-calib", type=int, default=0, metavar="MIB",
                     help="also run a plain copy of MIB MiB (counter calibration under rocprofv3)")
+    ap.add_argument("--counter-run", action="store_true",
+                    help="only the workload's spin-up, warm-up, timed and 20 cold calls (for rocprofv3 --pmc runs:"
+                         " the dispatch counts are printed, so counter rows can be matched to the phases)")
     ap.add_argument("--lds-probe", action="store_true",
                     help="only run the LDS bank probe over lds_banks.probe_patterns() (for rocprofv3 --pmc)")
     ap.add_argument("--vgg16-stack", type=int, default=0, metavar="REPS",
@@ -388,6 +391,19 @@ def main():
     if case is None:
         print(f"unknown workload {args.workload}", file=sys.stderr)
         sys.exit(2)
+
+    if args.counter_run:
+        r = bench_case(torch, ilpm, case, args.steps, args.warmup, graph=False)
+        cold = time_cold(torch, ilpm, *(workloads.to_device(torch, t) for t in (r["x"], r["w"], r["b"])),
+                         case.stride, case.pad, r["out"])
+        print(json.dumps({"workload": case.name, "us_per_layer": round(r["us"], 3), "cold_us": round(cold, 3),
+                          "dispatches": {"spinup": r["spin"]["calls"], "warmup": args.warmup, "timed": args.steps,
+                                         "cold_first_uncounted": 1, "cold": 20},
+                          "plan": ilpm.variant_name(r["plan"].path, r["plan"].variant) + f" x{r['plan'].splits}",
+                          "kernel_digest": kernel_source_digest(),
+                          "copy_calib_bytes_each_way": copy_calibration(torch, args.copy_calib) if args.copy_calib
+                          else None}))
+        return
 
     r = bench_case(torch, ilpm, case, args.steps, args.warmup, graph=True)
     us = r["us"]
@@ -429,17 +445,7 @@ def main():
         line["configs"] = config_rows(torch, ilpm, workloads, case.name, failures)
 
     if args.copy_calib:
-        import ctypes
-        plib = ctypes.CDLL(os.path.join(ROOT, "bench_peaks.so"))
-        n = args.copy_calib << 18  # floats
-        src = torch.ones(n, device="cuda")
-        dst = torch.empty(n, device="cuda")
-        st = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
-        for _ in range(3):
-            plib.copy_launch(ctypes.c_void_p(src.data_ptr()), ctypes.c_void_p(dst.data_ptr()),
-                             ctypes.c_size_t(n // 4), 4096, st)
-        torch.cuda.synchronize()
-        line["copy_calib_bytes_each_way"] = 4 * n
+        line["copy_calib_bytes_each_way"] = copy_calibration(torch, args.copy_calib)
 
     if args.peaks:
         line["measured_peaks"] = measure_peaks(torch)
@@ -475,6 +481,23 @@ def main():
 
 CONFIG_ROWS = ["tiny_3to16_32x32", "resnet_conv4_256to256_14x14", "resnet_strided_128to256_28x28_s2",
                "deep_1x1_512to512_7x7", "deep_5x5_512to512_7x7"]
+
+
+def copy_calibration(torch, mib):
+    """Three plain copies of `mib` MiB (16-byte loads and stores): under
+    rocprofv3 --pmc their FETCH_SIZE / WRITE_SIZE give the counters' scale
+    for a known number of bytes.  Returns the bytes moved each way per copy."""
+    import ctypes
+    plib = ctypes.CDLL(os.path.join(ROOT, "bench_peaks.so"))
+    n = mib << 18  # floats
+    src = torch.ones(n, device="cuda")
+    dst = torch.empty(n, device="cuda")
+    st = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    for _ in range(3):
+        plib.copy_launch(ctypes.c_void_p(src.data_ptr()), ctypes.c_void_p(dst.data_ptr()),
+                         ctypes.c_size_t(n // 4), 4096, st)
+    torch.cuda.synchronize()
+    return 4 * n
 
 
 def config_rows(torch, ilpm, workloads, headline, failures, steps=500, warmup=200):
