@@ -15,6 +15,7 @@ int variants_part4(const Variant **table)
     make_variant<Cfg<3, 1, 8, 8, 1, 1, 4, 1, 16, 3, 8, true>>("k3s1_t8x8_co16_k4_cc16_s8_wl"),
     make_variant<Cfg<3, 1, 7, 7, 4, 1, 1, 1, 4, 3, 4>>("k3s1_t7x7_co64_cc4_s4"),
     make_variant<Cfg<3, 1, 7, 7, 4, 1, 1, 1, 4, 3, 8>>("k3s1_t7x7_co64_cc4_s8"),
+    make_variant<Cfg<3, 1, 7, 7, 2, 1, 2, 1, 16, 3, 8>>("k3s1_t7x7_co32_k2_s8"),
     };
     *table = t;
     return (int)(sizeof(t) / sizeof(t[0]));

@@ -15,6 +15,7 @@ int variants_part5(const Variant **table)
     make_variant<Cfg<3, 2, 4, 4, 1, 1, 4, 1, 64>>("k3s2_t4x4_co16_k4"),
     make_variant<Cfg<3, 2, 4, 4, 1, 1, 4, 1, 16, 3, 8, true>>("k3s2_t4x4_co16_k4_cc16_s8_wl"),
     make_variant<Cfg<1, 1, 7, 7, 4, 1, 1, 1, 16>>("k1s1_t7x7_co64"),
+    make_variant<Cfg<3, 1, 7, 7, 1, 1, 4, 1, 16, 3, 4, true>>("k3s1_t7x7_co16_k4_s4_wl"),
     };
     *table = t;
     return (int)(sizeof(t) / sizeof(t[0]));

@@ -16,8 +16,6 @@ int variants_part6(const Variant **table)
     make_variant<Cfg<5, 1, 7, 7, 4, 1, 1, 1, 8>>("k5s1_t7x7_co64_cc8"),
     make_variant<Cfg<5, 1, 7, 7, 4, 1, 2, 1, 8>>("k5s1_t7x7_co64_k2"),
     make_variant<Cfg<3, 1, 7, 7, 2, 1, 2, 1, 16>>("k3s1_t7x7_co32_k2"),
-    make_variant<Cfg<3, 1, 7, 7, 1, 1, 4, 2, 16>>("k3s1_t7x7_co32_ma2_k4"),
-    make_variant<Cfg<3, 1, 7, 7, 2, 1, 2, 1, 16, 2, 0, true>>("k3s1_t7x7_co32_k2_wl"),
     };
     *table = t;
     return (int)(sizeof(t) / sizeof(t[0]));

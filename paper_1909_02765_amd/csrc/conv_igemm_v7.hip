@@ -13,7 +13,6 @@ int variants_part7(const Variant **table)
     make_variant<Cfg<5, 1, 4, 4, 1, 1, 4, 1, 16, 3, 8, true>>("k5s1_t4x4_co16_k4_cc16_s8_wl"),
     make_variant<Cfg<5, 1, 8, 8, 1, 1, 4, 1, 16, 3, 4, true>>("k5s1_t8x8_co16_k4_cc16_s4_wl"),
     make_variant<Cfg<5, 1, 4, 4, 1, 1, 4, 1, 16, 3, 16, true>>("k5s1_t4x4_co16_k4_cc16_s16_wl"),
-    make_variant<Cfg<3, 1, 7, 7, 2, 1, 2, 2, 16>>("k3s1_t7x7_co64_ma2_k2"),
     make_variant<Cfg<3, 1, 14, 14, 1, 1, 4, 1, 16>>("k3s1_t14x14_co16_k4"),
     make_variant<Cfg<3, 1, 7, 7, 1, 1, 4, 1, 16>>("k3s1_t7x7_co16_k4"),
     };
