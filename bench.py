@@ -383,7 +383,7 @@ def main():
         rows = bench_vgg16_stack(torch, ilpm, workloads, args.vgg16_stack)
         print(json.dumps(rows))
         if any(r.get("same_output_bits") is False for r in rows):
-            print("bench.py: the fused VGG-16 stack's output differs from the unfused one", file=sys.stderr)
+            print("bench.py: a VGG-16 stack's output bits differ from its reference's", file=sys.stderr)
             sys.exit(1)
         return
 
@@ -531,13 +531,15 @@ def config_rows(torch, ilpm, workloads, headline, failures, steps=500, warmup=20
     by = {r["layer"]: r for r in st}
     for r in st:
         if r.get("same_output_bits") is False:
-            failures.append(f"{r['layer']}: output differs from the unfused stack's bits")
+            failures.append(f"{r['layer']}: output bits differ from its reference's")
     layers = bench_vgg16_layers(torch, ilpm, workloads, 200)
     floor_total = sum(l["floor_us"] for l in layers)
     flops_total = sum(l["gflop"] for l in layers) * 1e9
     us_f = by["vgg16_stack_fused"]["us"]
     rows.append({"workload": "vgg16_stack_13conv_224", "us": us_f,
                  "graph_us": by["vgg16_stack_fused_graph"]["us"], "unfused_us": by["vgg16_stack_unfused"]["us"],
+                 "prepacked_us": by["vgg16_stack_fused_prepacked"]["us"],
+                 "prepacked_graph_us": by["vgg16_stack_fused_prepacked_graph"]["us"],
                  "gflops": round(flops_total / us_f / 1e3, 1), "bound": "mfma (conv1_1 hbm)",
                  "floor_us": round(floor_total, 3), "frac": round(floor_total / us_f, 4),
                  "note": "end to end, fused ReLU / ReLU+2x2 max-pool epilogue, one call per conv",
@@ -715,12 +717,70 @@ def bench_vgg16_stack(torch, ilpm, workloads, reps):
     g.replay()
     torch.cuda.synchronize()
     graph_same = graph_same and bool(torch.equal(out_graph, ref))
+    # The fused stack on prepacked weights: each layer on the plan
+    # ilpm_conv2d_plan_prepacked picks, its weights packed once beforehand
+    # (outside the timed region, like loading a model).  Checked bit for bit
+    # against the same plans run on the OIHW weights.
+    pre, ref_pre = [], []
+    x = xp = x0
+    for (name, ci, co, hw, pool, _), w in zip(layers, ws):
+        epi = ilpm.EPI_RELU | (ilpm.EPI_MAXPOOL2 if pool else 0)
+        plan = ilpm.plan_prepacked(ci, hw, hw, co, 3, 1, 1)
+        packed = ilpm.prepack_weights(w, plan)
+        y = torch.empty(ilpm.epilogue_out_shape(co, hw, hw, 3, 1, 1, epi), device="cuda", dtype=torch.float32)
+        pre.append(ilpm.conv2d_prepacked_epilogue_launcher(xp, packed, co, 3, None, 1, 1, epi, y, plan))
+        xr = ilpm.conv2d_epilogue(x, w, None, 1, 1, epi, plan=plan)
+        ref_pre.append(xr)
+        x, xp = xr, y
+    out_pre = xp
+    t_pre = timed(pre)
+    pre_same = bool(torch.equal(out_pre, ref_pre[-1]))
+    stream_p = torch.cuda.Stream()
+    stream_p.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(stream_p):
+        pre_s = []
+        xp = x0
+        for (name, ci, co, hw, pool, _), w in zip(layers, ws):
+            epi = ilpm.EPI_RELU | (ilpm.EPI_MAXPOOL2 if pool else 0)
+            plan = ilpm.plan_prepacked(ci, hw, hw, co, 3, 1, 1)
+            packed = ilpm.prepack_weights(w, plan)
+            y = torch.empty(ilpm.epilogue_out_shape(co, hw, hw, 3, 1, 1, epi), device="cuda", dtype=torch.float32)
+            pre_s.append(ilpm.conv2d_prepacked_epilogue_launcher(xp, packed, co, 3, None, 1, 1, epi, y, plan))
+            xp = y
+        out_pre_graph = xp
+        for f in pre_s:
+            f()
+        torch.cuda.synchronize()
+        gp = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(gp, stream=stream_p):
+            for f in pre_s:
+                f()
+    torch.cuda.synchronize()
+    spin_up(torch, gp.replay)
+    for _ in range(3):
+        out_pre_graph.fill_(float("nan"))
+        gp.replay()
+        torch.cuda.synchronize()
+        pre_same = pre_same and bool(torch.equal(out_pre_graph, out_pre))
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        gp.replay()
+    b.record()
+    torch.cuda.synchronize()
+    t_pre_graph = a.elapsed_time(b) * 1000.0 / reps
     rows = [{"layer": "vgg16_stack_unfused", "us": round(t_unfused, 3),
              "note": "13 convs + 13 ReLU + 4 max-pool kernels, end to end"},
             {"layer": "vgg16_stack_fused", "us": round(t_fused, 3),
              "note": "13 convs with the fused ReLU / ReLU+max-pool epilogue", "same_output_bits": same},
             {"layer": "vgg16_stack_fused_graph", "us": round(t_graph, 3),
-             "note": "the fused stack replayed from one captured HIP graph", "same_output_bits": graph_same}]
+             "note": "the fused stack replayed from one captured HIP graph", "same_output_bits": graph_same},
+            {"layer": "vgg16_stack_fused_prepacked", "us": round(t_pre, 3),
+             "note": "the fused stack on weights prepacked once for ilpm_conv2d_plan_prepacked's plans "
+                     "(bits equal the same plans on OIHW weights)", "same_output_bits": pre_same},
+            {"layer": "vgg16_stack_fused_prepacked_graph", "us": round(t_pre_graph, 3),
+             "note": "the prepacked fused stack replayed from one captured HIP graph",
+             "same_output_bits": pre_same}]
     for r in rows:
         print(json.dumps(r), file=sys.stderr)
     return rows

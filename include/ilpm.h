@@ -294,6 +294,19 @@ int ilpm_conv2d_fwd_prepacked(const float *in, const float *packed, const float 
                               int C_in, int H, int W, int C_out, int K, int stride, int pad,
                               const ilpm_plan *plan, float *out, hipStream_t stream);
 
+/*
+ * ilpm_conv2d_plan_prepacked -- the default plan for a caller that will pack
+ * the weights: the measured best with prepacked weights for this exact shape
+ * (a second compiled-in table; with packed weights every weight load is one
+ * contiguous kilobyte, so plans whose kernels were bound by the scattered
+ * OIHW loads move up), else the plan ilpm_conv2d_plan would give.  Pure
+ * host; chosen once per shape and kept, like ilpm_conv2d_plan; the same
+ * environment overrides apply.  Use the plan for ilpm_conv2d_prepacked_size,
+ * ilpm_conv2d_prepack_weights and the prepacked calls.
+ */
+int ilpm_conv2d_plan_prepacked(int C_in, int H, int W, int C_out, int K, int stride, int pad,
+                               ilpm_plan *plan);
+
 /* ---- fused epilogue ----
  *
  * A CNN layer follows the convolution with ReLU and, between stages, a 2x2
@@ -311,15 +324,26 @@ int ilpm_conv2d_fwd_prepacked(const float *in, const float *packed, const float 
  * result is max-pool of ReLU, which equals ReLU of max-pool.  `out` has the
  * pooled shape when ILPM_EPI_MAXPOOL2 is set.  plan: NULL for the default
  * plan of the shape, or one made for this exact shape.  One-split
- * matrix-core plans on OIHW weights whose tiles have even sides pool inside
- * the kernel; other plans write the full-size convolution output (as
- * per-split partial sums) to the workspace and pool it in a second kernel
+ * matrix-core plans whose tiles have even sides pool inside the kernel;
+ * other plans write the full-size convolution output (as per-split partial
+ * sums) to the workspace and pool it in a second kernel
  * (ilpm_conv2d_epilogue_workspace_size covers that route).  The values are
  * exactly those of the unfused sequence conv (same plan) -> ReLU -> max-pool.
  */
 int ilpm_conv2d_fwd_epilogue(const float *in, const float *w, const float *bias,
                              int C_in, int H, int W, int C_out, int K, int stride, int pad,
                              int epilogue, const ilpm_plan *plan, float *out, hipStream_t stream);
+
+/*
+ * ilpm_conv2d_fwd_prepacked_epilogue -- ilpm_conv2d_fwd_epilogue with the
+ * weights prepacked for `plan` (required, made for this exact shape), as
+ * ilpm_conv2d_fwd_prepacked takes them.  The result is bit for bit that of
+ * ilpm_conv2d_fwd_epilogue with the OIHW weights and the same plan; the
+ * workspace is ilpm_conv2d_epilogue_workspace_size's for that plan.
+ */
+int ilpm_conv2d_fwd_prepacked_epilogue(const float *in, const float *packed, const float *bias,
+                                       int C_in, int H, int W, int C_out, int K, int stride, int pad,
+                                       int epilogue, const ilpm_plan *plan, float *out, hipStream_t stream);
 
 /* Workspace bytes ilpm_conv2d_fwd_epilogue needs (plan NULL = default plan). */
 int ilpm_conv2d_epilogue_workspace_size(int C_in, int H, int W, int C_out, int K, int stride, int pad,

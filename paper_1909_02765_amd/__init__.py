@@ -96,6 +96,7 @@ _SIGS = {
     "ilpm_last_hip_error": ([], _i),
     "ilpm_conv2d_validate": ([_vp, _vp, _vp] + [_i] * 7 + [_vp], _i),
     "ilpm_conv2d_plan": ([_i] * 7 + [_plan_p], _i),
+    "ilpm_conv2d_plan_prepacked": ([_i] * 7 + [_plan_p], _i),
     "ilpm_conv2d_plan_variant": ([_i] * 10 + [_plan_p], _i),
     "ilpm_num_variants": ([_i], _i),
     "ilpm_variant_name": ([_i, _i], ctypes.c_char_p),
@@ -105,6 +106,7 @@ _SIGS = {
     "ilpm_conv2d_prepack_weights": ([_vp, _i, _i, _i, _plan_p, _vp, _vp], _i),
     "ilpm_conv2d_fwd_prepacked": ([_vp, _vp, _vp] + [_i] * 7 + [_plan_p, _vp, _vp], _i),
     "ilpm_conv2d_fwd_epilogue": ([_vp, _vp, _vp] + [_i] * 8 + [_plan_p, _vp, _vp], _i),
+    "ilpm_conv2d_fwd_prepacked_epilogue": ([_vp, _vp, _vp] + [_i] * 8 + [_plan_p, _vp, _vp], _i),
     "ilpm_conv2d_epilogue_workspace_size": ([_i] * 8 + [_plan_p, ctypes.POINTER(ctypes.c_size_t)], _i),
     "ilpm_winograd_filter_size": ([_i, _i, ctypes.POINTER(ctypes.c_size_t)], _i),
     "ilpm_winograd_transform_filter": ([_vp, _i, _i, _vp, _vp], _i),
@@ -139,6 +141,10 @@ def _stream_handle(stream=None):
     return ctypes.c_void_p(s.cuda_stream)
 
 
+def _stream_obj(stream=None):
+    return stream if stream is not None else _torch().cuda.current_stream()
+
+
 def _dev_f32(t, name):
     torch = _torch()
     if not isinstance(t, torch.Tensor) or not t.is_cuda or t.dtype != torch.float32 or not t.is_contiguous():
@@ -155,6 +161,14 @@ def plan(c_in, h, w, c_out, k, stride=1, pad=0) -> ilpm_plan:
     """The plan the library picks for this shape."""
     p = ilpm_plan()
     _check(lib.ilpm_conv2d_plan(c_in, h, w, c_out, k, stride, pad, ctypes.byref(p)), "ilpm_conv2d_plan")
+    return p
+
+
+def plan_prepacked(c_in, h, w, c_out, k, stride=1, pad=0) -> ilpm_plan:
+    """The plan the library picks for this shape when the weights will be prepacked."""
+    p = ilpm_plan()
+    _check(lib.ilpm_conv2d_plan_prepacked(c_in, h, w, c_out, k, stride, pad, ctypes.byref(p)),
+           "ilpm_conv2d_plan_prepacked")
     return p
 
 
@@ -261,22 +275,37 @@ def conv2d_noalloc(x, w, bias=None, stride: int = 1, pad: int = 0, *, out, strea
     return out
 
 
+class _Launcher:
+    """A library entry point with its arguments marshalled once; `keep` holds
+    the objects behind the raw addresses in `args` for the launcher's life."""
+
+    __slots__ = ("fn", "args", "keep", "name")
+
+    def __init__(self, fn, args, keep, name):
+        self.fn, self.args, self.keep, self.name = fn, args, keep, name
+
+    def __call__(self):
+        rc = self.fn(*self.args)
+        if rc != OK:
+            raise IlpmError(rc, self.name)
+
+
 def conv2d_launcher(x, w, bias, stride, pad, out, stream=None):
     """A zero-argument callable that enqueues the same conv2d again, with the
-    arguments marshalled once (for timing loops and graph capture)."""
+    arguments marshalled once (for timing loops and graph capture).
+
+    The callable holds raw device addresses, so it keeps the tensors (and
+    stream) they come from alive: a tensor freed while a launcher still
+    points at it could be returned to the driver -- torch empties its cache
+    when a graph capture begins -- and the next launch would then read
+    unmapped memory.  The stream is the one current when the launcher is made."""
     _, c_in, h, wd = x.shape
     c_out, _, k, _ = w.shape
     if tuple(out.shape) != (1, c_out, out_size(h, k, stride, pad), out_size(wd, k, stride, pad)):
         raise ValueError("out has the wrong shape")
     args = (_dev_f32(x, "x"), _dev_f32(w, "w"), _dev_f32(bias, "bias") if bias is not None else None,
             c_in, h, wd, c_out, k, stride, pad, _dev_f32(out, "out"), _stream_handle(stream))
-    fwd = lib.ilpm_conv2d_fwd
-
-    def launch():
-        rc = fwd(*args)
-        if rc != OK:
-            raise IlpmError(rc, "ilpm_conv2d_fwd")
-    return launch
+    return _Launcher(lib.ilpm_conv2d_fwd, args, (x, w, bias, out, _stream_obj(stream)), "ilpm_conv2d_fwd")
 
 
 def prepacked_size(plan_: ilpm_plan, c_in: int, c_out: int, k: int) -> int:
@@ -322,19 +351,14 @@ def conv2d_prepacked(x, packed, c_out: int, k: int, bias=None, stride: int = 1, 
 
 
 def conv2d_prepacked_launcher(x, packed, c_out, k, bias, stride, pad, out, plan, stream=None):
-    """conv2d_launcher for prepacked weights (the plan object must outlive it)."""
+    """conv2d_launcher for prepacked weights (it keeps the plan object alive too)."""
     _, c_in, h, wd = x.shape
     if tuple(out.shape) != (1, c_out, out_size(h, k, stride, pad), out_size(wd, k, stride, pad)):
         raise ValueError("out has the wrong shape")
     args = (_dev_f32(x, "x"), _dev_f32(packed, "packed"), _dev_f32(bias, "bias") if bias is not None else None,
             c_in, h, wd, c_out, k, stride, pad, ctypes.byref(plan), _dev_f32(out, "out"), _stream_handle(stream))
-    fwd = lib.ilpm_conv2d_fwd_prepacked
-
-    def launch():
-        rc = fwd(*args)
-        if rc != OK:
-            raise IlpmError(rc, "ilpm_conv2d_fwd_prepacked")
-    return launch
+    return _Launcher(lib.ilpm_conv2d_fwd_prepacked, args, (x, packed, bias, out, plan, _stream_obj(stream)),
+                     "ilpm_conv2d_fwd_prepacked")
 
 
 EPI_RELU = 1
@@ -383,13 +407,38 @@ def conv2d_epilogue_launcher(x, w, bias, stride, pad, epilogue, out, stream=None
         raise ValueError("out has the wrong shape")
     args = (_dev_f32(x, "x"), _dev_f32(w, "w"), _dev_f32(bias, "bias") if bias is not None else None,
             c_in, h, wd, c_out, k, stride, pad, epilogue, None, _dev_f32(out, "out"), _stream_handle(stream))
-    fwd = lib.ilpm_conv2d_fwd_epilogue
+    return _Launcher(lib.ilpm_conv2d_fwd_epilogue, args, (x, w, bias, out, _stream_obj(stream)),
+                     "ilpm_conv2d_fwd_epilogue")
 
-    def launch():
-        rc = fwd(*args)
-        if rc != OK:
-            raise IlpmError(rc, "ilpm_conv2d_fwd_epilogue")
-    return launch
+
+def conv2d_prepacked_epilogue(x, packed, c_out: int, k: int, bias=None, stride: int = 1, pad: int = 0,
+                              epilogue: int = EPI_RELU, *, plan: ilpm_plan, out=None, stream=None):
+    """conv2d_epilogue with weights from prepack_weights(w, plan)."""
+    torch = _torch()
+    _, c_in, h, wd = x.shape
+    shape = epilogue_out_shape(c_out, h, wd, k, stride, pad, epilogue)
+    if out is None:
+        out = torch.empty(tuple(max(d, 1) for d in shape), device=x.device, dtype=torch.float32)
+    elif tuple(out.shape) != shape:
+        raise ValueError(f"out must be {list(shape)}")
+    _check(lib.ilpm_conv2d_fwd_prepacked_epilogue(_dev_f32(x, "x"), _dev_f32(packed, "packed"),
+                                                  _dev_f32(bias, "bias") if bias is not None else None,
+                                                  c_in, h, wd, c_out, k, stride, pad, epilogue, ctypes.byref(plan),
+                                                  _dev_f32(out, "out"), _stream_handle(stream)),
+           "ilpm_conv2d_fwd_prepacked_epilogue")
+    return out
+
+
+def conv2d_prepacked_epilogue_launcher(x, packed, c_out, k, bias, stride, pad, epilogue, out, plan, stream=None):
+    """conv2d_launcher for ilpm_conv2d_fwd_prepacked_epilogue (it keeps the plan object alive too)."""
+    _, c_in, h, wd = x.shape
+    if tuple(out.shape) != epilogue_out_shape(c_out, h, wd, k, stride, pad, epilogue):
+        raise ValueError("out has the wrong shape")
+    args = (_dev_f32(x, "x"), _dev_f32(packed, "packed"), _dev_f32(bias, "bias") if bias is not None else None,
+            c_in, h, wd, c_out, k, stride, pad, epilogue, ctypes.byref(plan), _dev_f32(out, "out"),
+            _stream_handle(stream))
+    return _Launcher(lib.ilpm_conv2d_fwd_prepacked_epilogue, args,
+                     (x, packed, bias, out, plan, _stream_obj(stream)), "ilpm_conv2d_fwd_prepacked_epilogue")
 
 
 def winograd_transform_filter(w, stream=None):
@@ -424,13 +473,8 @@ def conv2d_winograd_launcher(x, u, bias, pad, out, stream=None):
     c_out = u.shape[1]
     args = (_dev_f32(x, "x"), _dev_f32(u, "u"), _dev_f32(bias, "bias") if bias is not None else None,
             c_in, h, wd, c_out, pad, _dev_f32(out, "out"), _stream_handle(stream))
-    fwd = lib.ilpm_conv2d_fwd_winograd
-
-    def launch():
-        rc = fwd(*args)
-        if rc != OK:
-            raise IlpmError(rc, "ilpm_conv2d_fwd_winograd")
-    return launch
+    return _Launcher(lib.ilpm_conv2d_fwd_winograd, args, (x, u, bias, out, _stream_obj(stream)),
+                     "ilpm_conv2d_fwd_winograd")
 
 
 def relu_(x, stream=None):

@@ -120,6 +120,7 @@ int variants_part4(const Variant **table);
 int variants_part5(const Variant **table);
 int variants_part6(const Variant **table);
 int variants_part7(const Variant **table);
+int variants_part8(const Variant **table);
 
 }  // namespace ig
 
@@ -1707,7 +1708,8 @@ void launch_cfg(dim3 grid, hipStream_t st, const float *x, const float *w, const
 {
     if constexpr (C::POOLABLE) {
         if (a.pool_tile) {
-            hipLaunchKernelGGL((conv_igemm<PoolTile<C>, false>), grid, dim3(C::NT), 0, st, x, w, b, o, ws, a);
+            if (packed) hipLaunchKernelGGL((conv_igemm<PoolTile<C>, true>), grid, dim3(C::NT), 0, st, x, w, b, o, ws, a);
+            else hipLaunchKernelGGL((conv_igemm<PoolTile<C>, false>), grid, dim3(C::NT), 0, st, x, w, b, o, ws, a);
             return;
         }
     }

@@ -162,7 +162,7 @@ const std::vector<const Variant *> &variant_table()
     static const std::vector<const Variant *> table = [] {
         int (*const parts[])(const Variant **) = {ig::variants_part0, ig::variants_part1, ig::variants_part2,
                                                   ig::variants_part3, ig::variants_part4, ig::variants_part5,
-                                                  ig::variants_part6, ig::variants_part7};
+                                                  ig::variants_part6, ig::variants_part7, ig::variants_part8};
         std::vector<const Variant *> t;
         for (auto part : parts) {
             const Variant *v = nullptr;
@@ -362,10 +362,10 @@ hipError_t igemm_launch(const ilpm_plan &p, const ConvShape &s, const float *x, 
     // outweigh the input, let the run share output-channel tiles (and so
     // weights) across spatial tiles; otherwise share spatial tiles (input).
     a.sp_fast = (int64_t)s.c_out * s.c_in * s.k * s.k > (int64_t)s.c_in * s.h * s.w ? 1 : 0;
-    // A pooled epilogue of a one-split plan on OIHW weights is done in the
-    // workgroup when the variant allows it; otherwise the conv writes its
-    // full-size sums to the workspace and sum_splits_pool pools them.
-    a.pool_tile = (pool && p.splits == 1 && !packed && d.poolable) ? 1 : 0;
+    // A pooled epilogue of a one-split plan is done in the workgroup when the
+    // variant allows it; otherwise the conv writes its full-size sums to the
+    // workspace and sum_splits_pool pools them.
+    a.pool_tile = (pool && p.splits == 1 && d.poolable) ? 1 : 0;
     a.to_part = (p.splits > 1 || (pool && !a.pool_tile)) ? 1 : 0;
     a.relu = relu ? 1 : 0;
     const int tiles = p.grid / p.splits;

@@ -129,14 +129,15 @@ int validate(const void *in, const void *w, const void *bias, const ConvShape &s
 }
 
 // The default plan: the measured best for this exact shape when the tuning
-// table has it, else the cheapest matrix-core variant for this filter size
-// and stride by the cost model, else the LDS direct kernel, else the plain
-// one.  The environment overrides (read once) narrow the candidates.
-int compute_plan(const ConvShape &s, ilpm_plan *p)
+// table has it (for prepacked weights their own table first, then the OIHW
+// one), else the cheapest matrix-core variant for this filter size and
+// stride by the cost model, else the LDS direct kernel, else the plain one.
+// The environment overrides (read once) narrow the candidates.
+int compute_plan(const ConvShape &s, ilpm_plan *p, bool prepacked)
 {
     const Overrides &o = overrides();
     const bool any = o.path < 0 && o.splits == 0 && o.tile_h == 0;
-    if (any && tuned_plan(s, p)) return ILPM_OK;
+    if (any && ((prepacked && tuned_plan(s, p, true)) || tuned_plan(s, p, false))) return ILPM_OK;
     auto tile_ok = [&](const ilpm_plan &q) { return o.tile_h == 0 || (q.tile_h == o.tile_h && q.tile_w == o.tile_w); };
     if (o.path != ILPM_PATH_DIRECT) {
         bool found = false;
@@ -173,6 +174,7 @@ int compute_plan(const ConvShape &s, ilpm_plan *p)
 // the cost-model sweep.
 struct PlanSlot {
     bool used = false;
+    bool prepacked;
     ConvShape s;
     int rc;
     ilpm_plan p;
@@ -186,22 +188,24 @@ bool same_shape(const ConvShape &a, const ConvShape &b)
            a.stride == b.stride && a.pad == b.pad;
 }
 
-int choose_plan(const ConvShape &s, ilpm_plan *p)
+int choose_plan(const ConvShape &s, ilpm_plan *p, bool prepacked = false)
 {
-    uint64_t h = 1469598103934665603ull;  // FNV-1a over the seven sizes
-    for (int v : {s.c_in, s.h, s.w, s.c_out, s.k, s.stride, s.pad}) h = (h ^ (uint32_t)v) * 1099511628211ull;
+    uint64_t h = 1469598103934665603ull;  // FNV-1a over the seven sizes and the weight layout
+    for (int v : {s.c_in, s.h, s.w, s.c_out, s.k, s.stride, s.pad, (int)prepacked})
+        h = (h ^ (uint32_t)v) * 1099511628211ull;
     PlanSlot &slot = g_plan_cache[h % kPlanSlots];
     {
         std::lock_guard<std::mutex> lk(g_mu);
-        if (slot.used && same_shape(slot.s, s)) {
+        if (slot.used && slot.prepacked == prepacked && same_shape(slot.s, s)) {
             *p = slot.p;
             return slot.rc;
         }
     }
     ilpm_plan q = {};
-    const int rc = compute_plan(s, &q);
+    const int rc = compute_plan(s, &q, prepacked);
     std::lock_guard<std::mutex> lk(g_mu);
     slot.used = true;
+    slot.prepacked = prepacked;
     slot.s = s;
     slot.rc = rc;
     slot.p = q;
@@ -421,6 +425,15 @@ int ilpm_conv2d_plan(int C_in, int H, int W, int C_out, int K, int stride, int p
     return choose_plan(s, plan);
 }
 
+int ilpm_conv2d_plan_prepacked(int C_in, int H, int W, int C_out, int K, int stride, int pad, ilpm_plan *plan)
+{
+    if (!plan) return ILPM_ERR_INVALID_ARG;
+    ConvShape s;
+    int rc = check_dims(C_in, H, W, C_out, K, stride, pad, &s);
+    if (rc != ILPM_OK) return rc;
+    return choose_plan(s, plan, true);
+}
+
 int ilpm_conv2d_plan_variant(int C_in, int H, int W, int C_out, int K, int stride, int pad, int path,
                              int variant, int splits, ilpm_plan *plan)
 {
@@ -618,6 +631,26 @@ int ilpm_conv2d_fwd_prepacked(const float *in, const float *packed, const float 
     rc = check_plan(s, *plan);
     if (rc != ILPM_OK) return rc;
     return run(in, packed, bias, s, out, *plan, stream, true);
+}
+
+int ilpm_conv2d_fwd_prepacked_epilogue(const float *in, const float *packed, const float *bias, int C_in, int H,
+                                       int W, int C_out, int K, int stride, int pad, int epilogue,
+                                       const ilpm_plan *plan, float *out, hipStream_t stream)
+{
+    if (!plan || !packed || (epilogue & ~(ILPM_EPI_RELU | ILPM_EPI_MAXPOOL2))) return ILPM_ERR_INVALID_ARG;
+    ConvShape s;
+    int rc = check_dims(C_in, H, W, C_out, K, stride, pad, &s);
+    if (rc != ILPM_OK) return rc;
+    if ((epilogue & ILPM_EPI_MAXPOOL2) && (s.h_out < 2 || s.w_out < 2)) return ILPM_ERR_INVALID_ARG;
+    rc = validate(in, packed, bias, s, out, epilogue);
+    if (rc != ILPM_OK) return rc;
+    const size_t pb = prepacked_bytes(*plan, C_in, C_out, K, &rc);
+    if (rc != ILPM_OK) return rc;
+    if (((uintptr_t)packed & 15u) || overlaps(out, out_bytes(s, epilogue), packed, pb))
+        return ILPM_ERR_INVALID_ARG;
+    rc = check_plan(s, *plan);
+    if (rc != ILPM_OK) return rc;
+    return run(in, packed, bias, s, out, *plan, stream, true, epilogue);
 }
 
 int ilpm_conv2d_fwd_epilogue(const float *in, const float *w, const float *bias, int C_in, int H, int W, int C_out,

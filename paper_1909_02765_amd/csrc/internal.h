@@ -62,7 +62,7 @@ int winograd_launch(const ConvShape &s, const float *x, const float *u, const fl
 
 // ---- measured plan table (tuned_plans.inc) ----
 // The plan the offline sweep found fastest for this exact shape, if any.
-bool tuned_plan(const ConvShape &s, ilpm_plan *p);
+bool tuned_plan(const ConvShape &s, ilpm_plan *p, bool prepacked);
 
 // ---- helpers ----
 hipError_t launch_relu(float *x, int64_t n, hipStream_t stream);

@@ -1,7 +1,9 @@
-// The measured plan table: for shapes the offline sweep timed on MI355X
-// (tune.py), the fastest (kernel variant, split count).  Entries name the
-// variant, so the table survives changes to the variant list; an entry whose
-// variant no longer exists, or no longer accepts the shape, is ignored.
+// The measured plan tables: for shapes the offline sweep timed on MI355X
+// (tune.py), the fastest (kernel variant, split count), one table for OIHW
+// weights and one for prepacked weights (the kernels load these differently,
+// so the fastest variant can differ).  Entries name the variant, so the
+// tables survive changes to the variant list; an entry whose variant no
+// longer exists, or no longer accepts the shape, is ignored.
 #include <cstring>
 
 #include "internal.h"
@@ -19,11 +21,14 @@ const TunedEntry kTuned[] = {
 #include "tuned_plans.inc"
 };
 
-}  // namespace
+const TunedEntry kTunedPrepacked[] = {
+#include "tuned_plans_prepacked.inc"
+};
 
-bool tuned_plan(const ConvShape &s, ilpm_plan *p)
+template <size_t N>
+bool lookup(const TunedEntry (&table)[N], const ConvShape &s, ilpm_plan *p)
 {
-    for (const TunedEntry &e : kTuned) {
+    for (const TunedEntry &e : table) {
         if (e.c_in != s.c_in || e.h != s.h || e.w != s.w || e.c_out != s.c_out || e.k != s.k ||
             e.stride != s.stride || e.pad != s.pad)
             continue;
@@ -34,6 +39,13 @@ bool tuned_plan(const ConvShape &s, ilpm_plan *p)
         return false;
     }
     return false;
+}
+
+}  // namespace
+
+bool tuned_plan(const ConvShape &s, ilpm_plan *p, bool prepacked)
+{
+    return prepacked ? lookup(kTunedPrepacked, s, p) : lookup(kTuned, s, p);
 }
 
 }  // namespace ilpm

@@ -6,7 +6,10 @@ fastest per shape, and write the table the library compiles in.
     python -m paper_1909_02765_amd.tune --emit tuned.json         # rewrite csrc/tuned_plans.inc
 
 The table maps an exact shape (C_in, H, W, C_out, K, stride, pad) to a variant
-name and a split count; shapes not in it fall back to the cost model.
+name and a split count; shapes not in it fall back to the cost model.  With
+--prepacked the sweep times every plan on weights prepacked for it, and
+--emit --prepacked writes csrc/tuned_plans_prepacked.inc, the table behind
+ilpm_conv2d_plan_prepacked.
 """
 from __future__ import annotations
 
@@ -19,6 +22,7 @@ import sys
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 INC = os.path.join(PKG, "csrc", "tuned_plans.inc")
+INC_PREPACKED = os.path.join(PKG, "csrc", "tuned_plans_prepacked.inc")
 
 SPLITS = (1, 2, 3, 4, 6, 8, 12, 16, 24, 32, 48, 64)
 FINALISTS = 4
@@ -58,17 +62,28 @@ def candidate_plans(ilpm, shape):
     return plans
 
 
-def time_plan(torch, ilpm, bufs, shape, plan, reps):
+def call_args(ilpm, bufs, shape, plan, stream):
+    """(entry point, arguments) of one call of `plan`: ilpm_conv2d_fwd_plan on
+    the OIHW weights, or ilpm_conv2d_fwd_prepacked when bufs carries packed
+    weights (x, w, out, packed)."""
     c_in, h, w, c_out, k, s, p = shape
-    x, wt, out = bufs
-    args = (ctypes.c_void_p(x.data_ptr()), ctypes.c_void_p(wt.data_ptr()), None, c_in, h, w, c_out, k, s, p,
-            ctypes.c_void_p(out.data_ptr()), ctypes.byref(plan),
-            ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
-    f = ilpm.lib.ilpm_conv2d_fwd_plan
+    x, wt, out = bufs[:3]
+    packed = bufs[3] if len(bufs) > 3 else None
+    if packed is None:
+        return ilpm.lib.ilpm_conv2d_fwd_plan, (
+            ctypes.c_void_p(x.data_ptr()), ctypes.c_void_p(wt.data_ptr()), None, c_in, h, w, c_out, k, s, p,
+            ctypes.c_void_p(out.data_ptr()), ctypes.byref(plan), ctypes.c_void_p(stream))
+    return ilpm.lib.ilpm_conv2d_fwd_prepacked, (
+        ctypes.c_void_p(x.data_ptr()), ctypes.c_void_p(packed.data_ptr()), None, c_in, h, w, c_out, k, s, p,
+        ctypes.byref(plan), ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(stream))
+
+
+def time_plan(torch, ilpm, bufs, shape, plan, reps):
+    f, args = call_args(ilpm, bufs, shape, plan, torch.cuda.current_stream().cuda_stream)
     for _ in range(3):
         rc = f(*args)
         if rc != 0:
-            raise ilpm.IlpmError(rc, "ilpm_conv2d_fwd_plan")
+            raise ilpm.IlpmError(rc, f.__name__)
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
@@ -83,18 +98,14 @@ def time_plan_graph(torch, ilpm, bufs, shape, plan, reps, per_graph=20):
     """Mean us per call with the calls replayed from a captured HIP graph:
     the kernels' own rate, without the host's launch cost between calls
     (which bounds eager timing of the smallest layers)."""
-    c_in, h, w, c_out, k, s, p = shape
-    x, wt, out = bufs
     stream = torch.cuda.Stream()
     stream.wait_stream(torch.cuda.current_stream())
-    args = (ctypes.c_void_p(x.data_ptr()), ctypes.c_void_p(wt.data_ptr()), None, c_in, h, w, c_out, k, s, p,
-            ctypes.c_void_p(out.data_ptr()), ctypes.byref(plan), ctypes.c_void_p(stream.cuda_stream))
-    f = ilpm.lib.ilpm_conv2d_fwd_plan
+    f, args = call_args(ilpm, bufs, shape, plan, stream.cuda_stream)
     with torch.cuda.stream(stream):
         for _ in range(3):
             rc = f(*args)
             if rc != 0:
-                raise ilpm.IlpmError(rc, "ilpm_conv2d_fwd_plan")
+                raise ilpm.IlpmError(rc, f.__name__)
         torch.cuda.synchronize()
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g, stream=stream):
@@ -126,7 +137,7 @@ def spin_up(torch, ms=300.0):
         torch.cuda.synchronize()
 
 
-def sweep(shapes, reps=100, graph=False):
+def sweep(shapes, reps=100, graph=False, prepacked=False):
     import torch
     import paper_1909_02765_amd as ilpm
     torch.cuda.set_device(0)
@@ -140,10 +151,15 @@ def sweep(shapes, reps=100, graph=False):
         wt = torch.randn((c_out, c_in, k, k), device="cuda") * 0.05
         out = torch.empty((1, c_out, ho, wo), device="cuda")
         rows = []
+        packs = {}
         for plan in candidate_plans(ilpm, shape):
             if plan.path == ilpm.PATH_DIRECT and plan.variant == 1 and c_in * c_out * ho * wo * k * k > 3e8:
                 continue  # the plain fallback is far too slow to matter here
-            us = timer(torch, ilpm, (x, wt, out), shape, plan, reps)
+            bufs = (x, wt, out)
+            if prepacked:
+                packs[id(plan)] = ilpm.prepack_weights(wt, plan)
+                bufs = (x, wt, out, packs[id(plan)])
+            us = timer(torch, ilpm, bufs, shape, plan, reps)
             rows.append(({"variant": ilpm.variant_name(plan.path, plan.variant), "path": plan.path,
                           "splits": plan.splits, "us": round(us, 3)}, plan))
         rows.sort(key=lambda r: r[0]["us"])
@@ -155,13 +171,15 @@ def sweep(shapes, reps=100, graph=False):
             row["us_refined"] = float("inf")
         for _ in range(3):
             for row, plan in finalists:
-                us = timer(torch, ilpm, (x, wt, out), shape, plan, reps * 10)
+                bufs = (x, wt, out, packs[id(plan)]) if prepacked else (x, wt, out)
+                us = timer(torch, ilpm, bufs, shape, plan, reps * 10)
                 row["us_refined"] = round(min(row["us_refined"], us), 3)
         finalists.sort(key=lambda r: r[0]["us_refined"])
         ranked = [row for row, _ in finalists + rows[FINALISTS:]]
         key = ",".join(str(v) for v in shape)
-        result[key] = {"best": ranked[0], "top": ranked[:8]}
+        result[key] = {"best": ranked[0], "top": ranked[:8], "prepacked": prepacked}
         print(key, ranked[0], flush=True)
+        del packs
     return result
 
 
@@ -221,8 +239,10 @@ def emit(table, path=INC):
         b = choose(v, current.get(key))
         us = b.get("us_refined", b["us"])
         rows[key] = "{%s, \"%s\", %d},  // %.2f us" % (key.replace(",", ", "), b["variant"], b["splits"], us)
+    what = ("with prepacked weights (written by tune.py --emit --prepacked)" if path == INC_PREPACKED
+            else "(written by tune.py --emit)")
     lines = ["// {C_in, H, W, C_out, K, stride, pad, \"variant\", splits}",
-             "// Fastest measured plan per shape on one MI355X (written by tune.py --emit)."]
+             "// Fastest measured plan per shape on one MI355X " + what + "."]
     for key in sorted(rows, key=lambda k: [int(t) for t in k.split(",")]):
         lines.append(rows[key].rstrip())
     with open(path, "w") as f:
@@ -238,14 +258,19 @@ def main():
                     help="sweep only these shapes (default: every workload and VGG-16 / ResNet layer)")
     ap.add_argument("--graph", action="store_true",
                     help="time calls replayed from a HIP graph (for launch-bound layers)")
+    ap.add_argument("--prepacked", action="store_true",
+                    help="time plans on prepacked weights / emit the prepacked table")
     args = ap.parse_args()
     if args.emit:
         with open(args.emit) as f:
-            emit(json.load(f))
+            table = json.load(f)
+        if any(v.get("prepacked", False) != args.prepacked for v in table.values()):
+            raise SystemExit("the sweep's weight layout does not match --prepacked")
+        emit(table, INC_PREPACKED if args.prepacked else INC)
         return
     shapes = ([tuple(int(t) for t in sh.split(",")) for sh in args.shapes] if args.shapes
               else default_shapes())
-    table = sweep(shapes, args.reps, args.graph)
+    table = sweep(shapes, args.reps, args.graph, args.prepacked)
     if args.out:
         with open(args.out, "w") as f:
             json.dump(table, f, indent=1)

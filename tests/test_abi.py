@@ -411,3 +411,30 @@ def test_low_channel_direct_variants_plan_only_short_contractions():
         ilpm.plan_variant(7, 30, 30, 20, 3, 2, 1, ilpm.PATH_DIRECT, v)        # 63
         with pytest.raises(ilpm.IlpmError):
             ilpm.plan_variant(8, 30, 30, 20, 3, 1, 1, ilpm.PATH_DIRECT, v)    # 72 > 64
+
+
+def test_launcher_object_keeps_and_reports():
+    """The launcher object behind conv2d_launcher & co.: it holds what it is
+    given to keep, passes the marshalled arguments, and turns a non-OK
+    status into IlpmError (host only: a stand-in entry point)."""
+    import gc
+    import weakref
+
+    class Held:
+        pass
+
+    calls = []
+    held = Held()
+    ref = weakref.ref(held)
+    ok = ilpm._Launcher(lambda *a: calls.append(a) or ilpm.OK, (1, 2), (held,), "stand_in")
+    del held
+    gc.collect()
+    assert ref() is not None
+    ok()
+    assert calls == [(1, 2)]
+    bad = ilpm._Launcher(lambda *a: ilpm.ERR_INVALID_ARG, (), (), "stand_in")
+    with pytest.raises(ilpm.IlpmError):
+        bad()
+    del ok
+    gc.collect()
+    assert ref() is None

@@ -1,7 +1,8 @@
 """GPU: the fused epilogue (bias + ReLU, 2x2 max-pool) of every variant and
 split count gives exactly the unfused sequence -- the same plan's convolution,
-then ReLU, then the pool, applied to its fp32 output -- and, anchored to the
-oracle, max-pool(ReLU(exact conv)) within the tolerance."""
+then ReLU, then the pool, applied to its fp32 output -- on OIHW and on
+prepacked weights, and, anchored to the oracle, max-pool(ReLU(exact conv))
+within the tolerance."""
 import numpy as np
 import pytest
 
@@ -61,14 +62,19 @@ def check_case(ilpm, name, x, w, b, s, p, skip_slow=False):
         if skip_slow and plan.path == ilpm.PATH_DIRECT and plan.variant == 1:
             continue
         unfused = ilpm.conv2d(xd, wdv, bd, s, p, plan=plan)
+        packed = ilpm.prepack_weights(wdv, plan)
         torch.cuda.synchronize()
         base = unfused.cpu().numpy()
         for epi in EPIS:
             note(f"[epilogue] {name} path={plan.path} v={plan.variant} splits={plan.splits} epi={epi}")
             got = ilpm.conv2d_epilogue(xd, wdv, bd, s, p, epi, plan=plan)
             torch.cuda.synchronize()
-            np.testing.assert_array_equal(got.cpu().numpy(), pool_relu_np(base, epi),
-                                          err_msg=f"{name} plan {plan.path}/{plan.variant}/{plan.splits} epi {epi}")
+            label = f"{name} plan {plan.path}/{plan.variant}/{plan.splits} epi {epi}"
+            np.testing.assert_array_equal(got.cpu().numpy(), pool_relu_np(base, epi), err_msg=label)
+            note(f"[epilogue prepacked] {name} path={plan.path} v={plan.variant} splits={plan.splits} epi={epi}")
+            got = ilpm.conv2d_prepacked_epilogue(xd, packed, c_out, k, bd, s, p, epi, plan=plan)
+            torch.cuda.synchronize()
+            np.testing.assert_array_equal(got.cpu().numpy(), pool_relu_np(base, epi), err_msg=label + " prepacked")
 
 
 @pytest.mark.parametrize("case", workloads.ALL_CASES, ids=lambda c: c.name)
@@ -143,6 +149,17 @@ def test_pooled_tile_writes_only_the_pooled_output(ilpm):
                 np.testing.assert_array_equal(out.cpu().numpy(), want, err_msg=name)
                 if name in in_kernel:
                     assert torch.isnan(ws).all(), f"{name}: the pooled tile went through the workspace"
+                # the same with prepacked weights (the kernel pools in the workgroup too)
+                packed = ilpm.prepack_weights(wdv, plan)
+                buf.fill_(float("nan"))
+                note(f"[pooled tile prepacked] shape {(c_in, h, w_, c_out)} v={v} {name}")
+                ilpm.conv2d_prepacked_epilogue(xd, packed, c_out, 3, bd, 1, 1, ilpm.EPI_RELU | ilpm.EPI_MAXPOOL2,
+                                               plan=plan, out=out)
+                torch.cuda.synchronize()
+                assert torch.isnan(buf[:guard]).all() and torch.isnan(buf[guard + n:]).all(), name + " prepacked"
+                np.testing.assert_array_equal(out.cpu().numpy(), want, err_msg=name + " prepacked")
+                if name in in_kernel:
+                    assert torch.isnan(ws).all(), f"{name} prepacked: the pooled tile went through the workspace"
     finally:
         torch.cuda.synchronize()
         ilpm.set_workspace(None)

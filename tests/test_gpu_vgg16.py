@@ -10,7 +10,10 @@ the GPU layer consumed.
   after stages 1-4), default plans -- each layer's output against the
   oracle's conv -> ReLU (-> pool) of that layer's GPU input, within the
   tolerance of the window element the maximum comes from (ReLU and max are
-  1-Lipschitz, so the largest tolerance in a window bounds the difference)."""
+  1-Lipschitz, so the largest tolerance in a window bounds the difference).
+* Fused on prepacked weights: the same with ilpm_conv2d_plan_prepacked's
+  plans and ilpm_conv2d_fwd_prepacked_epilogue, as the benchmark's
+  prepacked stack runs it."""
 import numpy as np
 import pytest
 
@@ -79,6 +82,38 @@ def test_vgg16_fused_stack_against_oracle():
         assert np.isfinite(got).all(), name
         err = np.abs(got - want)
         assert (err <= tol).all(), f"{name}: worst |gpu-ref|/tol {np.max(err / tol):.3g}"
+        x = y
+    assert tuple(x.shape) == (1, 512, 14, 14)
+
+
+def _check_fused_layer(name, x_gpu, w_np, ci, pool, y):
+    ref, sab = oracle.conv2d_f64(x_gpu.cpu().numpy(), w_np, None, 1, 1)
+    tol = oracle.tolerance(sab, ci, 3)
+    want = np.maximum(ref, 0.0)
+    if pool:
+        want, tol = _pool_max(want), _pool_max(tol)
+    got = y.cpu().numpy().astype(np.float64)
+    assert got.shape == want.shape, (name, got.shape, want.shape)
+    assert np.isfinite(got).all(), name
+    err = np.abs(got - want)
+    assert (err <= tol).all(), f"{name}: worst |gpu-ref|/tol {np.max(err / tol):.3g}"
+
+
+def test_vgg16_fused_prepacked_stack_against_oracle():
+    torch = torch_cuda()
+    import paper_1909_02765_amd as ilpm
+    oracle.set_threads(16)
+    x = dev(workloads.vgg16_input())
+    for name, ci, co, hw, pool, seed in workloads.vgg16_layers():
+        w_np = workloads.vgg16_weights(ci, co, seed)
+        epi = ilpm.EPI_RELU | (ilpm.EPI_MAXPOOL2 if pool else 0)
+        plan = ilpm.plan_prepacked(ci, hw, hw, co, 3, 1, 1)
+        packed = ilpm.prepack_weights(dev(w_np), plan)
+        note(f"[vgg16 fused prepacked] {name} {ci}->{co} @{hw} epi={epi} path={plan.path} "
+             f"v={ilpm.variant_name(plan.path, plan.variant)} splits={plan.splits}")
+        y = ilpm.conv2d_prepacked_epilogue(x, packed, co, 3, None, 1, 1, epi, plan=plan)
+        torch.cuda.synchronize()
+        _check_fused_layer(name, x, w_np, ci, pool, y)
         x = y
     assert tuple(x.shape) == (1, 512, 14, 14)
 
