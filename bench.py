@@ -135,10 +135,16 @@ def time_layer_graph(torch, ilpm, x, w, b, s, p, out, steps, per_graph=20):
     graph of `per_graph` launches (no host launch cost between calls).  The
     library allocates nothing during capture: the calls made before it have
     already sized its workspace."""
+    return time_graph(torch, lambda: ilpm.conv2d_launcher(x, w, b, s, p, out), steps, per_graph)
+
+
+def time_graph(torch, make_launch, steps, per_graph=20):
+    """time_layer_graph for any launcher: make_launch() is called with the
+    capture stream current, so the launcher it returns is bound to it."""
     stream = torch.cuda.Stream()
     stream.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(stream):
-        launch = ilpm.conv2d_launcher(x, w, b, s, p, out)
+        launch = make_launch()
         for _ in range(3):
             launch()
         torch.cuda.synchronize()
@@ -467,6 +473,8 @@ def main():
                          "gflops": round(rr["flops"] / rr["us"] / 1e3, 1),
                          "floor_us": round(fl, 3), "bound": kind, "frac": round(fl / rr["us"], 4),
                          "plan": rr["plan"].as_dict()})
+            rows[-1].update(prepacked_plan_row(torch, ilpm, c.c_in, c.h, c.w, c.c_out, c.k, c.stride, c.pad,
+                                               rr["x"], rr["w"], rr["b"], rr["out"], max(200, args.steps // 4)))
             print(json.dumps(rows[-1]), file=sys.stderr)
         rows += bench_vgg16(torch, ilpm, workloads, max(200, args.steps // 10))
         if args.report:
@@ -521,6 +529,14 @@ def config_rows(torch, ilpm, workloads, headline, failures, steps=500, warmup=20
         row = {"workload": name, "us": round(us, 3), "graph_us": round(gus, 3),
                "gflops": round(flops / us / 1e3, 1), "bound": kind, "floor_us": round(fl, 3),
                "frac": round(fl / us, 4), "plan": ilpm.variant_name(plan.path, plan.variant) + f" x{plan.splits}"}
+        # The same layer on weights packed once beforehand for the plan
+        # ilpm_conv2d_plan_prepacked picks (graph replay).
+        pplan = ilpm.plan_prepacked(c.c_in, c.h, c.w, c.c_out, c.k, c.stride, c.pad)
+        packed = ilpm.prepack_weights(wd, pplan)
+        pus = time_graph(torch, lambda: ilpm.conv2d_prepacked_launcher(xd, packed, c.c_out, c.k, bd, c.stride, c.pad,
+                                                                      out, pplan), steps)
+        row["prepacked_graph_us"] = round(pus, 3)
+        row["prepacked_plan"] = ilpm.variant_name(pplan.path, pplan.variant) + f" x{pplan.splits}"
         if kind == "hbm":
             cus = time_cold(torch, ilpm, xd, wd, bd, c.stride, c.pad, out)
             row["cold_us"] = round(cus, 3)
@@ -589,6 +605,18 @@ def run_lds_probe(torch, iters=1000):
     return {"lds_probe_iters": iters, "patterns": names}
 
 
+def prepacked_plan_row(torch, ilpm, c_in, h, w_, c_out, k, s, p, x, w, b, out, steps):
+    """The layer on weights packed once for ilpm_conv2d_plan_prepacked's plan:
+    graph-replay µs and the plan's name."""
+    from workloads import to_device
+    x, w, b = (t if t is None or hasattr(t, "is_cuda") else to_device(torch, t) for t in (x, w, b))
+    plan = ilpm.plan_prepacked(c_in, h, w_, c_out, k, s, p)
+    packed = ilpm.prepack_weights(w, plan)
+    us = time_graph(torch, lambda: ilpm.conv2d_prepacked_launcher(x, packed, c_out, k, b, s, p, out, plan), steps)
+    return {"prepacked_plan_graph_us": round(us, 3),
+            "prepacked_plan": ilpm.variant_name(plan.path, plan.variant) + f" x{plan.splits}"}
+
+
 def bench_vgg16(torch, ilpm, workloads, steps):
     from workloads import to_device
     rows = []
@@ -605,6 +633,7 @@ def bench_vgg16(torch, ilpm, workloads, steps):
         rows.append({"layer": f"vgg16_{name}", "us": round(us, 3), "graph_us": round(gus, 3),
                      "gflops": round(flops / us / 1e3, 1),
                      "floor_us": round(fl, 3), "bound": kind, "frac": round(fl / us, 4), "plan": plan.as_dict()})
+        rows[-1].update(prepacked_plan_row(torch, ilpm, ci, hw, hw, co, 3, 1, 1, x, w, None, out, steps))
         print(json.dumps(rows[-1]), file=sys.stderr)
         total_us += us
         total_graph_us += gus
