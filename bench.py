@@ -662,7 +662,10 @@ def bench_vgg16_stack(torch, ilpm, workloads, reps):
     x = x0
     for (name, ci, co, hw, pool, _), w in zip(layers, ws):
         y = torch.empty((1, co, hw, hw), device="cuda", dtype=torch.float32)
-        conv = ilpm.conv2d_launcher(x, w, None, 1, 1, y)
+        # the plan the fused call below picks for this layer's epilogue, so
+        # that the two sequences round alike and must match bit for bit
+        plan = ilpm.plan_for(ci, hw, hw, co, 3, 1, 1, ilpm.EPI_RELU | (ilpm.EPI_MAXPOOL2 if pool else 0))
+        conv = ilpm.conv2d_launcher(x, w, None, 1, 1, y, plan=plan)
         launches.append(conv)
         launches.append(lambda y=y: ilpm.relu_(y))
         if pool:
@@ -747,14 +750,14 @@ def bench_vgg16_stack(torch, ilpm, workloads, reps):
     torch.cuda.synchronize()
     graph_same = graph_same and bool(torch.equal(out_graph, ref))
     # The fused stack on prepacked weights: each layer on the plan
-    # ilpm_conv2d_plan_prepacked picks, its weights packed once beforehand
+    # ilpm_conv2d_plan_for picks for its epilogue, its weights packed once beforehand
     # (outside the timed region, like loading a model).  Checked bit for bit
     # against the same plans run on the OIHW weights.
     pre, ref_pre = [], []
     x = xp = x0
     for (name, ci, co, hw, pool, _), w in zip(layers, ws):
         epi = ilpm.EPI_RELU | (ilpm.EPI_MAXPOOL2 if pool else 0)
-        plan = ilpm.plan_prepacked(ci, hw, hw, co, 3, 1, 1)
+        plan = ilpm.plan_for(ci, hw, hw, co, 3, 1, 1, epi, prepacked=True)
         packed = ilpm.prepack_weights(w, plan)
         y = torch.empty(ilpm.epilogue_out_shape(co, hw, hw, 3, 1, 1, epi), device="cuda", dtype=torch.float32)
         pre.append(ilpm.conv2d_prepacked_epilogue_launcher(xp, packed, co, 3, None, 1, 1, epi, y, plan))
@@ -771,7 +774,7 @@ def bench_vgg16_stack(torch, ilpm, workloads, reps):
         xp = x0
         for (name, ci, co, hw, pool, _), w in zip(layers, ws):
             epi = ilpm.EPI_RELU | (ilpm.EPI_MAXPOOL2 if pool else 0)
-            plan = ilpm.plan_prepacked(ci, hw, hw, co, 3, 1, 1)
+            plan = ilpm.plan_for(ci, hw, hw, co, 3, 1, 1, epi, prepacked=True)
             packed = ilpm.prepack_weights(w, plan)
             y = torch.empty(ilpm.epilogue_out_shape(co, hw, hw, 3, 1, 1, epi), device="cuda", dtype=torch.float32)
             pre_s.append(ilpm.conv2d_prepacked_epilogue_launcher(xp, packed, co, 3, None, 1, 1, epi, y, plan))
@@ -805,7 +808,7 @@ def bench_vgg16_stack(torch, ilpm, workloads, reps):
             {"layer": "vgg16_stack_fused_graph", "us": round(t_graph, 3),
              "note": "the fused stack replayed from one captured HIP graph", "same_output_bits": graph_same},
             {"layer": "vgg16_stack_fused_prepacked", "us": round(t_pre, 3),
-             "note": "the fused stack on weights prepacked once for ilpm_conv2d_plan_prepacked's plans "
+             "note": "the fused stack on weights prepacked once for ilpm_conv2d_plan_for's plans "
                      "(bits equal the same plans on OIHW weights)", "same_output_bits": pre_same},
             {"layer": "vgg16_stack_fused_prepacked_graph", "us": round(t_pre_graph, 3),
              "note": "the prepacked fused stack replayed from one captured HIP graph",

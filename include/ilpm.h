@@ -307,6 +307,21 @@ int ilpm_conv2d_fwd_prepacked(const float *in, const float *packed, const float 
 int ilpm_conv2d_plan_prepacked(int C_in, int H, int W, int C_out, int K, int stride, int pad,
                                ilpm_plan *plan);
 
+/*
+ * ilpm_conv2d_plan_for -- the default plan for this shape, epilogue (the
+ * ILPM_EPI_* bits the calls will pass) and weight layout (prepacked 0: OIHW,
+ * 1: packed for the plan).  With ILPM_EPI_MAXPOOL2 the plan comes from the
+ * measured tables of the pooled epilogue, where a plan whose tiles pool in
+ * the workgroup can beat a faster convolution that needs the second kernel;
+ * a shape missing there falls back as ilpm_conv2d_plan_prepacked /
+ * ilpm_conv2d_plan do.  ilpm_conv2d_fwd_epilogue with plan NULL uses this
+ * plan (prepacked 0).  Pure host; chosen once per (shape, epilogue kind,
+ * layout) and kept.  ILPM_ERR_INVALID_ARG for unknown epilogue bits or
+ * prepacked other than 0 or 1.
+ */
+int ilpm_conv2d_plan_for(int C_in, int H, int W, int C_out, int K, int stride, int pad, int epilogue,
+                         int prepacked, ilpm_plan *plan);
+
 /* ---- fused epilogue ----
  *
  * A CNN layer follows the convolution with ReLU and, between stages, a 2x2
@@ -323,7 +338,8 @@ int ilpm_conv2d_plan_prepacked(int C_in, int H, int W, int C_out, int K, int str
  * combination of the ILPM_EPI_* bits (0 = none).  With both bits set the
  * result is max-pool of ReLU, which equals ReLU of max-pool.  `out` has the
  * pooled shape when ILPM_EPI_MAXPOOL2 is set.  plan: NULL for the default
- * plan of the shape, or one made for this exact shape.  One-split
+ * plan of the shape and epilogue (ilpm_conv2d_plan_for), or one made for
+ * this exact shape.  One-split
  * matrix-core plans whose tiles have even sides pool inside the kernel;
  * other plans write the full-size convolution output (as per-split partial
  * sums) to the workspace and pool it in a second kernel

@@ -97,6 +97,7 @@ _SIGS = {
     "ilpm_conv2d_validate": ([_vp, _vp, _vp] + [_i] * 7 + [_vp], _i),
     "ilpm_conv2d_plan": ([_i] * 7 + [_plan_p], _i),
     "ilpm_conv2d_plan_prepacked": ([_i] * 7 + [_plan_p], _i),
+    "ilpm_conv2d_plan_for": ([_i] * 9 + [_plan_p], _i),
     "ilpm_conv2d_plan_variant": ([_i] * 10 + [_plan_p], _i),
     "ilpm_num_variants": ([_i], _i),
     "ilpm_variant_name": ([_i, _i], ctypes.c_char_p),
@@ -169,6 +170,14 @@ def plan_prepacked(c_in, h, w, c_out, k, stride=1, pad=0) -> ilpm_plan:
     p = ilpm_plan()
     _check(lib.ilpm_conv2d_plan_prepacked(c_in, h, w, c_out, k, stride, pad, ctypes.byref(p)),
            "ilpm_conv2d_plan_prepacked")
+    return p
+
+
+def plan_for(c_in, h, w, c_out, k, stride=1, pad=0, epilogue=0, prepacked=False) -> ilpm_plan:
+    """The plan the library picks for this shape, epilogue and weight layout."""
+    p = ilpm_plan()
+    _check(lib.ilpm_conv2d_plan_for(c_in, h, w, c_out, k, stride, pad, epilogue, 1 if prepacked else 0,
+                                    ctypes.byref(p)), "ilpm_conv2d_plan_for")
     return p
 
 
@@ -290,7 +299,7 @@ class _Launcher:
             raise IlpmError(rc, self.name)
 
 
-def conv2d_launcher(x, w, bias, stride, pad, out, stream=None):
+def conv2d_launcher(x, w, bias, stride, pad, out, stream=None, plan: Optional[ilpm_plan] = None):
     """A zero-argument callable that enqueues the same conv2d again, with the
     arguments marshalled once (for timing loops and graph capture).
 
@@ -298,11 +307,17 @@ def conv2d_launcher(x, w, bias, stride, pad, out, stream=None):
     stream) they come from alive: a tensor freed while a launcher still
     points at it could be returned to the driver -- torch empties its cache
     when a graph capture begins -- and the next launch would then read
-    unmapped memory.  The stream is the one current when the launcher is made."""
+    unmapped memory.  The stream is the one current when the launcher is made.
+    With `plan`, the calls run that plan (ilpm_conv2d_fwd_plan)."""
     _, c_in, h, wd = x.shape
     c_out, _, k, _ = w.shape
     if tuple(out.shape) != (1, c_out, out_size(h, k, stride, pad), out_size(wd, k, stride, pad)):
         raise ValueError("out has the wrong shape")
+    if plan is not None:
+        args = (_dev_f32(x, "x"), _dev_f32(w, "w"), _dev_f32(bias, "bias") if bias is not None else None,
+                c_in, h, wd, c_out, k, stride, pad, _dev_f32(out, "out"), ctypes.byref(plan), _stream_handle(stream))
+        return _Launcher(lib.ilpm_conv2d_fwd_plan, args, (x, w, bias, out, plan, _stream_obj(stream)),
+                         "ilpm_conv2d_fwd_plan")
     args = (_dev_f32(x, "x"), _dev_f32(w, "w"), _dev_f32(bias, "bias") if bias is not None else None,
             c_in, h, wd, c_out, k, stride, pad, _dev_f32(out, "out"), _stream_handle(stream))
     return _Launcher(lib.ilpm_conv2d_fwd, args, (x, w, bias, out, _stream_obj(stream)), "ilpm_conv2d_fwd")

@@ -128,16 +128,22 @@ int validate(const void *in, const void *w, const void *bias, const ConvShape &s
     return ILPM_OK;
 }
 
-// The default plan: the measured best for this exact shape when the tuning
-// table has it (for prepacked weights their own table first, then the OIHW
-// one), else the cheapest matrix-core variant for this filter size and
-// stride by the cost model, else the LDS direct kernel, else the plain one.
-// The environment overrides (read once) narrow the candidates.
-int compute_plan(const ConvShape &s, ilpm_plan *p, bool prepacked)
+// The default plan: the measured best for this exact shape when a tuning
+// table has it -- the table of this weight layout and epilogue first, then
+// (pooled) the plain table of the same layout, then the OIHW tables -- else
+// the cheapest matrix-core variant for this filter size and stride by the
+// cost model, else the LDS direct kernel, else the plain one.  The
+// environment overrides (read once) narrow the candidates.
+int compute_plan(const ConvShape &s, ilpm_plan *p, bool prepacked, bool pooled)
 {
     const Overrides &o = overrides();
     const bool any = o.path < 0 && o.splits == 0 && o.tile_h == 0;
-    if (any && ((prepacked && tuned_plan(s, p, true)) || tuned_plan(s, p, false))) return ILPM_OK;
+    if (any) {
+        if (pooled && prepacked && tuned_plan(s, p, true, true)) return ILPM_OK;
+        if (prepacked && tuned_plan(s, p, true, false)) return ILPM_OK;
+        if (pooled && tuned_plan(s, p, false, true)) return ILPM_OK;
+        if (tuned_plan(s, p, false, false)) return ILPM_OK;
+    }
     auto tile_ok = [&](const ilpm_plan &q) { return o.tile_h == 0 || (q.tile_h == o.tile_h && q.tile_w == o.tile_w); };
     if (o.path != ILPM_PATH_DIRECT) {
         bool found = false;
@@ -174,7 +180,7 @@ int compute_plan(const ConvShape &s, ilpm_plan *p, bool prepacked)
 // the cost-model sweep.
 struct PlanSlot {
     bool used = false;
-    bool prepacked;
+    int mode;  // 1: prepacked weights, 2: pooled epilogue
     ConvShape s;
     int rc;
     ilpm_plan p;
@@ -188,24 +194,25 @@ bool same_shape(const ConvShape &a, const ConvShape &b)
            a.stride == b.stride && a.pad == b.pad;
 }
 
-int choose_plan(const ConvShape &s, ilpm_plan *p, bool prepacked = false)
+int choose_plan(const ConvShape &s, ilpm_plan *p, bool prepacked = false, bool pooled = false)
 {
-    uint64_t h = 1469598103934665603ull;  // FNV-1a over the seven sizes and the weight layout
-    for (int v : {s.c_in, s.h, s.w, s.c_out, s.k, s.stride, s.pad, (int)prepacked})
+    const int mode = (prepacked ? 1 : 0) | (pooled ? 2 : 0);
+    uint64_t h = 1469598103934665603ull;  // FNV-1a over the seven sizes and the mode
+    for (int v : {s.c_in, s.h, s.w, s.c_out, s.k, s.stride, s.pad, mode})
         h = (h ^ (uint32_t)v) * 1099511628211ull;
     PlanSlot &slot = g_plan_cache[h % kPlanSlots];
     {
         std::lock_guard<std::mutex> lk(g_mu);
-        if (slot.used && slot.prepacked == prepacked && same_shape(slot.s, s)) {
+        if (slot.used && slot.mode == mode && same_shape(slot.s, s)) {
             *p = slot.p;
             return slot.rc;
         }
     }
     ilpm_plan q = {};
-    const int rc = compute_plan(s, &q, prepacked);
+    const int rc = compute_plan(s, &q, prepacked, pooled);
     std::lock_guard<std::mutex> lk(g_mu);
     slot.used = true;
-    slot.prepacked = prepacked;
+    slot.mode = mode;
     slot.s = s;
     slot.rc = rc;
     slot.p = q;
@@ -434,6 +441,17 @@ int ilpm_conv2d_plan_prepacked(int C_in, int H, int W, int C_out, int K, int str
     return choose_plan(s, plan, true);
 }
 
+int ilpm_conv2d_plan_for(int C_in, int H, int W, int C_out, int K, int stride, int pad, int epilogue,
+                         int prepacked, ilpm_plan *plan)
+{
+    if (!plan || (epilogue & ~(ILPM_EPI_RELU | ILPM_EPI_MAXPOOL2)) || (prepacked != 0 && prepacked != 1))
+        return ILPM_ERR_INVALID_ARG;
+    ConvShape s;
+    int rc = check_dims(C_in, H, W, C_out, K, stride, pad, &s);
+    if (rc != ILPM_OK) return rc;
+    return choose_plan(s, plan, prepacked != 0, (epilogue & ILPM_EPI_MAXPOOL2) != 0);
+}
+
 int ilpm_conv2d_plan_variant(int C_in, int H, int W, int C_out, int K, int stride, int pad, int path,
                              int variant, int splits, ilpm_plan *plan)
 {
@@ -513,7 +531,7 @@ int ilpm_conv2d_epilogue_workspace_size(int C_in, int H, int W, int C_out, int K
         rc = check_plan(s, *plan);
         p = *plan;
     } else {
-        rc = choose_plan(s, &p);
+        rc = choose_plan(s, &p, false, (epilogue & ILPM_EPI_MAXPOOL2) != 0);
     }
     if (rc != ILPM_OK) return rc;
     *bytes = workspace_need(p, s, epilogue);
@@ -669,7 +687,7 @@ int ilpm_conv2d_fwd_epilogue(const float *in, const float *w, const float *bias,
         rc = check_plan(s, *plan);
         p = *plan;
     } else {
-        rc = choose_plan(s, &p);
+        rc = choose_plan(s, &p, false, (epilogue & ILPM_EPI_MAXPOOL2) != 0);
     }
     if (rc != ILPM_OK) return rc;
     return run(in, w, bias, s, out, p, stream, false, epilogue);

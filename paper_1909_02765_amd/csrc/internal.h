@@ -60,9 +60,10 @@ hipError_t winograd_filter_launch(const float *w, int c_in, int c_out, float *u,
 int winograd_launch(const ConvShape &s, const float *x, const float *u, const float *bias, float *out,
                     void *workspace, int dev, hipStream_t stream, hipError_t *err);
 
-// ---- measured plan table (tuned_plans.inc) ----
-// The plan the offline sweep found fastest for this exact shape, if any.
-bool tuned_plan(const ConvShape &s, ilpm_plan *p, bool prepacked);
+// ---- measured plan tables (tuned_plans*.inc) ----
+// The plan the offline sweep found fastest for this exact shape, weight
+// layout and epilogue (pooled: ReLU + 2x2 max-pool), if any.
+bool tuned_plan(const ConvShape &s, ilpm_plan *p, bool prepacked, bool pooled);
 
 // ---- helpers ----
 hipError_t launch_relu(float *x, int64_t n, hipStream_t stream);

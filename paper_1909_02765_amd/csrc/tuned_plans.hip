@@ -1,7 +1,9 @@
 // The measured plan tables: for shapes the offline sweep timed on MI355X
-// (tune.py), the fastest (kernel variant, split count), one table for OIHW
-// weights and one for prepacked weights (the kernels load these differently,
-// so the fastest variant can differ).  Entries name the variant, so the
+// (tune.py), the fastest (kernel variant, split count), one table per
+// (weight layout, epilogue) pair: OIHW or prepacked weights (the kernels load
+// these differently, so the fastest variant can differ), and the plain
+// convolution or the fused ReLU + 2x2 max-pool epilogue (a plan whose tiles
+// pool in the workgroup saves the second kernel the others need).  Entries name the variant, so the
 // tables survive changes to the variant list; an entry whose variant no
 // longer exists, or no longer accepts the shape, is ignored.
 #include <cstring>
@@ -25,6 +27,14 @@ const TunedEntry kTunedPrepacked[] = {
 #include "tuned_plans_prepacked.inc"
 };
 
+const TunedEntry kTunedPooled[] = {
+#include "tuned_plans_pooled.inc"
+};
+
+const TunedEntry kTunedPooledPrepacked[] = {
+#include "tuned_plans_pooled_prepacked.inc"
+};
+
 template <size_t N>
 bool lookup(const TunedEntry (&table)[N], const ConvShape &s, ilpm_plan *p)
 {
@@ -43,8 +53,9 @@ bool lookup(const TunedEntry (&table)[N], const ConvShape &s, ilpm_plan *p)
 
 }  // namespace
 
-bool tuned_plan(const ConvShape &s, ilpm_plan *p, bool prepacked)
+bool tuned_plan(const ConvShape &s, ilpm_plan *p, bool prepacked, bool pooled)
 {
+    if (pooled) return prepacked ? lookup(kTunedPooledPrepacked, s, p) : lookup(kTunedPooled, s, p);
     return prepacked ? lookup(kTunedPrepacked, s, p) : lookup(kTuned, s, p);
 }
 

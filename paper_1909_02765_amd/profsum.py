@@ -17,6 +17,8 @@ mean over the dispatches that each follow a 512 MiB scrub.
 
     python -m paper_1909_02765_amd.profsum trace D --log L  # kernel-trace table (markdown)
     python -m paper_1909_02765_amd.profsum counters D LOG   # mean of each counter, timed dispatches
+    python -m paper_1909_02765_amd.profsum layers D W...     # per-layer table from <D>/<W>_{FETCH_SIZE,
+                                                            # WRITE_SIZE,sqa,sqb,kt} runs (markdown)
 """
 from __future__ import annotations
 
@@ -110,6 +112,52 @@ def traffic(fetch_dir, write_dir):
         "us_per_layer_under_counters": [f["line"]["us_per_layer"], w["line"]["us_per_layer"]]}
 
 
+def timed_trace_ns(d, line):
+    """Durations (ns) of the timed dispatches of the run's most frequent
+    convolution kernel, from a kernel trace and the run's bench line (either
+    a --counter-run line or the default one)."""
+    durs = trace_durations(d)
+    name = max((n for n in durs if is_conv_kernel(n)), key=lambda n: len(durs[n]))
+    if "dispatches" in line:
+        dsp = line["dispatches"]
+        skip, n = dsp["spinup"] + dsp["warmup"], dsp["timed"]
+    else:
+        skip, n = line["spinup_calls"] + line["warmup"], line["steps"]
+    return name, durs[name][skip:skip + n]
+
+
+def layers_table(root, workloads):
+    """One row per workload: plan, median kernel duration, counters per
+    dispatch and derived shares, HBM bytes (calibrated)."""
+    out = ["| layer | plan | kernel µs (median) | waves | VALU inst | MFMA inst | SALU inst | LDS inst | "
+           "bank-conflict cycles / LDS inst | MFMA busy | TA busy | fetch MB | write MB |",
+           "|---|---|---|---|---|---|---|---|---|---|---|---|---|"]
+    for w in workloads:
+        base = os.path.join(root, w)
+        _, t = traffic(base + "_FETCH_SIZE", base + "_WRITE_SIZE")
+        la = _bench_line(base + "_sqa.log")
+        _, ca = timed_conv(dispatch_counters(base + "_sqa"), la)
+        lb = _bench_line(base + "_sqb.log")
+        _, cb = timed_conv(dispatch_counters(base + "_sqb"), lb)
+        lk = _bench_line(base + "_kt.log")
+        _, d = timed_trace_ns(base + "_kt", lk)
+        med = statistics.median(d)
+        m = {k: counter_mean(ca, k) for k in ca[0]}
+        m.update({k: counter_mean(cb, k) for k in cb[0]})
+        # Shares over the kernel's own duration at the measured clock: the
+        # matrix-pipe cycles per SIMD (1024 SIMDs) and the address-unit busy
+        # cycles per CU (256 TAs), against median duration x 2.4 GHz.
+        cyc = med * 2.4
+        mfma = m["SQ_VALU_MFMA_BUSY_CYCLES"] / 1024.0 / cyc
+        ta = m["TA_TA_BUSY"] / 256.0 / cyc
+        bank = m["SQ_LDS_BANK_CONFLICT"] / m["SQ_INSTS_LDS"] if m["SQ_INSTS_LDS"] else 0.0
+        out.append(f"| {w} | {la['plan']} | {med / 1e3:.2f} | {m['SQ_WAVES']:.0f} | {m['SQ_INSTS_VALU']:.0f} | "
+                   f"{m['SQ_INSTS_MFMA']:.0f} | {m['SQ_INSTS_SALU']:.0f} | {m['SQ_INSTS_LDS']:.0f} | {bank:.2f} | "
+                   f"{100 * mfma:.1f}% | {100 * ta:.1f}% | {t['fetch_bytes_per_launch'] / 1e6:.3f} | "
+                   f"{t['write_bytes_per_launch'] / 1e6:.3f} |")
+    return "\n".join(out)
+
+
 def trace_table(d):
     rows = list(csv.DictReader(open(_one(d, "kernel_stats.csv"))))
     out = ["| Kernel | Calls | Average ns | Min ns | Max ns |", "|---|---|---|---|---|"]
@@ -140,6 +188,9 @@ def main():
     c = sub.add_parser("counters")
     c.add_argument("dir")
     c.add_argument("log")
+    y = sub.add_parser("layers")
+    y.add_argument("dir")
+    y.add_argument("workloads", nargs="+")
     a = ap.parse_args()
     if a.cmd == "traffic":
         wl, e = traffic(a.fetch_dir, a.write_dir)
@@ -156,13 +207,11 @@ def main():
     elif a.cmd == "trace":
         print(trace_table(a.dir))
         if a.log:
-            line = _bench_line(a.log)
-            skip = line["spinup_calls"] + line["warmup"]
-            durs = trace_durations(a.dir)
-            name = max((n for n in durs if is_conv_kernel(n)), key=lambda n: len(durs[n]))
-            v = durs[name][skip:skip + line["steps"]]
+            name, v = timed_trace_ns(a.dir, _bench_line(a.log))
             print(f"\n`{name[:120]}`: {len(v)} timed dispatches, median {statistics.median(v):.0f} ns, "
                   f"mean {statistics.mean(v):.0f} ns, min {min(v)} ns")
+    elif a.cmd == "layers":
+        print(layers_table(a.dir, a.workloads))
     else:
         line = _bench_line(a.log)
         name, timed = timed_conv(dispatch_counters(a.dir), line)

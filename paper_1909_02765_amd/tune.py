@@ -9,7 +9,9 @@ The table maps an exact shape (C_in, H, W, C_out, K, stride, pad) to a variant
 name and a split count; shapes not in it fall back to the cost model.  With
 --prepacked the sweep times every plan on weights prepacked for it, and
 --emit --prepacked writes csrc/tuned_plans_prepacked.inc, the table behind
-ilpm_conv2d_plan_prepacked.
+ilpm_conv2d_plan_prepacked.  With --pooled the calls carry the ReLU + 2x2
+max-pool epilogue (tables tuned_plans_pooled*.inc, behind
+ilpm_conv2d_plan_for and the epilogue call's default plan).
 """
 from __future__ import annotations
 
@@ -23,6 +25,15 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 INC = os.path.join(PKG, "csrc", "tuned_plans.inc")
 INC_PREPACKED = os.path.join(PKG, "csrc", "tuned_plans_prepacked.inc")
+INC_POOLED = os.path.join(PKG, "csrc", "tuned_plans_pooled.inc")
+INC_POOLED_PREPACKED = os.path.join(PKG, "csrc", "tuned_plans_pooled_prepacked.inc")
+EPI_POOL = 3  # ReLU + 2x2 max-pool
+
+
+def table_path(prepacked, pooled):
+    if pooled:
+        return INC_POOLED_PREPACKED if prepacked else INC_POOLED
+    return INC_PREPACKED if prepacked else INC
 
 SPLITS = (1, 2, 3, 4, 6, 8, 12, 16, 24, 32, 48, 64)
 FINALISTS = 4
@@ -62,13 +73,19 @@ def candidate_plans(ilpm, shape):
     return plans
 
 
-def call_args(ilpm, bufs, shape, plan, stream):
+def call_args(ilpm, bufs, shape, plan, stream, epilogue=0):
     """(entry point, arguments) of one call of `plan`: ilpm_conv2d_fwd_plan on
     the OIHW weights, or ilpm_conv2d_fwd_prepacked when bufs carries packed
-    weights (x, w, out, packed)."""
+    weights (x, w, out, packed); with an epilogue, the epilogue entry points
+    (out then has the epilogue's shape)."""
     c_in, h, w, c_out, k, s, p = shape
     x, wt, out = bufs[:3]
     packed = bufs[3] if len(bufs) > 3 else None
+    if epilogue:
+        src = packed if packed is not None else wt
+        fn = ilpm.lib.ilpm_conv2d_fwd_prepacked_epilogue if packed is not None else ilpm.lib.ilpm_conv2d_fwd_epilogue
+        return fn, (ctypes.c_void_p(x.data_ptr()), ctypes.c_void_p(src.data_ptr()), None, c_in, h, w, c_out, k, s, p,
+                    epilogue, ctypes.byref(plan), ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(stream))
     if packed is None:
         return ilpm.lib.ilpm_conv2d_fwd_plan, (
             ctypes.c_void_p(x.data_ptr()), ctypes.c_void_p(wt.data_ptr()), None, c_in, h, w, c_out, k, s, p,
@@ -78,8 +95,8 @@ def call_args(ilpm, bufs, shape, plan, stream):
         ctypes.byref(plan), ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(stream))
 
 
-def time_plan(torch, ilpm, bufs, shape, plan, reps):
-    f, args = call_args(ilpm, bufs, shape, plan, torch.cuda.current_stream().cuda_stream)
+def time_plan(torch, ilpm, bufs, shape, plan, reps, epilogue=0):
+    f, args = call_args(ilpm, bufs, shape, plan, torch.cuda.current_stream().cuda_stream, epilogue)
     for _ in range(3):
         rc = f(*args)
         if rc != 0:
@@ -94,13 +111,13 @@ def time_plan(torch, ilpm, bufs, shape, plan, reps):
     return e0.elapsed_time(e1) * 1000.0 / reps
 
 
-def time_plan_graph(torch, ilpm, bufs, shape, plan, reps, per_graph=20):
+def time_plan_graph(torch, ilpm, bufs, shape, plan, reps, epilogue=0, per_graph=20):
     """Mean us per call with the calls replayed from a captured HIP graph:
     the kernels' own rate, without the host's launch cost between calls
     (which bounds eager timing of the smallest layers)."""
     stream = torch.cuda.Stream()
     stream.wait_stream(torch.cuda.current_stream())
-    f, args = call_args(ilpm, bufs, shape, plan, stream.cuda_stream)
+    f, args = call_args(ilpm, bufs, shape, plan, stream.cuda_stream, epilogue)
     with torch.cuda.stream(stream):
         for _ in range(3):
             rc = f(*args)
@@ -137,7 +154,7 @@ def spin_up(torch, ms=300.0):
         torch.cuda.synchronize()
 
 
-def sweep(shapes, reps=100, graph=False, prepacked=False):
+def sweep(shapes, reps=100, graph=False, prepacked=False, pooled=False):
     import torch
     import paper_1909_02765_amd as ilpm
     torch.cuda.set_device(0)
@@ -149,7 +166,9 @@ def sweep(shapes, reps=100, graph=False, prepacked=False):
         ho, wo = ilpm.out_size(h, k, s, p), ilpm.out_size(w, k, s, p)
         x = torch.rand((1, c_in, h, w), device="cuda")
         wt = torch.randn((c_out, c_in, k, k), device="cuda") * 0.05
-        out = torch.empty((1, c_out, ho, wo), device="cuda")
+        epi = EPI_POOL if pooled else 0
+        out = torch.empty(ilpm.epilogue_out_shape(c_out, h, w, k, s, p, epi) if pooled else (1, c_out, ho, wo),
+                          device="cuda")
         rows = []
         packs = {}
         for plan in candidate_plans(ilpm, shape):
@@ -159,7 +178,7 @@ def sweep(shapes, reps=100, graph=False, prepacked=False):
             if prepacked:
                 packs[id(plan)] = ilpm.prepack_weights(wt, plan)
                 bufs = (x, wt, out, packs[id(plan)])
-            us = timer(torch, ilpm, bufs, shape, plan, reps)
+            us = timer(torch, ilpm, bufs, shape, plan, reps, epi)
             rows.append(({"variant": ilpm.variant_name(plan.path, plan.variant), "path": plan.path,
                           "splits": plan.splits, "us": round(us, 3)}, plan))
         rows.sort(key=lambda r: r[0]["us"])
@@ -172,12 +191,12 @@ def sweep(shapes, reps=100, graph=False, prepacked=False):
         for _ in range(3):
             for row, plan in finalists:
                 bufs = (x, wt, out, packs[id(plan)]) if prepacked else (x, wt, out)
-                us = timer(torch, ilpm, bufs, shape, plan, reps * 10)
+                us = timer(torch, ilpm, bufs, shape, plan, reps * 10, epi)
                 row["us_refined"] = round(min(row["us_refined"], us), 3)
         finalists.sort(key=lambda r: r[0]["us_refined"])
         ranked = [row for row, _ in finalists + rows[FINALISTS:]]
         key = ",".join(str(v) for v in shape)
-        result[key] = {"best": ranked[0], "top": ranked[:8], "prepacked": prepacked}
+        result[key] = {"best": ranked[0], "top": ranked[:8], "prepacked": prepacked, "pooled": pooled}
         print(key, ranked[0], flush=True)
         del packs
     return result
@@ -239,8 +258,11 @@ def emit(table, path=INC):
         b = choose(v, current.get(key))
         us = b.get("us_refined", b["us"])
         rows[key] = "{%s, \"%s\", %d},  // %.2f us" % (key.replace(",", ", "), b["variant"], b["splits"], us)
-    what = ("with prepacked weights (written by tune.py --emit --prepacked)" if path == INC_PREPACKED
-            else "(written by tune.py --emit)")
+    what = {INC_PREPACKED: "with prepacked weights (written by tune.py --emit --prepacked)",
+            INC_POOLED: "with the ReLU + 2x2 max-pool epilogue (written by tune.py --emit --pooled)",
+            INC_POOLED_PREPACKED: "with prepacked weights and the ReLU + 2x2 max-pool epilogue "
+                                  "(written by tune.py --emit --pooled --prepacked)"}.get(
+        path, "(written by tune.py --emit)")
     lines = ["// {C_in, H, W, C_out, K, stride, pad, \"variant\", splits}",
              "// Fastest measured plan per shape on one MI355X " + what + "."]
     for key in sorted(rows, key=lambda k: [int(t) for t in k.split(",")]):
@@ -260,17 +282,20 @@ def main():
                     help="time calls replayed from a HIP graph (for launch-bound layers)")
     ap.add_argument("--prepacked", action="store_true",
                     help="time plans on prepacked weights / emit the prepacked table")
+    ap.add_argument("--pooled", action="store_true",
+                    help="time plans with the ReLU + 2x2 max-pool epilogue / emit the pooled table")
     args = ap.parse_args()
     if args.emit:
         with open(args.emit) as f:
             table = json.load(f)
-        if any(v.get("prepacked", False) != args.prepacked for v in table.values()):
-            raise SystemExit("the sweep's weight layout does not match --prepacked")
-        emit(table, INC_PREPACKED if args.prepacked else INC)
+        if any(v.get("prepacked", False) != args.prepacked or v.get("pooled", False) != args.pooled
+               for v in table.values()):
+            raise SystemExit("the sweep's weight layout or epilogue does not match --prepacked / --pooled")
+        emit(table, table_path(args.prepacked, args.pooled))
         return
     shapes = ([tuple(int(t) for t in sh.split(",")) for sh in args.shapes] if args.shapes
               else default_shapes())
-    table = sweep(shapes, args.reps, args.graph, args.prepacked)
+    table = sweep(shapes, args.reps, args.graph, args.prepacked, args.pooled)
     if args.out:
         with open(args.out, "w") as f:
             json.dump(table, f, indent=1)

@@ -438,3 +438,26 @@ def test_launcher_object_keeps_and_reports():
     del ok
     gc.collect()
     assert ref() is None
+
+
+def test_plan_for_layouts_and_epilogues():
+    """ilpm_conv2d_plan_for: no epilogue / OIHW is ilpm_conv2d_plan, prepacked is
+    ilpm_conv2d_plan_prepacked; a pooled epilogue takes the pooled table's
+    plan (VGG conv4_3: 512->512 at 28x28), ReLU alone does not; bad epilogue
+    bits or layouts are refused (host only)."""
+    shape = (512, 28, 28, 512, 3, 1, 1)
+    same = lambda a, b: a.as_dict() == b.as_dict()
+    assert same(ilpm.plan_for(*shape), ilpm.plan(*shape))
+    assert same(ilpm.plan_for(*shape, prepacked=True), ilpm.plan_prepacked(*shape))
+    assert same(ilpm.plan_for(*shape, epilogue=ilpm.EPI_RELU), ilpm.plan(*shape))
+    pooled = ilpm.plan_for(*shape, epilogue=ilpm.EPI_RELU | ilpm.EPI_MAXPOOL2)
+    tables = {}
+    for name in ("tuned_plans_pooled.inc",):
+        for line in open(os.path.join(os.path.dirname(ilpm.__file__), "csrc", name)):
+            if line.startswith("{512, 28, 28, 512, 3, 1, 1,"):
+                tables[name] = line.split('"')[1], int(line.split('"')[2].strip(" ,}").split("}")[0])
+    variant, splits = tables["tuned_plans_pooled.inc"]
+    assert ilpm.variant_name(pooled.path, pooled.variant) == variant and pooled.splits == splits
+    out = ilpm.ilpm_plan()
+    for epi, packed in ((4, 0), (0, 2), (0, -1)):
+        assert ilpm.lib.ilpm_conv2d_plan_for(*shape, epi, packed, ctypes.byref(out)) == ilpm.ERR_INVALID_ARG

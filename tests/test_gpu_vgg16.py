@@ -11,9 +11,9 @@ the GPU layer consumed.
   oracle's conv -> ReLU (-> pool) of that layer's GPU input, within the
   tolerance of the window element the maximum comes from (ReLU and max are
   1-Lipschitz, so the largest tolerance in a window bounds the difference).
-* Fused on prepacked weights: the same with ilpm_conv2d_plan_prepacked's
-  plans and ilpm_conv2d_fwd_prepacked_epilogue, as the benchmark's
-  prepacked stack runs it."""
+* Fused on prepacked weights: the same with ilpm_conv2d_plan_for's plans
+  (prepacked, per epilogue) and ilpm_conv2d_fwd_prepacked_epilogue, as the
+  benchmark's prepacked stack runs it."""
 import numpy as np
 import pytest
 
@@ -66,7 +66,7 @@ def test_vgg16_fused_stack_against_oracle():
     for name, ci, co, hw, pool, seed in workloads.vgg16_layers():
         w_np = workloads.vgg16_weights(ci, co, seed)
         epi = ilpm.EPI_RELU | (ilpm.EPI_MAXPOOL2 if pool else 0)
-        plan = ilpm.plan(ci, hw, hw, co, 3, 1, 1)
+        plan = ilpm.plan_for(ci, hw, hw, co, 3, 1, 1, epi)
         note(f"[vgg16 fused] {name} {ci}->{co} @{hw} epi={epi} path={plan.path} "
              f"v={ilpm.variant_name(plan.path, plan.variant)} splits={plan.splits}")
         y = torch.empty(ilpm.epilogue_out_shape(co, hw, hw, 3, 1, 1, epi), device="cuda", dtype=torch.float32)
@@ -107,7 +107,7 @@ def test_vgg16_fused_prepacked_stack_against_oracle():
     for name, ci, co, hw, pool, seed in workloads.vgg16_layers():
         w_np = workloads.vgg16_weights(ci, co, seed)
         epi = ilpm.EPI_RELU | (ilpm.EPI_MAXPOOL2 if pool else 0)
-        plan = ilpm.plan_prepacked(ci, hw, hw, co, 3, 1, 1)
+        plan = ilpm.plan_for(ci, hw, hw, co, 3, 1, 1, epi, prepacked=True)
         packed = ilpm.prepack_weights(dev(w_np), plan)
         note(f"[vgg16 fused prepacked] {name} {ci}->{co} @{hw} epi={epi} path={plan.path} "
              f"v={ilpm.variant_name(plan.path, plan.variant)} splits={plan.splits}")
