@@ -66,25 +66,31 @@ def roofline_floor_us(flops, nbytes):
 
 
 def kernel_source_digest():
+    """sha256 (first 16 hex digits) of the kernel and library sources under
+    csrc/, the measured plan tables (tuned_plans*.inc) left out: those choose
+    among the kernels without changing any, and a traffic entry names the
+    plan it was measured on."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_1909_02765_amd", "csrc")
     for name in sorted(os.listdir(csrc)):
+        if name.startswith("tuned_plans") and name.endswith(".inc"):
+            continue
         with open(os.path.join(csrc, name), "rb") as f:
             h.update(name.encode())
             h.update(f.read())
     return h.hexdigest()[:16]
 
 
-def measured_traffic(workload, digest):
+def measured_traffic(workload, digest, plan_name):
     """HBM bytes per launch from the committed counter summary, if it was taken
-    on the current kernel sources; else None."""
+    on the current kernel sources and the plan that runs now; else None."""
     try:
         with open(TRAFFIC_FILE) as f:
             t = json.load(f)
     except (OSError, ValueError):
         return None
     e = t.get(workload)
-    if not e or e.get("kernel_digest") != digest:
+    if not e or e.get("kernel_digest") != digest or e.get("plan") != plan_name:
         return None
     return e.get("hbm_bytes_per_launch")
 
@@ -423,7 +429,8 @@ def main():
         roof = {"bound": "hbm", "achieved": round(r["nbytes"] / (us * 1e-6) / 1e9, 1),
                 "peak": PEAK_HBM_GBS, "unit": "GB/s"}
     roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
-    roof["traffic"] = measured_traffic(case.name, digest)
+    roof["traffic"] = measured_traffic(case.name, digest,
+                                       ilpm.variant_name(r["plan"].path, r["plan"].variant) + f" x{r['plan'].splits}")
     roof["algorithmic_bytes"] = int(r["nbytes"])
     roof["floor_us"] = round(floor_us, 3)
     roof["kernel_digest"] = digest
