@@ -244,6 +244,17 @@ struct Cfg {
     // LDS for the cross-wave sum of the NWK partial accumulators.
     static constexpr int RED = (NWK - 1) * NWC * NWP * MA * NB * 4 * 64;
     static constexpr int BUF0 = cmax(SBUF, RED);
+    // The last stage streamed: computed a group of SGB pixel blocks at a time
+    // (see compute_stage_streamed).  With the input channels split over
+    // waves (NWK > 1) and more than one group, each group's partials are
+    // summed across the waves as soon as the group is done (SSPLIT), through
+    // an LDS area of their own (the stage buffer is still being read),
+    // double-buffered by group: SSLOTS block slots (the group's blocks and,
+    // with group 0, the tail's) per wave and group.
+    static constexpr int SGB = NBM >= 9 ? 3 : 4;
+    static constexpr bool SSPLIT = NWK > 1 && NBM > SGB;
+    static constexpr int SSLOTS = SGB + (TAIL4 ? 1 : 0);
+    static constexpr int PARKS = SSPLIT ? 2 * (NWK - 1) * NWC * NWP * MA * SSLOTS * 4 * 64 : 0;
     // Progressive first stage (PF): the first stage's halo goes to buffers of
     // its own, one per group of four channels (GSZ words each), and its
     // weights to registers group by group, so that its matrix work starts
@@ -254,7 +265,8 @@ struct Cfg {
     static_assert(!PF || (QUAD && NW == 4 && NWK == 1 && MA == 1 && !WL && NBUF == 2 && G4 >= 2 && G4 <= 4),
                   "progressive first stage: four-row halo DMA, one channel group per wave, two buffers");
     static constexpr int GSZ = 4 * PL;
-    static constexpr int LDS_BYTES = (BUF0 + (NBUF - 1) * SBUF + (PF ? G4 * GSZ : 0)) * 4;
+    static constexpr int LDS_BYTES = (BUF0 + (NBUF - 1) * SBUF + (PF ? G4 * GSZ : 0) + PARKS) * 4;
+    static_assert(!SSPLIT || (NBUF == 2 && NWP == 1), "the streamed split last stage follows a two-buffer loop");
     static_assert(CC % (4 * NWK) == 0, "a stage holds whole groups of 4 channels per wave");
     static_assert(LDS_BYTES <= 160 * 1024, "LDS budget of one compute unit");
     static_assert(NT <= 1024, "workgroup size");
@@ -267,7 +279,8 @@ struct Cfg {
     // fit in LDS beside the stage buffers.
     static constexpr bool POOL = false;
     static constexpr int POOL_FLOATS = COT * NPIX;
-    static constexpr bool POOLABLE = TH % 2 == 0 && TW % 2 == 0 && LDS_BYTES + 4 * POOL_FLOATS <= 160 * 1024;
+    static constexpr bool POOLABLE =
+        TH % 2 == 0 && TW % 2 == 0 && LDS_BYTES - 4 * PARKS + 4 * POOL_FLOATS <= 160 * 1024;
 };
 
 // The same configuration for split plans whose tiles sum their own partial
@@ -1142,7 +1155,7 @@ __device__ __forceinline__ void compute_stage_streamed(const float *xl, const AS
                                                        const Epilogue<C> &ep)
 {
     constexpr int kSteps = C::KK * C::G4;
-    constexpr int GB = C::NBM >= 9 ? 3 : 4;
+    constexpr int GB = C::SGB;
     constexpr int kGroups = (C::NBM + GB - 1) / GB;  // 16x16x4 groups
     static_assert(!C::TAIL4 || kGroups > 0, "the tail burst follows group 0");
     // Stores of one group, and of the tail (stored with group 0).
@@ -1233,6 +1246,156 @@ __device__ __forceinline__ void compute_stage_streamed(const float *xl, const AS
     for (int i = 0; i < kDeferred; ++i) store_item(kGroups - 1, i);
 }
 
+// LDS writes of this wave done, then every wave: a bare barrier (the global
+// stores in flight need not complete, and __syncthreads() would wait for
+// them).  The empty asm statements keep the compiler from moving memory
+// accesses across.
+__device__ __forceinline__ void lds_barrier()
+{
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0); vmcnt and expcnt left at their maxima
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+// The last stage streamed with the input channels split over waves
+// (Cfg::SSPLIT): as compute_stage_streamed, group by group, but after each
+// group (for group 0 with the tail burst, folded) the waves wk > 0 park the
+// group's partial accumulators in `park` (double-buffered by group), one
+// barrier, and the waves wk = 0 add them in wk order -- the order and sums
+// of the unstreamed cross-wave sum, so the results are the same bits -- and
+// store the group's outputs a few per step during the next group.  A
+// group's park slot is written again two groups later, after the barrier
+// that the readers reach only once they have read it.
+template <class C, int RELU>
+__device__ __forceinline__ void compute_stage_streamed_split(const float *xl, const AStage<C> &A,
+                                                             const int (&b_base)[C::NB],
+                                                             floatx4 (&acc)[C::MA][C::NACC], float *park, int wave,
+                                                             int wk, int lane, const Epilogue<C> &ep)
+{
+    constexpr int kSteps = C::KK * C::G4;
+    constexpr int GB = C::SGB;
+    constexpr int kGroups = (C::NBM + GB - 1) / GB;
+    constexpr int kGroupStores = C::MA * GB * 4;
+    constexpr int kTailStores = C::TAIL4 ? C::MA * 4 : 0;
+    constexpr int kDeferred = kGroupStores + kTailStores;
+    constexpr int kStoreRate = (kDeferred + kSteps - 1) / kSteps;
+    constexpr int DS = 2;
+    constexpr int kWaveSlots = C::MA * C::SSLOTS * 4 * 64;  // floats per wave and group
+    constexpr int kWaves = C::NWC * C::NWP;
+    const int wcp = wave % kWaves;
+    float bv[DS + 1][GB];
+    float avs[C::WL ? C::MA : 1][C::WL ? C::G4 : 1][C::WL ? C::KK : 1];
+    if constexpr (C::WL) load_stage_a<C>(xl, A, avs);
+    float tb[C::TAIL4 ? kSteps : 1];
+    auto read = [&](int grp, int st, float(&dst)[GB]) {
+        const int t = st / C::G4, c4 = st % C::G4;
+        const int kh = t / C::KS, kw = t % C::KS;
+        const int off = 4 * C::NWK * c4 * C::PL + kh * C::HCP + kw;
+#pragma unroll
+        for (int j = 0; j < GB; ++j) {
+            const int n = grp * GB + j;
+            if (n < C::NBM) dst[j] = xl[b_base[n] + off];
+        }
+        if (C::TAIL4 && grp == 0) tb[st] = xl[b_base[C::NB - 1] + off];
+    };
+    auto store_item = [&](int grp, int i) {
+        if (i < kGroupStores) {
+            const int m = i / (GB * 4), j = (i / 4) % GB, r = i % 4;
+            const int n = grp * GB + j;
+            if (n < C::NBM) ep.template store_one<RELU>(m, n, r, acc[m][n][r]);
+        } else if (C::TAIL4 && grp == 0 && i < kDeferred) {
+            const int m = (i - kGroupStores) / 4, r = (i - kGroupStores) % 4;
+            ep.template store_tail_one<RELU>(m, r, acc[m][C::NB - 1][r]);
+        }
+    };
+    // Block slot j of group grp (j = GB: the tail, group 0 only).
+    auto block_of = [&](int grp, int j) { return j < GB ? grp * GB + j : C::NB - 1; };
+    auto slot_used = [&](int grp, int j) {
+        return j < GB ? grp * GB + j < C::NBM : (C::TAIL4 && grp == 0);
+    };
+    auto sum_group = [&](int grp) {
+        float *const buf = park + (grp & 1) * (C::NWK - 1) * kWaves * kWaveSlots;
+        if (wk > 0) {
+            float *dst = buf + ((wk - 1) * kWaves + wcp) * kWaveSlots + lane;
+#pragma unroll
+            for (int m = 0; m < C::MA; ++m)
+#pragma unroll
+                for (int j = 0; j < C::SSLOTS; ++j)
+                    if (slot_used(grp, j)) {
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) dst[((m * C::SSLOTS + j) * 4 + r) * 64] = acc[m][block_of(grp, j)][r];
+                    }
+        }
+        lds_barrier();
+        if (wk == 0) {
+#pragma unroll
+            for (int k = 1; k < C::NWK; ++k) {
+                const float *src = buf + ((k - 1) * kWaves + wcp) * kWaveSlots + lane;
+#pragma unroll
+                for (int m = 0; m < C::MA; ++m)
+#pragma unroll
+                    for (int j = 0; j < C::SSLOTS; ++j)
+                        if (slot_used(grp, j)) {
+#pragma unroll
+                            for (int r = 0; r < 4; ++r)
+                                acc[m][block_of(grp, j)][r] += src[((m * C::SSLOTS + j) * 4 + r) * 64];
+                        }
+            }
+        }
+    };
+#pragma unroll
+    for (int i = 0; i < DS && i < kGroups * kSteps; ++i) read(i / kSteps, i % kSteps, bv[i]);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int grp = 0; grp < kGroups; ++grp) {
+#pragma unroll
+        for (int st = 0; st < kSteps; ++st) {
+            const int t = st / C::G4, c4 = st % C::G4;
+            const int lin = grp * kSteps + st, cur = lin % (DS + 1), ahead = lin + DS;
+            if (ahead < kGroups * kSteps) read(ahead / kSteps, ahead % kSteps, bv[ahead % (DS + 1)]);
+#pragma unroll
+            for (int m = 0; m < C::MA; ++m)
+#pragma unroll
+                for (int j = 0; j < GB; ++j) {
+                    const int n = grp * GB + j;
+                    if (n < C::NBM) {
+                        float a_op;
+                        if constexpr (C::WL) a_op = avs[m][c4][t];
+                        else a_op = A.v[m][c4][t];
+                        acc[m][n] = __builtin_amdgcn_mfma_f32_16x16x4f32(a_op, bv[cur][j], acc[m][n], 0, 0, 0);
+                    }
+                }
+            if (grp > 0 && wk == 0) {
+#pragma unroll
+                for (int k = 0; k < kStoreRate; ++k) store_item(grp - 1, st * kStoreRate + k);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        if (C::TAIL4 && grp == 0) {
+#pragma unroll
+            for (int st = 0; st < kSteps; ++st) {
+                const int t = st / C::G4, c4 = st % C::G4;
+#pragma unroll
+                for (int m = 0; m < C::MA; ++m) {
+                    float a_op;
+                    if constexpr (C::WL) a_op = avs[m][c4][t];
+                    else a_op = A.v[m][c4][t];
+                    acc[m][C::NB - 1 + st % 4] =
+                        __builtin_amdgcn_mfma_f32_4x4x1f32(a_op, tb[st], acc[m][C::NB - 1 + st % 4], 0, 0, 0);
+                }
+            }
+            fold_tail<C>(acc);
+        }
+        sum_group(grp);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    if (wk == 0) {
+#pragma unroll
+        for (int i = 0; i < kDeferred; ++i) store_item(kGroups - 1, i);
+    }
+}
+
 // The last stage and the output.  NWK = 1: streamed.  NWK > 1: compute, then
 // sum the NWK channel-group partials (waves wk > 0 park theirs in LDS once
 // every wave is past the last stage, waves wk = 0 add and store).
@@ -1247,6 +1410,10 @@ __device__ __forceinline__ void final_stage(const float *xl, const AStage<C> &A,
         // matrix instructions.
         if (ep.relu) compute_stage_streamed<C, 2>(xl, A, b_base, acc, ep);
         else compute_stage_streamed<C, 1>(xl, A, b_base, acc, ep);
+    } else if constexpr (C::SSPLIT && !C::POOL) {
+        // park_area is the streamed split's own LDS area here (Cfg::PARKS).
+        if (ep.relu) compute_stage_streamed_split<C, 2>(xl, A, b_base, acc, park_area, wave, wk, lane, ep);
+        else compute_stage_streamed_split<C, 1>(xl, A, b_base, acc, park_area, wave, wk, lane, ep);
     } else if constexpr (C::NWK == 1) {
         // PoolTile: the results go to LDS, whose queue the matrix steps'
         // operand reads use; written in one burst after the stage instead of
@@ -1537,6 +1704,8 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
     __shared__ __attribute__((aligned(16))) float gb3[kPF && C::G4 > 3 ? C::GSZ : 1];
     __shared__ unsigned last_arrival[1];  // fused split sum: this workgroup completes its tile
     __shared__ __attribute__((aligned(16))) float pool_lds[C::POOL ? C::POOL_FLOATS : 1];  // PoolTile's tile
+    constexpr bool kStreamSplit = C::SSPLIT && !C::POOL;
+    __shared__ __attribute__((aligned(16))) float park_s[kStreamSplit ? C::PARKS : 1];  // streamed split sums
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -1695,11 +1864,11 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
             first_stage<C>(gb, rx0, ws0, a0, xo, wave, b_base, acc, next);
         }
         stage_ready();
-        stage_loop<C, WS>(lds1, a1, lds0, a0, lds0, c_begin + 1, c_end, x, a, wctx, wave, wk, lane, xo, b_base,
-                          acc, ep);
+        stage_loop<C, WS>(lds1, a1, lds0, a0, kStreamSplit ? park_s : lds0, c_begin + 1, c_end, x, a, wctx, wave,
+                          wk, lane, xo, b_base, acc, ep);
     } else {
-        stage_loop<C, WS>(lds0, a0, lds1, a1, lds0, c_begin, c_end, x, a, wctx, wave, wk, lane, xo, b_base, acc,
-                          ep);
+        stage_loop<C, WS>(lds0, a0, lds1, a1, kStreamSplit ? park_s : lds0, c_begin, c_end, x, a, wctx, wave, wk,
+                          lane, xo, b_base, acc, ep);
     }
     if constexpr (C::FUSED) finish_split_tile<C>(a, part, out, tile, co0, oh0, ow0, last_arrival);
     if constexpr (C::POOL) pool_tile_finish<C>(pool_lds, out, a, co0, oh0, ow0);
