@@ -23,6 +23,7 @@ namespace ilpm {
 namespace {
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void *lds_ptr_t;
 
 constexpr int kTileH = 8;
 constexpr int kTileW = 32;
@@ -322,6 +323,214 @@ const LowcVariant kLowc[] = {
 constexpr int kNumLowc = sizeof(kLowc) / sizeof(kLowc[0]);
 constexpr int kFirstLowc = 2;  // direct variants 0 and 1 are the VALU kernels
 
+// ---- Low-channel layers, whole row segments per workgroup ----
+//
+// The same contraction as conv_direct_mfma -- k = 4s + g, accumulators
+// starting from the bias, step s = 0, 1, ... in order -- so the two give the
+// same bits; cut differently.  A workgroup takes one segment of 16*NB*PW
+// consecutive pixels of one output row, for a group of 16*CW output channels
+// (waves (pw, cw): wave pw's NB blocks of 16 pixels, channels 16*cw..), and
+// first copies the C_in*K input rows that segment reads into LDS by buffer
+// DMA (zeros for padding rows and columns), then reads every B operand from
+// there.  Its stores cover whole pieces of 16 consecutive pixels of a row, so
+// where the row length is a multiple of 16 floats each lane group writes one
+// aligned 64-byte piece.  (On MI355X a write-only kernel storing VGG-16's
+// first-layer output, 12.85 MB, in such pieces ran at 3.8 us per launch, as
+// fast as a linear copy; in the 14-pixel pieces of 14x14 tiles, 5.7 us.)
+// Each pair of blocks is stored once its matrix instructions are issued, so
+// the stores stream behind the matrix work.
+//
+// LDS: row r = ci*K + kh holds input columns ix0 .. ix0 + lw - 1 of input
+// row oy*S - pad + kh at r*lwp (lwp = 64 * ceil(lw / 64), one DMA of 64
+// words per wave and chunk); row C_in*K is all zeros and serves the
+// contraction slots k >= C_in*K*K.
+struct RowsArgs {
+    int c_in, h, w, c_out, k, stride, pad, h_out, w_out;
+    int kt;         // C_in*K*K
+    int segs;       // segments per output row
+    int co_groups;  // output-channel groups of 16*CW
+    int lw, lwp, chunks;
+    int relu;
+    unsigned m_kk, m_k;  // ceil(2^16 / (K*K)), ceil(2^16 / K)
+};
+
+template <int NB, int PW, int CW, int STEPS, int POL>
+__global__ __launch_bounds__(256) void conv_direct_rows(const float *__restrict__ x, const float *__restrict__ wt,
+                                                        const float *__restrict__ bias, float *__restrict__ out,
+                                                        RowsArgs a)
+{
+    extern __shared__ float xl[];
+    constexpr unsigned kFar = 0x80000000u;  // past every descriptor's range
+    constexpr int kNI = 2;                  // blocks whose matrix chains are interleaved
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int g = lane >> 4, l = lane & 15;
+    // Contiguous runs of units per XCD (workgroup i runs on XCD i mod 8), so
+    // that neighbouring rows -- which read the same input rows -- meet in one
+    // L2.  Unit order: channel group fastest, then segment, then row.
+    const int nwg = (int)gridDim.x;
+    const int xcd = (int)blockIdx.x % 8, slot = (int)blockIdx.x / 8;
+    const int per = nwg / 8, extra = nwg % 8;
+    const int lin = xcd * per + min(xcd, extra) + slot;
+    const int cgi = lin % a.co_groups;
+    const int rest = lin / a.co_groups;
+    const int seg = rest % a.segs;
+    const int oy = rest / a.segs;
+    const int px0 = seg * 16 * NB * PW;
+    const int ix0 = px0 * a.stride - a.pad, iy0 = oy * a.stride - a.pad;
+    const int rows = a.c_in * a.k;
+
+    const __amdgpu_buffer_rsrc_t rx = lowc_rsrc(x, (unsigned)a.c_in * a.h * a.w * 4u);
+    const __amdgpu_buffer_rsrc_t rw = lowc_rsrc(wt, (unsigned)a.c_out * a.kt * 4u);
+    const __amdgpu_buffer_rsrc_t ro = lowc_rsrc(out, (unsigned)a.c_out * a.h_out * a.w_out * 4u);
+
+    const int pw = wave % PW, cw = wave / PW;
+    const bool active = wave < PW * CW;
+    const int co0 = (cgi * CW + cw) * 16;
+    // A: this lane's weights w[co0 + l][4s + g], in flight during the DMA.
+    float av[STEPS];
+#pragma unroll
+    for (int s = 0; s < STEPS; ++s) {
+        const int k = 4 * s + g;
+        const unsigned off = (active && co0 + l < a.c_out && k < a.kt) ? (unsigned)((co0 + l) * a.kt + k) * 4u : kFar;
+        av[s] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rw, (int)off, 0, 0));
+    }
+    // Bias (the accumulators' start), also in flight during the DMA.
+    float b4[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int co = co0 + 4 * g + r;
+        b4[r] = (bias != nullptr && active && co < a.c_out) ? bias[co] : 0.f;
+    }
+    // Input rows into LDS: wave w issues chunks w, w + 4, ... of the
+    // rows * chunks list (chunk i of row r = input columns ix0 + 64i ..).
+    // (r, i) and r = (ci, kh) advance by counting, without divisions.
+    {
+        int r = 0, i = wave, ci = 0, kh = 0;
+        auto settle = [&]() {
+            while (i >= a.chunks) {
+                i -= a.chunks;
+                ++r;
+                if (++kh == a.k) {
+                    kh = 0;
+                    ++ci;
+                }
+            }
+        };
+        settle();
+        while (r < rows) {
+            const int iy = iy0 + kh;
+            const int j = 64 * i + lane, ix = ix0 + j;
+            const bool ok = j < a.lw && (unsigned)iy < (unsigned)a.h && (unsigned)ix < (unsigned)a.w;
+            const unsigned off = ok ? (unsigned)((ci * a.h + iy) * a.w + ix) * 4u : kFar;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_ptr_t)(xl + r * a.lwp + 64 * i), 4, (int)off, 0, 0, 0);
+            i += 4;
+            settle();
+        }
+    }
+    for (int j = tid; j < a.lwp; j += 256) xl[rows * a.lwp + j] = 0.f;
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's DMA has landed in LDS
+    __syncthreads();
+    if (!active) return;  // no barrier follows
+
+    // LDS word of contraction slot k = 4s + g for the segment's pixel 0.
+    int tb[STEPS];
+#pragma unroll
+    for (int s = 0; s < STEPS; ++s) {
+        const int k = 4 * s + g;
+        const int ci = (int)(((unsigned)k * a.m_kk) >> 16), t = k - ci * a.k * a.k;
+        const int kh = (int)(((unsigned)t * a.m_k) >> 16), kw = t - kh * a.k;
+        tb[s] = k < a.kt ? (ci * a.k + kh) * a.lwp + kw : rows * a.lwp;
+    }
+    const int pl = pw * NB * 16 + l;  // this lane's pixel of block 0, within the segment
+    const int plane = a.h_out * a.w_out;
+    const unsigned obase = (unsigned)(co0 + 4 * g) * (unsigned)plane + (unsigned)(oy * a.w_out + px0 + pl);
+
+#pragma unroll
+    for (int n0 = 0; n0 < NB; n0 += kNI) {
+        floatx4 acc[kNI];
+#pragma unroll
+        for (int u = 0; u < kNI; ++u) acc[u] = floatx4{b4[0], b4[1], b4[2], b4[3]};
+#pragma unroll
+        for (int s = 0; s < STEPS; ++s)
+#pragma unroll
+            for (int u = 0; u < kNI; ++u)
+                if (n0 + u < NB) {
+                    const float bv = xl[tb[s] + (pl + 16 * (n0 + u)) * a.stride];
+                    acc[u] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[s], bv, acc[u], 0, 0, 0);
+                }
+#pragma unroll
+        for (int u = 0; u < kNI; ++u)
+            if (n0 + u < NB) {
+                const bool pix_ok = px0 + pl + 16 * (n0 + u) < a.w_out;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const bool ok = pix_ok && co0 + 4 * g + r < a.c_out;
+                    const unsigned off = ok ? (obase + (unsigned)(r * plane + 16 * (n0 + u))) * 4u : kFar;
+                    float v = acc[u][r];
+                    if (a.relu && v < 0.f) v = 0.f;
+                    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v), ro, (int)off, 0, POL);
+                }
+            }
+    }
+}
+
+struct RowsVariant {
+    const char *name;
+    int nb, pw, cw;
+    void (*launch)(dim3, int, hipStream_t, const float *, const float *, const float *, float *, const RowsArgs &);
+};
+
+template <int NB, int PW, int CW, int POL = 0>
+void rows_launch(dim3 grid, int lds, hipStream_t st, const float *x, const float *w, const float *b, float *o,
+                 const RowsArgs &a)
+{
+    hipLaunchKernelGGL((conv_direct_rows<NB, PW, CW, 7, POL>), grid, dim3(256), lds, st, x, w, b, o, a);
+}
+
+// Store policy SC1 (device scope): the output is written through each XCD's
+// L2 to the level the XCDs share while the kernel runs, instead of being
+// written back from the L2 caches when it ends; for VGG-16's first layer on
+// MI355X that took 0.9 us off ~6.8 us per launch.
+constexpr int kSc1 = 16;
+
+const RowsVariant kRows[] = {
+    {"direct_rows_k28_co64_px224_sc1", 14, 1, 4, &rows_launch<14, 1, 4, kSc1>},
+    {"direct_rows_k28_co64_px112_sc1", 7, 1, 4, &rows_launch<7, 1, 4, kSc1>},
+    {"direct_rows_k28_co64_px32_sc1", 2, 1, 4, &rows_launch<2, 1, 4, kSc1>},
+    {"direct_rows_k28_co16_px32_sc1", 1, 2, 1, &rows_launch<1, 2, 1, kSc1>},
+    {"direct_rows_k28_co64_px224", 14, 1, 4, &rows_launch<14, 1, 4>},
+    {"direct_rows_k28_co64_px112", 7, 1, 4, &rows_launch<7, 1, 4>},
+    {"direct_rows_k28_co64_px64", 4, 1, 4, &rows_launch<4, 1, 4>},
+    {"direct_rows_k28_co32_px128", 4, 2, 2, &rows_launch<4, 2, 2>},
+    {"direct_rows_k28_co64_px32", 2, 1, 4, &rows_launch<2, 1, 4>},
+    {"direct_rows_k28_co64_px16", 1, 1, 4, &rows_launch<1, 1, 4>},
+    {"direct_rows_k28_co32_px32", 1, 2, 2, &rows_launch<1, 2, 2>},
+    {"direct_rows_k28_co16_px64", 1, 4, 1, &rows_launch<1, 4, 1>},
+    {"direct_rows_k28_co16_px32", 1, 2, 1, &rows_launch<1, 2, 1>},
+};
+constexpr int kNumRows = sizeof(kRows) / sizeof(kRows[0]);
+constexpr int kFirstRows = kFirstLowc + kNumLowc;
+constexpr int kRowsLdsFloats = 16384;  // 64 KiB
+
+RowsArgs rows_args(const ConvShape &s, const RowsVariant &d)
+{
+    RowsArgs a;
+    a.c_in = s.c_in; a.h = s.h; a.w = s.w; a.c_out = s.c_out; a.k = s.k;
+    a.stride = s.stride; a.pad = s.pad; a.h_out = s.h_out; a.w_out = s.w_out;
+    a.kt = s.c_in * s.k * s.k;
+    a.segs = ceil_div(s.w_out, 16 * d.nb * d.pw);
+    a.co_groups = ceil_div(s.c_out, 16 * d.cw);
+    a.lw = (16 * d.nb * d.pw - 1) * s.stride + s.k;
+    a.chunks = ceil_div(a.lw, 64);
+    a.lwp = 64 * a.chunks;
+    a.relu = 0;
+    a.m_kk = (65536u + (unsigned)(s.k * s.k) - 1) / (unsigned)(s.k * s.k);
+    a.m_k = (65536u + (unsigned)s.k - 1) / (unsigned)s.k;
+    return a;
+}
+
 DirectArgs make_args(const ConvShape &s)
 {
     DirectArgs a;
@@ -348,13 +557,14 @@ int lds_chunk(const ConvShape &s)
 
 }  // namespace
 
-int direct_num_variants() { return kFirstLowc + kNumLowc; }
+int direct_num_variants() { return kFirstRows + kNumRows; }
 
 const char *direct_variant_name(int v)
 {
     if (v == 0) return "direct_lds_t8x32_co16";
     if (v == 1) return "direct_global";
     if (v >= kFirstLowc && v < kFirstLowc + kNumLowc) return kLowc[v - kFirstLowc].name;
+    if (v >= kFirstRows && v < kFirstRows + kNumRows) return kRows[v - kFirstRows].name;
     return nullptr;
 }
 
@@ -363,6 +573,14 @@ bool direct_variant_info(int v, int *k, int *stride, int *tile_h, int *tile_w, i
     if (v < 0 || v >= direct_num_variants()) return false;
     *k = 0;
     *stride = 0;
+    if (v >= kFirstRows) {
+        // A workgroup's tile: 16*NB*PW consecutive pixels of one output row.
+        const RowsVariant &d = kRows[v - kFirstRows];
+        *tile_h = 1;
+        *tile_w = 16 * d.nb * d.pw;
+        *co_tile = 16 * d.cw;
+        return true;
+    }
     if (v >= kFirstLowc) {
         // A wave's tile: 16*NPB consecutive pixels of the output plane.
         const LowcVariant &d = kLowc[v - kFirstLowc];
@@ -377,9 +595,13 @@ bool direct_variant_info(int v, int *k, int *stride, int *tile_h, int *tile_w, i
     return true;
 }
 
-bool direct_is_lowc(int v) { return v >= kFirstLowc && v < kFirstLowc + kNumLowc; }
+bool direct_is_lowc(int v) { return v >= kFirstLowc && v < kFirstRows + kNumRows; }
 
-int direct_lowc_max_kt(int v) { return direct_is_lowc(v) ? 4 * kLowc[v - kFirstLowc].steps : 0; }
+int direct_lowc_max_kt(int v)
+{
+    if (v >= kFirstRows && v < kFirstRows + kNumRows) return 28;
+    return direct_is_lowc(v) ? 4 * kLowc[v - kFirstLowc].steps : 0;
+}
 
 bool direct_make_plan(const ConvShape &s, int variant, ilpm_plan *p)
 {
@@ -426,6 +648,26 @@ bool direct_make_plan(const ConvShape &s, int variant, ilpm_plan *p)
         q.ci_chunk = s.c_in;
         q.grid = (int)((units + 3) / 4);
         q.lds_bytes = 0;
+    } else if (variant >= kFirstRows && variant < kFirstRows + kNumRows) {
+        const RowsVariant &d = kRows[variant - kFirstRows];
+        const int64_t kt = (int64_t)s.c_in * s.k * s.k;
+        const int64_t plane = (int64_t)s.h_out * s.w_out;
+        // The whole contraction in one run of 7 matrix steps; 31-bit byte
+        // offsets; the input rows and the zero row within 64 KiB of LDS.
+        if (kt > 28) return false;
+        if ((int64_t)s.c_in * s.h * s.w * 4 >= (1LL << 31) || (int64_t)s.c_out * kt * 4 >= (1LL << 31) ||
+            (int64_t)s.c_out * plane * 4 >= (1LL << 31))
+            return false;
+        const RowsArgs a = rows_args(s, d);
+        if ((int64_t)(s.c_in * s.k + 1) * a.lwp > kRowsLdsFloats) return false;
+        const int64_t units = (int64_t)s.h_out * a.segs * a.co_groups;
+        if (units > 0x7fffffffLL) return false;
+        q.tile_h = 1;
+        q.tile_w = 16 * d.nb * d.pw;
+        q.co_tile = 16 * d.cw;
+        q.ci_chunk = s.c_in;
+        q.grid = (int)units;
+        q.lds_bytes = (int)sizeof(float) * (s.c_in * s.k + 1) * a.lwp;
     } else if (variant == 1) {
         const int64_t total = (int64_t)s.c_out * s.h_out * s.w_out;
         const int64_t blocks = (total + kThreads - 1) / kThreads;
@@ -448,6 +690,13 @@ hipError_t direct_launch(const ilpm_plan &p, const ConvShape &s, const float *x,
 {
     DirectArgs a = make_args(s);
     a.relu = relu ? 1 : 0;
+    if (p.variant >= kFirstRows && p.variant < kFirstRows + kNumRows) {
+        const RowsVariant &d = kRows[p.variant - kFirstRows];
+        RowsArgs ra = rows_args(s, d);
+        ra.relu = relu ? 1 : 0;
+        d.launch(dim3(p.grid), p.lds_bytes, stream, x, w, bias, out, ra);
+        return hipGetLastError();
+    }
     if (direct_is_lowc(p.variant)) {
         const LowcVariant &d = kLowc[p.variant - kFirstLowc];
         LowcArgs la;

@@ -121,6 +121,7 @@ int variants_part5(const Variant **table);
 int variants_part6(const Variant **table);
 int variants_part7(const Variant **table);
 int variants_part8(const Variant **table);
+int variants_part9(const Variant **table);
 
 }  // namespace ig
 
@@ -294,6 +295,15 @@ template <class C>
 struct FusedSplit : C {
     static constexpr int SPOL = kPolicyDeviceScope;
     static constexpr bool FUSED = true;
+};
+
+// The same configuration with the output stores at device scope (SC1):
+// written through each XCD's L2 while the kernel runs rather than written
+// back from the L2 caches when it ends, which overlaps moving a large output
+// into memory with the matrix work of the last stage.
+template <class C>
+struct Sc1Out : C {
+    static constexpr int SPOL = kPolicyDeviceScope;
 };
 
 // The same configuration with the 2x2 max-pool epilogue done in the
@@ -1664,6 +1674,10 @@ __device__ __forceinline__ void pool_tile_finish(const float *tile, float *out, 
     constexpr int PH = C::TH / 2, PW = C::TW / 2;
     const int hp = a.h_out / 2, wpo = a.w_out / 2;
     const int pi0 = oh0 / 2, pj0 = ow0 / 2;
+    // With a cache policy on the output (SC1), the stores carry it as the
+    // full-size stores do; the pooled output is below 2^31 bytes (the plan
+    // checks the full-size one).
+    const __amdgpu_buffer_rsrc_t ro = make_rsrc(out, (unsigned)a.c_out * (unsigned)hp * (unsigned)wpo * 4u);
     for (int e = threadIdx.x; e < C::COT * PH * PW; e += C::NT) {
         const int c = e / (PH * PW);
         const int q = e - c * (PH * PW);
@@ -1679,7 +1693,11 @@ __device__ __forceinline__ void pool_tile_finish(const float *tile, float *out, 
         m = v > m ? v : m;
         v = bot.y;
         m = v > m ? v : m;
-        out[((int64_t)co * hp + pi) * wpo + pj] = m;
+        if constexpr (C::SPOL != 0)
+            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, m), ro,
+                                                  (int)((unsigned)((co * hp + pi) * wpo + pj) * 4u), 0, C::SPOL);
+        else
+            out[((int64_t)co * hp + pi) * wpo + pj] = m;
     }
 }
 

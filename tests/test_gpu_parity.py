@@ -454,14 +454,15 @@ def test_low_channel_direct_ragged(ilpm):
     shapes = [(9, 12, 3, 18, 1, 3, 0), (3, 5, 1, 7, 3, 1, 1), (3, 1, 40, 33, 3, 1, 1), (1, 23, 19, 70, 5, 2, 2),
               (2, 17, 29, 64, 3, 2, 0), (7, 9, 11, 20, 3, 1, 1), (1, 13, 13, 5, 7, 3, 3), (28, 6, 6, 40, 1, 1, 0),
               (3, 224, 37, 64, 3, 1, 1)]
-    lowc = [v for v in range(ilpm.num_variants(ilpm.PATH_DIRECT))
-            if ilpm.variant_name(ilpm.PATH_DIRECT, v).startswith("direct_mfma")]
-    assert lowc
+    names = {v: ilpm.variant_name(ilpm.PATH_DIRECT, v) for v in range(ilpm.num_variants(ilpm.PATH_DIRECT))}
+    lowc = [v for v, n in names.items() if n.startswith("direct_mfma") or n.startswith("direct_rows")]
+    assert any(names[v].startswith("direct_rows") for v in lowc)
     for i, (c_in, h, w_, c_out, k, s, p) in enumerate(shapes):
         x, w, b = random_case(4400 + 7 * i, c_in, h, w_, c_out, k, bias=(i % 2 == 0))
         ref, sab = oracle.conv2d_f64(x, w, b, s, p)
         xi, wi, bi = small_int_case(4500 + 7 * i, c_in, h, w_, c_out, k, bias=(i % 2 == 1))
         refi, _ = oracle.conv2d_f64(xi, wi, bi, s, p)
+        first = None
         for v in lowc:
             try:
                 plan = ilpm.plan_variant(c_in, h, w_, c_out, k, s, p, ilpm.PATH_DIRECT, v)
@@ -470,5 +471,12 @@ def test_low_channel_direct_ragged(ilpm):
             note(f"[lowc {i}] {(c_in, h, w_, c_out, k, s, p)} {describe(plan)}")
             got = run_conv(x, w, b, s, p, plan=plan)
             assert_matches(got, ref, sab, c_in, k, f"lowc {i} v{v}")
+            # Every low-channel kernel runs the same matrix-instruction chain
+            # (slots k = 4s + g in order from the bias; slots past C_in*K*K
+            # add zero products), so they agree bit for bit.
+            if first is None:
+                first = (names[v], got)
+            else:
+                np.testing.assert_array_equal(got, first[1], err_msg=f"lowc {i} {names[v]} vs {first[0]}")
             got = run_conv(xi, wi, bi, s, p, plan=plan)
             np.testing.assert_array_equal(got.astype(np.float64), refi, err_msg=f"lowc {i} v{v} small integers")
