@@ -251,8 +251,11 @@ struct Cfg {
     // summed across the waves as soon as the group is done (SSPLIT), through
     // an LDS area of their own (the stage buffer is still being read),
     // double-buffered by group: SSLOTS block slots (the group's blocks and,
-    // with group 0, the tail's) per wave and group.
-    static constexpr int SGB = NBM >= 9 ? 3 : 4;
+    // with group 0, the tail's) per wave and group.  Without that split a
+    // group is one block: its stores start after the first block and trail
+    // the matrix work by one block (VGG-early 64->64 at 224^2 with device-
+    // scope stores: 29.2 us, against 29.9 with groups of three).
+    static constexpr int SGB = NWK > 1 ? (NBM >= 9 ? 3 : 4) : 1;
     static constexpr bool SSPLIT = NWK > 1 && NBM > SGB;
     static constexpr int SSLOTS = SGB + (TAIL4 ? 1 : 0);
     static constexpr int PARKS = SSPLIT ? 2 * (NWK - 1) * NWC * NWP * MA * SSLOTS * 4 * 64 : 0;
@@ -1146,19 +1149,20 @@ struct Epilogue {
 };
 
 // The last stage of a one-channel-group-per-wave plan (NWK = 1), computed in
-// groups of pixel blocks with every step of the stage before moving to the
-// next group, so that the output write overlaps the matrix work instead of
-// following it: a finished group's stores are issued a few per step during
-// the next group's steps, behind the step's matrix instructions.  (Issued
-// in one burst they stall the wave, since
-// every workgroup reaches the same group at about the same time and the
-// burst is HBM-write bound.)  Three or four blocks per group keep that many
-// independent accumulator chains in flight (two were too few: each matrix
-// instruction then waited on its chain's previous one); with twelve blocks,
-// four groups of three leave a quarter fewer stores after the last matrix
-// instruction than three groups of four (measured 0.2 us faster on 14x14
-// tiles).  The 4x4x1 tail block, if any, follows group 0 as one burst on
-// its four accumulators and is stored with group 0.
+// groups of pixel blocks (Cfg::SGB, one block) with every step of the stage
+// before moving to the next group, so that the output write overlaps the
+// matrix work instead of following it: a finished group's stores are issued
+// a few per step during the next group's steps, behind the step's matrix
+// instructions.  (Issued in one burst they stall the wave, since every
+// workgroup reaches the same group at about the same time and the burst is
+// write bound.)  Smaller groups start the stores earlier and leave fewer
+// after the last matrix instruction; a one-block group's chain of dependent
+// 16x16x4 instructions still issues at the matrix pipe's rate.  Measured on
+// 14x14 tiles (12 blocks + tail): groups of 1, 2, 3, 4, 6 and 12 blocks took
+// 29.2, 29.5, 29.9, 30.4, 31.3 and 34.7 us with device-scope output stores,
+// groups of 1 and 3 took 30.1 and 30.3 us with ordinary ones.  The 4x4x1
+// tail block, if any, follows group 0 as one burst on its four accumulators
+// and is stored with group 0.
 template <class C, int RELU>
 __device__ __forceinline__ void compute_stage_streamed(const float *xl, const AStage<C> &A,
                                                        const int (&b_base)[C::NB], floatx4 (&acc)[C::MA][C::NACC],
