@@ -282,6 +282,7 @@ struct Cfg {
     // tile's windows do not cross tiles (even TH, TW) and the tile's outputs
     // fit in LDS beside the stage buffers.
     static constexpr bool POOL = false;
+    static constexpr bool STREAM_POOL = false;
     static constexpr int POOL_FLOATS = COT * NPIX;
     static constexpr bool POOLABLE =
         TH % 2 == 0 && TW % 2 == 0 && LDS_BYTES - 4 * PARKS + 4 * POOL_FLOATS <= 160 * 1024;
@@ -319,6 +320,11 @@ template <class C>
 struct PoolTile : C {
     static_assert(C::POOLABLE, "pooled tiles need even tile sides and LDS room for the tile");
     static constexpr bool POOL = true;
+    // One channel group per wave and every pixel of the tile in each wave:
+    // a wave's rows of the LDS tile are its own, so it pools them as they
+    // fill, during the streamed last stage (see compute_stage_streamed),
+    // with no workgroup barrier.
+    static constexpr bool STREAM_POOL = C::NWK == 1 && C::NWP == 1;
 };
 
 
@@ -1000,6 +1006,10 @@ struct Epilogue {
     // row c); the offsets above then address it in bytes.
     float *pl;
     int pool_co0;
+    // STREAM_POOL: the pooled output, its sizes, this tile's first pooled
+    // row and column, and this wave's first channel row in the LDS tile.
+    __amdgpu_buffer_rsrc_t pro;
+    int pool_hp, pool_wpo, pool_pi0, pool_pj0, pool_wc0;
 
     // RELU: 0 = as the launch says (relu), 1 = no ReLU, 2 = ReLU (the last
     // stage decides once instead of per store).
@@ -1071,13 +1081,19 @@ struct Epilogue {
     // of the tile at byte 4*p, channel co0 + c at byte 4*c*NPIX; pixels
     // outside the image or the tile and channels past C_out keep the
     // out-of-range offset and are not written.
-    __device__ __forceinline__ void pool_init(float *tile, int co0, int co_lane, int wp, int g, int l16, int oh0,
-                                              int ow0, const IgArgs &a)
+    __device__ __forceinline__ void pool_init(float *tile, float *out, int co0, int co_lane, int wp, int g, int l16,
+                                              int oh0, int ow0, const IgArgs &a)
     {
         constexpr unsigned kFar = 1u << 30;
         pl = tile;
         pool_co0 = co0;
         plane_b = 4u * C::NPIX;
+        pool_hp = a.h_out / 2;
+        pool_wpo = a.w_out / 2;
+        pool_pi0 = oh0 / 2;
+        pool_pj0 = ow0 / 2;
+        pool_wc0 = co_lane - 4 * g - co0;
+        pro = make_rsrc(out, (unsigned)a.c_out * (unsigned)pool_hp * (unsigned)pool_wpo * 4u);
         const int rows = a.h_out - oh0, cols = a.w_out - ow0;
 #pragma unroll
         for (int n = 0; n < C::NB; ++n) {
@@ -1097,6 +1113,37 @@ struct Epilogue {
             const int q = p / C::TW, r = p - q * C::TW;
             const bool lane_stores = g == 0 && j < C::TAILP && q < rows && r < cols;
             tail_pix = lane_stores ? 4u * p : kFar;
+        }
+    }
+
+    // STREAM_POOL: pooled row i of this wave's 16*MA channels (tile rows 2i
+    // and 2i + 1), read from the wave's own rows of the LDS tile, which this
+    // wave wrote (LDS instructions of one wave complete in order).  Maxima
+    // in the order pool_tile_finish takes them; windows with a pixel outside
+    // the image have no output (floor) and channels past C_out none.
+    __device__ __forceinline__ void pool_row(int i) const
+    {
+        constexpr int PWo = C::TW / 2, kOut = 16 * C::MA * PWo;
+        const int lane = __lane_id();
+        const int pi = pool_pi0 + i;
+#pragma unroll
+        for (int e0 = 0; e0 < kOut; e0 += 64) {
+            const int e = e0 + lane;
+            const int c = e / PWo, j = e - (e / PWo) * PWo;
+            const int tc = pool_wc0 + c, co = pool_co0 + tc, pj = pool_pj0 + j;
+            if (e < kOut && co < c_out && pi < pool_hp && pj < pool_wpo) {
+                const float2 top = *reinterpret_cast<const float2 *>(pl + tc * C::NPIX + 2 * i * C::TW + 2 * j);
+                const float2 bot = *reinterpret_cast<const float2 *>(pl + tc * C::NPIX + (2 * i + 1) * C::TW + 2 * j);
+                float m = top.x, v = top.y;
+                m = v > m ? v : m;
+                v = bot.x;
+                m = v > m ? v : m;
+                v = bot.y;
+                m = v > m ? v : m;
+                __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, m), pro,
+                                                      (int)((unsigned)((co * pool_hp + pi) * pool_wpo + pj) * 4u), 0,
+                                                      C::SPOL);
+            }
         }
     }
 
@@ -1163,6 +1210,19 @@ struct Epilogue {
 // groups of 1 and 3 took 30.1 and 30.3 us with ordinary ones.  The 4x4x1
 // tail block, if any, follows group 0 as one burst on its four accumulators
 // and is stored with group 0.
+// STREAM_POOL: the group iteration of compute_stage_streamed after which
+// pooled row i (tile pixels up to (2i + 2)*TW - 1 in tile order) is all in
+// LDS.  Group g's stores go out during iteration g + 1 (the last group's
+// after the loop, "iteration kGroups"); the tail block's with group 0's.
+template <class C>
+constexpr int pool_row_ready(int i)
+{
+    const int last_px = (2 * i + 2) * C::TW - 1;
+    const int last_full = 16 * C::NBM - 1;
+    const int px = last_px < last_full ? last_px : last_full;
+    return px / 16 / C::SGB + 1;
+}
+
 template <class C, int RELU>
 __device__ __forceinline__ void compute_stage_streamed(const float *xl, const AStage<C> &A,
                                                        const int (&b_base)[C::NB], floatx4 (&acc)[C::MA][C::NACC],
@@ -1238,6 +1298,18 @@ __device__ __forceinline__ void compute_stage_streamed(const float *xl, const AS
             }
             __builtin_amdgcn_sched_barrier(0);
         }
+        if constexpr (C::STREAM_POOL) {
+            // Rows whose pixels are all in LDS now: group grp - 1's stores
+            // went out during this group's steps.
+            if (grp >= 1) {
+                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+                __builtin_amdgcn_wave_barrier();
+                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+                for (int i = 0; i < C::TH / 2; ++i)
+                    if (pool_row_ready<C>(i) == grp) ep.pool_row(i);
+            }
+        }
         if (C::TAIL4 && grp == 0) {
 #pragma unroll
             for (int st = 0; st < kSteps; ++st) {
@@ -1258,6 +1330,14 @@ __device__ __forceinline__ void compute_stage_streamed(const float *xl, const AS
     // The last group's stores (and, with a single group, the tail's).
 #pragma unroll
     for (int i = 0; i < kDeferred; ++i) store_item(kGroups - 1, i);
+    if constexpr (C::STREAM_POOL) {
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+        for (int i = 0; i < C::TH / 2; ++i)
+            if (pool_row_ready<C>(i) == kGroups) ep.pool_row(i);
+    }
 }
 
 // LDS writes of this wave done, then every wave: a bare barrier (the global
@@ -1418,10 +1498,11 @@ __device__ __forceinline__ void final_stage(const float *xl, const AStage<C> &A,
                                             floatx4 (&acc)[C::MA][C::NACC], float *park_area, int wave, int wk,
                                             int lane, const Epilogue<C> &ep)
 {
-    if constexpr (C::NWK == 1 && !C::POOL) {
+    if constexpr (C::NWK == 1 && (!C::POOL || C::STREAM_POOL)) {
         // The ReLU choice is made once here: per store it cost a compare, a
         // mask and a select (with their register hazards) between the
-        // matrix instructions.
+        // matrix instructions.  STREAM_POOL: the stores go to the LDS tile
+        // and the wave pools its rows as they fill.
         if (ep.relu) compute_stage_streamed<C, 2>(xl, A, b_base, acc, ep);
         else compute_stage_streamed<C, 1>(xl, A, b_base, acc, ep);
     } else if constexpr (C::SSPLIT && !C::POOL) {
@@ -1429,9 +1510,10 @@ __device__ __forceinline__ void final_stage(const float *xl, const AStage<C> &A,
         if (ep.relu) compute_stage_streamed_split<C, 2>(xl, A, b_base, acc, park_area, wave, wk, lane, ep);
         else compute_stage_streamed_split<C, 1>(xl, A, b_base, acc, park_area, wave, wk, lane, ep);
     } else if constexpr (C::NWK == 1) {
-        // PoolTile: the results go to LDS, whose queue the matrix steps'
-        // operand reads use; written in one burst after the stage instead of
-        // between its steps.
+        // PoolTile with pixels split over waves: the results go to LDS,
+        // whose queue the matrix steps' operand reads use; written in one
+        // burst after the stage instead of between its steps, and pooled
+        // by the workgroup (pool_tile_finish) after a barrier.
         NoNextStage none;
         compute_stage<C>(xl, A, b_base, acc, none);
         fold_tail<C>(acc);
@@ -1840,7 +1922,7 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
     // or channel) gets an offset of at least 2^30 bytes, past the descriptor's
     // range (< 2^30, checked when the plan is made), and its store is dropped.
     ep.init(a, out, part, bias, split, co0 + wc * 16 * C::MA + 4 * g, wp, g, l16, oh0, ow0, !kPF);
-    if constexpr (C::POOL) ep.pool_init(pool_lds, co0, co0 + wc * 16 * C::MA + 4 * g, wp, g, l16, oh0, ow0, a);
+    if constexpr (C::POOL) ep.pool_init(pool_lds, out, co0, co0 + wc * 16 * C::MA + 4 * g, wp, g, l16, oh0, ow0, a);
 
     // The 16x16x4 blocks' accumulators start from the bias (zero for splits
     // other than 0, and for the waves wk > 0 whose partials are added to wave
@@ -1871,7 +1953,7 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
         run_stages<C, WS>(std::make_integer_sequence<int, C::NS>{}, bufs, regs, x, a, wctx, c_begin, wave, wk, lane,
                           xo, b_base, acc, ep);
         if constexpr (C::FUSED) finish_split_tile<C>(a, part, out, tile, co0, oh0, ow0, last_arrival);
-        if constexpr (C::POOL) pool_tile_finish<C>(pool_lds, out, a, co0, oh0, ow0);
+        if constexpr (C::POOL && !C::STREAM_POOL) pool_tile_finish<C>(pool_lds, out, a, co0, oh0, ow0);
         return;
     }
 
@@ -1893,7 +1975,7 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
                           lane, xo, b_base, acc, ep);
     }
     if constexpr (C::FUSED) finish_split_tile<C>(a, part, out, tile, co0, oh0, ow0, last_arrival);
-    if constexpr (C::POOL) pool_tile_finish<C>(pool_lds, out, a, co0, oh0, ow0);
+    if constexpr (C::POOL && !C::STREAM_POOL) pool_tile_finish<C>(pool_lds, out, a, co0, oh0, ow0);
 }
 
 
