@@ -118,7 +118,8 @@ def test_pooled_tile_writes_only_the_pooled_output(ilpm):
     the workgroup) a NaN-filled registered workspace is left untouched."""
     torch = torch_cuda()
     guard = 4096
-    in_kernel = {"k3s1_t14x14_co64_cc16_pf", "k3s1_t14x14_co32_k2", "k3s1_t14x14_co64"}
+    in_kernel = {"k3s1_t14x14_co64_cc16_pf", "k3s1_t14x14_co32_k2", "k3s1_t14x14_co64",
+                 "k3s1_t14x14_co64_cc16_pf_sc1", "k3s1_t14x14_co64_cc4_sc1", "k3s1_t14x14_co32_k2_sc1"}
     ws = torch.full((1 << 22,), float("nan"), device="cuda", dtype=torch.float32)
     ilpm.set_workspace(ws)
     try:
@@ -163,3 +164,35 @@ def test_pooled_tile_writes_only_the_pooled_output(ilpm):
     finally:
         torch.cuda.synchronize()
         ilpm.set_workspace(None)
+
+
+def test_device_scope_store_variants_match_their_plain_twins(ilpm):
+    """The `_sc1` variants differ from their plain twins only in the cache
+    policy of the output stores: same bits, plain and with ReLU + 2x2
+    max-pool (in the workgroup or after split partial sums), on OIHW and on
+    prepacked weights, on shapes that leave partial tiles."""
+    torch = torch_cuda()
+    names = {ilpm.variant_name(ilpm.PATH_IGEMM, v): v for v in range(ilpm.num_variants(ilpm.PATH_IGEMM))}
+    pairs = [(names[n[:-4]], v) for n, v in names.items() if n.endswith("_sc1") and n[:-4] in names]
+    assert len(pairs) >= 5
+    for seed, (c_in, h, w_, c_out) in enumerate([(64, 30, 30, 70), (48, 17, 23, 40)]):
+        x, w, b = random_case(8800 + 10 * seed, c_in, h, w_, c_out, 3)
+        xd, wdv, bd = dev(x), dev(w), dev(b)
+        for v_plain, v_sc1 in pairs:
+            for splits in (1, 3):
+                try:
+                    p_plain = ilpm.plan_variant(c_in, h, w_, c_out, 3, 1, 1, ilpm.PATH_IGEMM, v_plain, splits)
+                    p_sc1 = ilpm.plan_variant(c_in, h, w_, c_out, 3, 1, 1, ilpm.PATH_IGEMM, v_sc1, splits)
+                except ilpm.IlpmError:
+                    continue
+                label = f"{ilpm.variant_name(ilpm.PATH_IGEMM, v_sc1)} x{p_sc1.splits} {(c_in, h, w_, c_out)}"
+                note(f"[sc1 twin] {label}")
+                for epi in (0, 3):
+                    want = ilpm.conv2d_epilogue(xd, wdv, bd, 1, 1, epi, plan=p_plain)
+                    got = ilpm.conv2d_epilogue(xd, wdv, bd, 1, 1, epi, plan=p_sc1)
+                    packed = ilpm.prepack_weights(wdv, p_sc1)
+                    got_pk = ilpm.conv2d_prepacked_epilogue(xd, packed, c_out, 3, bd, 1, 1, epi, plan=p_sc1)
+                    torch.cuda.synchronize()
+                    np.testing.assert_array_equal(got.cpu().numpy(), want.cpu().numpy(), err_msg=f"{label} epi {epi}")
+                    np.testing.assert_array_equal(got_pk.cpu().numpy(), want.cpu().numpy(),
+                                                  err_msg=f"{label} epi {epi} prepacked")
