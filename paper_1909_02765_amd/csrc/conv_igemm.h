@@ -122,6 +122,7 @@ int variants_part6(const Variant **table);
 int variants_part7(const Variant **table);
 int variants_part8(const Variant **table);
 int variants_part9(const Variant **table);
+int variants_part10(const Variant **table);
 
 }  // namespace ig
 

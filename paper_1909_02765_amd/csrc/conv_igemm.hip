@@ -163,7 +163,7 @@ const std::vector<const Variant *> &variant_table()
         int (*const parts[])(const Variant **) = {ig::variants_part0, ig::variants_part1, ig::variants_part2,
                                                   ig::variants_part3, ig::variants_part4, ig::variants_part5,
                                                   ig::variants_part6, ig::variants_part7, ig::variants_part8,
-                                                  ig::variants_part9};
+                                                  ig::variants_part9, ig::variants_part10};
         std::vector<const Variant *> t;
         for (auto part : parts) {
             const Variant *v = nullptr;
