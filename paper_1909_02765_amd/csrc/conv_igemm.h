@@ -275,9 +275,12 @@ struct Cfg {
     static_assert(CC % (4 * NWK) == 0, "a stage holds whole groups of 4 channels per wave");
     static_assert(LDS_BYTES <= 160 * 1024, "LDS budget of one compute unit");
     static_assert(NT <= 1024, "workgroup size");
-    // Cache policy of the output stores, and whether the workgroups of a tile
-    // finish the split sum themselves (see FusedSplit).
+    // Cache policy of the kernel's own stores (the output, or the partial
+    // sums of a split plan), of the final sums a self-summing split writes
+    // (OPOL), and whether the workgroups of a tile finish the split sum
+    // themselves (see FusedSplit).
     static constexpr int SPOL = 0;
+    static constexpr int OPOL = 0;
     static constexpr bool FUSED = false;
     // A 2x2 max-pool can be applied inside the workgroup (PoolTile) when the
     // tile's windows do not cross tiles (even TH, TW) and the tile's outputs
@@ -302,6 +305,16 @@ struct FusedSplit : C {
     static constexpr bool FUSED = true;
 };
 
+// The same configuration for split plans whose partial sums a second kernel
+// adds (sum_splits, sum_splits_pool): the partial sums are stored at device
+// scope, written through each XCD's L2 while the kernel runs instead of
+// being written back from the L2 caches when it ends (512->512 at 28^2 in
+// eight splits: 38.0 -> 33.3 us).
+template <class C>
+struct SplitPart : C {
+    static constexpr int SPOL = kPolicyDeviceScope;
+};
+
 // The same configuration with the output stores at device scope (SC1):
 // written through each XCD's L2 while the kernel runs rather than written
 // back from the L2 caches when it ends, which overlaps moving a large output
@@ -309,6 +322,7 @@ struct FusedSplit : C {
 template <class C>
 struct Sc1Out : C {
     static constexpr int SPOL = kPolicyDeviceScope;
+    static constexpr int OPOL = kPolicyDeviceScope;
 };
 
 // The same configuration with the 2x2 max-pool epilogue done in the
@@ -1196,6 +1210,19 @@ struct Epilogue {
     }
 };
 
+// STREAM_POOL: the group iteration of compute_stage_streamed after which
+// pooled row i (tile pixels up to (2i + 2)*TW - 1 in tile order) is all in
+// LDS.  Group g's stores go out during iteration g + 1 (the last group's
+// after the loop, "iteration kGroups"); the tail block's with group 0's.
+template <class C>
+constexpr int pool_row_ready(int i)
+{
+    const int last_px = (2 * i + 2) * C::TW - 1;
+    const int last_full = 16 * C::NBM - 1;
+    const int px = last_px < last_full ? last_px : last_full;
+    return px / 16 / C::SGB + 1;
+}
+
 // The last stage of a one-channel-group-per-wave plan (NWK = 1), computed in
 // groups of pixel blocks (Cfg::SGB, one block) with every step of the stage
 // before moving to the next group, so that the output write overlaps the
@@ -1211,19 +1238,6 @@ struct Epilogue {
 // groups of 1 and 3 took 30.1 and 30.3 us with ordinary ones.  The 4x4x1
 // tail block, if any, follows group 0 as one burst on its four accumulators
 // and is stored with group 0.
-// STREAM_POOL: the group iteration of compute_stage_streamed after which
-// pooled row i (tile pixels up to (2i + 2)*TW - 1 in tile order) is all in
-// LDS.  Group g's stores go out during iteration g + 1 (the last group's
-// after the loop, "iteration kGroups"); the tail block's with group 0's.
-template <class C>
-constexpr int pool_row_ready(int i)
-{
-    const int last_px = (2 * i + 2) * C::TW - 1;
-    const int last_full = 16 * C::NBM - 1;
-    const int px = last_px < last_full ? last_px : last_full;
-    return px / 16 / C::SGB + 1;
-}
-
 template <class C, int RELU>
 __device__ __forceinline__ void compute_stage_streamed(const float *xl, const AStage<C> &A,
                                                        const int (&b_base)[C::NB], floatx4 (&acc)[C::MA][C::NACC],
@@ -1713,6 +1727,8 @@ __device__ __forceinline__ void finish_split_tile(const IgArgs &a, const float *
     constexpr int kTP = C::TH * C::TW;
     constexpr int kB = 8;
     const int64_t slice = (int64_t)a.c_out * a.h_out * a.w_out;
+    // The output is below 2^30 bytes (checked when the plan is made).
+    const __amdgpu_buffer_rsrc_t ro = make_rsrc(out, (unsigned)slice * 4u);
     for (int e0 = threadIdx.x; e0 < C::COT * kTP; e0 += kFuseElems * C::NT) {
         int64_t off[kFuseElems];
         bool ok[kFuseElems];
@@ -1743,7 +1759,14 @@ __device__ __forceinline__ void finish_split_tile(const IgArgs &a, const float *
         }
 #pragma unroll
         for (int j = 0; j < kFuseElems; ++j)
-            if (ok[j]) out[off[j]] = a.relu && v[j] < 0.f ? 0.f : v[j];
+            if (ok[j]) {
+                const float r = a.relu && v[j] < 0.f ? 0.f : v[j];
+                if constexpr (C::OPOL != 0)
+                    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, r), ro, (int)(off[j] * 4), 0,
+                                                          C::OPOL);
+                else
+                    out[off[j]] = r;
+            }
     }
 }
 
@@ -1995,6 +2018,11 @@ void launch_cfg(dim3 grid, hipStream_t st, const float *x, const float *w, const
     if (a.fuse) {
         if (packed) hipLaunchKernelGGL((conv_igemm<F, true>), grid, dim3(C::NT), 0, st, x, w, b, o, ws, a);
         else hipLaunchKernelGGL((conv_igemm<F, false>), grid, dim3(C::NT), 0, st, x, w, b, o, ws, a);
+    } else if (a.to_part) {
+        // (A configuration whose stores are at device scope already serves.)
+        using P = typename std::conditional<C::SPOL == kPolicyDeviceScope, C, SplitPart<C>>::type;
+        if (packed) hipLaunchKernelGGL((conv_igemm<P, true>), grid, dim3(C::NT), 0, st, x, w, b, o, ws, a);
+        else hipLaunchKernelGGL((conv_igemm<P, false>), grid, dim3(C::NT), 0, st, x, w, b, o, ws, a);
     } else {
         if (packed) hipLaunchKernelGGL((conv_igemm<C, true>), grid, dim3(C::NT), 0, st, x, w, b, o, ws, a);
         else hipLaunchKernelGGL((conv_igemm<C, false>), grid, dim3(C::NT), 0, st, x, w, b, o, ws, a);
