@@ -60,14 +60,17 @@ __global__ __launch_bounds__(128) void sum_splits(const float *__restrict__ part
     const int64_t nvec = total / V;
     const T *pv = reinterpret_cast<const T *>(part);
     const int64_t step = (int64_t)gridDim.x * 128;
+    // Stores at device scope (the output is below 2^30 bytes).
+    const __amdgpu_buffer_rsrc_t ro = make_rsrc(out, (unsigned)total * 4u);
     for (int64_t i = (int64_t)blockIdx.x * 128 + threadIdx.x; i < nvec; i += step) {
         const T s = sum_slices<T>(pv, nvec, i, splits);
-        float *o = out + i * V;
         const float *sv = reinterpret_cast<const float *>(&s);
 #pragma unroll
         for (int e = 0; e < V; ++e) {
             const float v = sv[e];
-            o[e] = relu && v < 0.f ? 0.f : v;
+            const float r = relu && v < 0.f ? 0.f : v;
+            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, r), ro, (int)((i * V + e) * 4), 0,
+                                                  kPolicyDeviceScope);
         }
     }
 }
@@ -88,6 +91,7 @@ __global__ __launch_bounds__(256) void sum_splits_pool(const float *__restrict__
     const unsigned total = (unsigned)c * hp * wp;
     const int64_t slice = (int64_t)c * h_out * w_out;
     const unsigned step = gridDim.x * 256u;
+    const __amdgpu_buffer_rsrc_t ro = make_rsrc(out, total * 4u);  // stores at device scope
     for (unsigned i = blockIdx.x * 256u + threadIdx.x; i < total; i += step) {
         const unsigned t = fast_div(i, wp_d);
         const unsigned j = i - t * wp;
@@ -115,7 +119,9 @@ __global__ __launch_bounds__(256) void sum_splits_pool(const float *__restrict__
             v = sum_slices<float>(part, slice, base + w_out + 1, splits);
             m = v > m ? v : m;
         }
-        out[i] = relu && m < 0.f ? 0.f : m;
+        const float res = relu && m < 0.f ? 0.f : m;
+        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, res), ro, (int)(i * 4u), 0,
+                                              kPolicyDeviceScope);
     }
 }
 
