@@ -340,21 +340,37 @@ constexpr int kFirstLowc = 2;  // direct variants 0 and 1 are the VALU kernels
 // Each pair of blocks is stored once its matrix instructions are issued, so
 // the stores stream behind the matrix work.
 //
+// The weights and bias come in by the same DMA: a channel group's weights
+// are 16*CW*C_in*K*K consecutive words of the OIHW tensor, copied whole in
+// 16-byte lanes (4-byte lanes where C_out*C_in*K*K is not a multiple of 4,
+// so that no lane's access crosses the end of the tensor), and each lane
+// reads its A operands from LDS after the barrier.  (Loaded per lane from
+// the tensor instead -- lane (g, l) reading w[co0 + l][4s + g], 16 lanes at
+// a stride of C_in*K*K words -- every workgroup sent ~400 cache-line
+// requests for the same few lines at kernel start; on MI355X, for VGG-16's
+// first layer, the DMA form ran 0.6 us per launch faster.)
+//
 // LDS: row r = ci*K + kh holds input columns ix0 .. ix0 + lw - 1 of input
 // row oy*S - pad + kh at r*lwp (lwp = 64 * ceil(lw / 64), one DMA of 64
 // words per wave and chunk); row C_in*K is all zeros and serves the
-// contraction slots k >= C_in*K*K.
+// contraction slots k >= C_in*K*K.  The group's weights follow at
+// (C_in*K + 1)*lwp (wregion = 256 * ceil(16*CW*C_in*K*K / 256) words, whole
+// 16-byte DMAs), then its 16*CW biases (64 words, one DMA).
 struct RowsArgs {
     int c_in, h, w, c_out, k, stride, pad, h_out, w_out;
     int kt;         // C_in*K*K
     int segs;       // segments per output row
     int co_groups;  // output-channel groups of 16*CW
     int lw, lwp, chunks;
+    int wregion;    // LDS words of the weight area
+    int w16;        // 1: weights by 16-byte DMA lanes (C_out*kt a multiple of 4)
     int relu;
     unsigned m_kk, m_k;  // ceil(2^16 / (K*K)), ceil(2^16 / K)
 };
 
-template <int NB, int PW, int CW, int STEPS, int POL>
+// SK = 1: instantiated for stride 1 (B operand offsets fold into the LDS
+// reads' immediates); SK = 0: any stride.
+template <int NB, int PW, int CW, int STEPS, int POL, int SK>
 __global__ __launch_bounds__(256) void conv_direct_rows(const float *__restrict__ x, const float *__restrict__ wt,
                                                         const float *__restrict__ bias, float *__restrict__ out,
                                                         RowsArgs a)
@@ -383,25 +399,37 @@ __global__ __launch_bounds__(256) void conv_direct_rows(const float *__restrict_
 
     const __amdgpu_buffer_rsrc_t rx = lowc_rsrc(x, (unsigned)a.c_in * a.h * a.w * 4u);
     const __amdgpu_buffer_rsrc_t rw = lowc_rsrc(wt, (unsigned)a.c_out * a.kt * 4u);
+    const __amdgpu_buffer_rsrc_t rb = lowc_rsrc(bias, bias != nullptr ? (unsigned)a.c_out * 4u : 0u);
     const __amdgpu_buffer_rsrc_t ro = lowc_rsrc(out, (unsigned)a.c_out * a.h_out * a.w_out * 4u);
 
     const int pw = wave % PW, cw = wave / PW;
     const bool active = wave < PW * CW;
-    const int co0 = (cgi * CW + cw) * 16;
-    // A: this lane's weights w[co0 + l][4s + g], in flight during the DMA.
-    float av[STEPS];
-#pragma unroll
-    for (int s = 0; s < STEPS; ++s) {
-        const int k = 4 * s + g;
-        const unsigned off = (active && co0 + l < a.c_out && k < a.kt) ? (unsigned)((co0 + l) * a.kt + k) * 4u : kFar;
-        av[s] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rw, (int)off, 0, 0));
-    }
-    // Bias (the accumulators' start), also in flight during the DMA.
-    float b4[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-        const int co = co0 + 4 * g + r;
-        b4[r] = (bias != nullptr && active && co < a.c_out) ? bias[co] : 0.f;
+    const int cg0 = cgi * CW * 16;  // the group's first channel
+    const int co0 = cg0 + cw * 16;
+    float *const wl = xl + (rows + 1) * a.lwp;
+    float *const bl = wl + a.wregion;
+    // The group's weights and biases into LDS (channels past C_out read as
+    // zeros: their offsets lie past the descriptors' ranges).
+    {
+        const unsigned wbase = (unsigned)cg0 * (unsigned)a.kt;
+        const int nw = 16 * CW * a.kt;
+        if (a.w16) {
+            for (int q = wave; 256 * q < nw; q += 4) {
+                const int j = 256 * q + 4 * lane;
+                const unsigned off = j < nw ? (wbase + (unsigned)j) * 4u : kFar;
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_ptr_t)(wl + 256 * q), 16, (int)off, 0, 0, 0);
+            }
+        } else {
+            for (int q = wave; 64 * q < nw; q += 4) {
+                const int j = 64 * q + lane;
+                const unsigned off = j < nw ? (wbase + (unsigned)j) * 4u : kFar;
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_ptr_t)(wl + 64 * q), 4, (int)off, 0, 0, 0);
+            }
+        }
+        if (wave == 3) {
+            const unsigned off = lane < 16 * CW ? (unsigned)(cg0 + lane) * 4u : kFar;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_ptr_t)bl, 4, (int)off, 0, 0, 0);
+        }
     }
     // Input rows into LDS: wave w issues chunks w, w + 4, ... of the
     // rows * chunks list (chunk i of row r = input columns ix0 + 64i ..).
@@ -430,22 +458,43 @@ __global__ __launch_bounds__(256) void conv_direct_rows(const float *__restrict_
         }
     }
     for (int j = tid; j < a.lwp; j += 256) xl[rows * a.lwp + j] = 0.f;
-    __builtin_amdgcn_s_waitcnt(0);  // this wave's DMA has landed in LDS
-    __syncthreads();
-    if (!active) return;  // no barrier follows
 
-    // LDS word of contraction slot k = 4s + g for the segment's pixel 0.
+    // While the DMA is in flight: the LDS word that contraction slot
+    // k = 4s + g reads for this lane's pixel of block 0 (slots past
+    // C_in*K*K read the zero row), and the output offsets.
+    const int stride = SK ? 1 : a.stride;
+    const int pl = pw * NB * 16 + l;  // this lane's pixel of block 0, within the segment
     int tb[STEPS];
 #pragma unroll
     for (int s = 0; s < STEPS; ++s) {
         const int k = 4 * s + g;
         const int ci = (int)(((unsigned)k * a.m_kk) >> 16), t = k - ci * a.k * a.k;
         const int kh = (int)(((unsigned)t * a.m_k) >> 16), kw = t - kh * a.k;
-        tb[s] = k < a.kt ? (ci * a.k + kh) * a.lwp + kw : rows * a.lwp;
+        tb[s] = (k < a.kt ? (ci * a.k + kh) * a.lwp + kw : rows * a.lwp) + pl * stride;
     }
-    const int pl = pw * NB * 16 + l;  // this lane's pixel of block 0, within the segment
     const int plane = a.h_out * a.w_out;
     const unsigned obase = (unsigned)(co0 + 4 * g) * (unsigned)plane + (unsigned)(oy * a.w_out + px0 + pl);
+    // Every pixel and channel of this wave's tile inside the output: stores
+    // without per-lane checks, the channel row's offset in the scalar operand.
+    const bool full = px0 + (pw + 1) * NB * 16 <= a.w_out && co0 + 16 <= a.c_out;
+
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's DMA has landed in LDS
+    __syncthreads();
+    if (!active) return;  // no barrier follows
+
+    // A: this lane's weights w[co0 + l][4s + g] (read for every slot: the
+    // word a slot past C_in*K*K would read lies inside the weight and bias
+    // areas); the accumulators start at the bias.
+    float av[STEPS];
+#pragma unroll
+    for (int s = 0; s < STEPS; ++s) {
+        const int k = 4 * s + g;
+        const float wv = wl[(cw * 16 + l) * a.kt + k];
+        av[s] = k < a.kt ? wv : 0.f;
+    }
+    float b4[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) b4[r] = bl[cw * 16 + 4 * g + r];
 
 #pragma unroll
     for (int n0 = 0; n0 < NB; n0 += kNI) {
@@ -457,22 +506,42 @@ __global__ __launch_bounds__(256) void conv_direct_rows(const float *__restrict_
 #pragma unroll
             for (int u = 0; u < kNI; ++u)
                 if (n0 + u < NB) {
-                    const float bv = xl[tb[s] + (pl + 16 * (n0 + u)) * a.stride];
+                    const float bv = xl[tb[s] + 16 * (n0 + u) * stride];
                     acc[u] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[s], bv, acc[u], 0, 0, 0);
                 }
+        if (a.relu) {
 #pragma unroll
-        for (int u = 0; u < kNI; ++u)
-            if (n0 + u < NB) {
-                const bool pix_ok = px0 + pl + 16 * (n0 + u) < a.w_out;
+            for (int u = 0; u < kNI; ++u)
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const bool ok = pix_ok && co0 + 4 * g + r < a.c_out;
-                    const unsigned off = ok ? (obase + (unsigned)(r * plane + 16 * (n0 + u))) * 4u : kFar;
-                    float v = acc[u][r];
-                    if (a.relu && v < 0.f) v = 0.f;
-                    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v), ro, (int)off, 0, POL);
+                for (int r = 0; r < 4; ++r)
+                    if (acc[u][r] < 0.f) acc[u][r] = 0.f;
+        }
+        if (full) {
+#pragma unroll
+            for (int u = 0; u < kNI; ++u)
+                if (n0 + u < NB) {
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const float v = acc[u][r];
+                        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v), ro,
+                                                              (int)((obase + 16u * (n0 + u)) * 4u),
+                                                              (int)((unsigned)(r * plane) * 4u), POL);
+                    }
                 }
-            }
+        } else {
+#pragma unroll
+            for (int u = 0; u < kNI; ++u)
+                if (n0 + u < NB) {
+                    const bool pix_ok = px0 + pl + 16 * (n0 + u) < a.w_out;
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const bool ok = pix_ok && co0 + 4 * g + r < a.c_out;
+                        const unsigned off = ok ? (obase + (unsigned)(r * plane + 16 * (n0 + u))) * 4u : kFar;
+                        const float v = acc[u][r];
+                        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v), ro, (int)off, 0, POL);
+                    }
+                }
+        }
     }
 }
 
@@ -486,7 +555,10 @@ template <int NB, int PW, int CW, int POL>
 void rows_launch(dim3 grid, int lds, hipStream_t st, const float *x, const float *w, const float *b, float *o,
                  const RowsArgs &a)
 {
-    hipLaunchKernelGGL((conv_direct_rows<NB, PW, CW, 7, POL>), grid, dim3(256), lds, st, x, w, b, o, a);
+    if (a.stride == 1)
+        hipLaunchKernelGGL((conv_direct_rows<NB, PW, CW, 7, POL, 1>), grid, dim3(256), lds, st, x, w, b, o, a);
+    else
+        hipLaunchKernelGGL((conv_direct_rows<NB, PW, CW, 7, POL, 0>), grid, dim3(256), lds, st, x, w, b, o, a);
 }
 
 // Store policy SC1 (device scope): the output is written through each XCD's
@@ -521,6 +593,8 @@ RowsArgs rows_args(const ConvShape &s, const RowsVariant &d)
     a.lw = (16 * d.nb * d.pw - 1) * s.stride + s.k;
     a.chunks = ceil_div(a.lw, 64);
     a.lwp = 64 * a.chunks;
+    a.wregion = 256 * ceil_div(16 * d.cw * a.kt, 256);
+    a.w16 = ((int64_t)s.c_out * a.kt) % 4 == 0 ? 1 : 0;
     a.relu = 0;
     a.m_kk = (65536u + (unsigned)(s.k * s.k) - 1) / (unsigned)(s.k * s.k);
     a.m_k = (65536u + (unsigned)s.k - 1) / (unsigned)s.k;
@@ -655,7 +729,8 @@ bool direct_make_plan(const ConvShape &s, int variant, ilpm_plan *p)
             (int64_t)s.c_out * plane * 4 >= (1LL << 31))
             return false;
         const RowsArgs a = rows_args(s, d);
-        if ((int64_t)(s.c_in * s.k + 1) * a.lwp > kRowsLdsFloats) return false;
+        const int64_t lds_floats = (int64_t)(s.c_in * s.k + 1) * a.lwp + a.wregion + 64;
+        if (lds_floats > kRowsLdsFloats) return false;
         const int64_t units = (int64_t)s.h_out * a.segs * a.co_groups;
         if (units > 0x7fffffffLL) return false;
         q.tile_h = 1;
@@ -663,7 +738,7 @@ bool direct_make_plan(const ConvShape &s, int variant, ilpm_plan *p)
         q.co_tile = 16 * d.cw;
         q.ci_chunk = s.c_in;
         q.grid = (int)units;
-        q.lds_bytes = (int)sizeof(float) * (s.c_in * s.k + 1) * a.lwp;
+        q.lds_bytes = (int)(sizeof(float) * lds_floats);
     } else if (variant == 1) {
         const int64_t total = (int64_t)s.c_out * s.h_out * s.w_out;
         const int64_t blocks = (total + kThreads - 1) / kThreads;

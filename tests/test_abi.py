@@ -411,13 +411,15 @@ def test_low_channel_direct_variants_plan_only_short_contractions():
     for v in rows:
         # One workgroup per (output row, row segment, channel group); LDS
         # holds the C_in*K input rows the segment reads and one zero row,
-        # each padded to whole 64-word DMA chunks.
+        # each padded to whole 64-word DMA chunks, then the group's weights
+        # (whole 256-word DMAs) and 64 words of biases.
         p = ilpm.plan_variant(3, 224, 224, 64, 3, 1, 1, ilpm.PATH_DIRECT, v)
         info = ilpm.variant_info(ilpm.PATH_DIRECT, v)
         segs, groups = -(-224 // info["tile_w"]), -(-64 // info["co_tile"])
         lwp = 64 * -(-(info["tile_w"] - 1 + 3) // 64)
+        wregion = 256 * -(-(info["co_tile"] * 27) // 256)
         assert p.grid == 224 * segs * groups and p.block == 256 and p.workspace_bytes == 0
-        assert p.lds_bytes == 4 * (3 * 3 + 1) * lwp
+        assert p.lds_bytes == 4 * ((3 * 3 + 1) * lwp + wregion + 64)
         with pytest.raises(ilpm.IlpmError):
             ilpm.plan_variant(4, 224, 224, 64, 3, 1, 1, ilpm.PATH_DIRECT, v)  # 36 > 28
     big = [v for v in range(ilpm.num_variants(ilpm.PATH_DIRECT))
