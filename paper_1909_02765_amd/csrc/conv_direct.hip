@@ -350,10 +350,16 @@ constexpr int kFirstLowc = 2;  // direct variants 0 and 1 are the VALU kernels
 // requests for the same few lines at kernel start; on MI355X, for VGG-16's
 // first layer, the DMA form ran 0.6 us per launch faster.)
 //
-// LDS: row r = ci*K + kh holds input columns ix0 .. ix0 + lw - 1 of input
-// row oy*S - pad + kh at r*lwp (lwp = 64 * ceil(lw / 64), one DMA of 64
-// words per wave and chunk); row C_in*K is all zeros and serves the
-// contraction slots k >= C_in*K*K.  The group's weights follow at
+// LDS: row r = ci*K + kh holds input row oy*S - pad + kh from column ax0
+// on at r*lwp; row C_in*K is all zeros and serves the contraction slots
+// k >= C_in*K*K.  Where W is a multiple of 4 and the input 16-byte aligned,
+// ax0 = ix0 rounded down to a multiple of 4 and each row is copied in
+// 16-byte lanes (lwp = 256 * ceil((lw + 3) / 256): one DMA of 256 words per
+// wave and chunk), so that a lane's four columns lie all inside the input
+// row or all in its padding; else ax0 = ix0 and 4-byte lanes (one DMA of 64
+// words per chunk; lwp = 64 * ceil(lw / 64), or the 16-byte layout's pitch
+// where the plan allotted it).  For VGG-16's first layer the 16-byte rows
+// halve the input DMAs (9 instead of 18 per workgroup).  The group's weights follow at
 // (C_in*K + 1)*lwp (wregion = 256 * ceil(16*CW*C_in*K*K / 256) words, whole
 // 16-byte DMAs), then its 16*CW biases (64 words, one DMA).
 struct RowsArgs {
@@ -362,6 +368,8 @@ struct RowsArgs {
     int segs;       // segments per output row
     int co_groups;  // output-channel groups of 16*CW
     int lw, lwp, chunks;
+    int chunks16;   // 256-word chunks per row in the 16-byte layout (0: the plan has no such layout)
+    int x16;        // 1: input rows by 16-byte DMA lanes (chunks16 > 0, input 16-byte aligned)
     int wregion;    // LDS words of the weight area
     int w16;        // 1: weights by 16-byte DMA lanes (C_out*kt a multiple of 4)
     int relu;
@@ -432,13 +440,17 @@ __global__ __launch_bounds__(256) void conv_direct_rows(const float *__restrict_
         }
     }
     // Input rows into LDS: wave w issues chunks w, w + 4, ... of the
-    // rows * chunks list (chunk i of row r = input columns ix0 + 64i ..).
-    // (r, i) and r = (ci, kh) advance by counting, without divisions.
+    // rows * chunks list (chunk i of row r = input columns ax0 + 64i .. in
+    // 4-byte lanes, ax0 + 256i .. in 16-byte lanes).  (r, i) and
+    // r = (ci, kh) advance by counting, without divisions.
+    const int ax0 = a.x16 ? (ix0 & ~3) : ix0;
+    const int shift = ix0 - ax0;  // LDS column of input column ix0
     {
+        const int nch = a.x16 ? a.chunks16 : a.chunks;
         int r = 0, i = wave, ci = 0, kh = 0;
         auto settle = [&]() {
-            while (i >= a.chunks) {
-                i -= a.chunks;
+            while (i >= nch) {
+                i -= nch;
                 ++r;
                 if (++kh == a.k) {
                     kh = 0;
@@ -447,14 +459,28 @@ __global__ __launch_bounds__(256) void conv_direct_rows(const float *__restrict_
             }
         };
         settle();
-        while (r < rows) {
-            const int iy = iy0 + kh;
-            const int j = 64 * i + lane, ix = ix0 + j;
-            const bool ok = j < a.lw && (unsigned)iy < (unsigned)a.h && (unsigned)ix < (unsigned)a.w;
-            const unsigned off = ok ? (unsigned)((ci * a.h + iy) * a.w + ix) * 4u : kFar;
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_ptr_t)(xl + r * a.lwp + 64 * i), 4, (int)off, 0, 0, 0);
-            i += 4;
-            settle();
+        if (a.x16) {
+            while (r < rows) {
+                const int iy = iy0 + kh;
+                const int j = 256 * i + 4 * lane, cx = ax0 + j;
+                const bool ok = j < a.lw + shift && (unsigned)iy < (unsigned)a.h && (unsigned)cx < (unsigned)a.w;
+                const unsigned off = ok ? (unsigned)((ci * a.h + iy) * a.w + cx) * 4u : kFar;
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_ptr_t)(xl + r * a.lwp + 256 * i), 16, (int)off, 0, 0,
+                                                         0);
+                i += 4;
+                settle();
+            }
+        } else {
+            while (r < rows) {
+                const int iy = iy0 + kh;
+                const int j = 64 * i + lane, ix = ix0 + j;
+                const bool ok = j < a.lw && (unsigned)iy < (unsigned)a.h && (unsigned)ix < (unsigned)a.w;
+                const unsigned off = ok ? (unsigned)((ci * a.h + iy) * a.w + ix) * 4u : kFar;
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_ptr_t)(xl + r * a.lwp + 64 * i), 4, (int)off, 0, 0,
+                                                         0);
+                i += 4;
+                settle();
+            }
         }
     }
     for (int j = tid; j < a.lwp; j += 256) xl[rows * a.lwp + j] = 0.f;
@@ -470,7 +496,7 @@ __global__ __launch_bounds__(256) void conv_direct_rows(const float *__restrict_
         const int k = 4 * s + g;
         const int ci = (int)(((unsigned)k * a.m_kk) >> 16), t = k - ci * a.k * a.k;
         const int kh = (int)(((unsigned)t * a.m_k) >> 16), kw = t - kh * a.k;
-        tb[s] = (k < a.kt ? (ci * a.k + kh) * a.lwp + kw : rows * a.lwp) + pl * stride;
+        tb[s] = (k < a.kt ? (ci * a.k + kh) * a.lwp + kw : rows * a.lwp) + shift + pl * stride;
     }
     const int plane = a.h_out * a.w_out;
     const unsigned obase = (unsigned)(co0 + 4 * g) * (unsigned)plane + (unsigned)(oy * a.w_out + px0 + pl);
@@ -593,9 +619,19 @@ RowsArgs rows_args(const ConvShape &s, const RowsVariant &d)
     a.lw = (16 * d.nb * d.pw - 1) * s.stride + s.k;
     a.chunks = ceil_div(a.lw, 64);
     a.lwp = 64 * a.chunks;
+    a.chunks16 = 0;
+    a.x16 = 0;
     a.wregion = 256 * ceil_div(16 * d.cw * a.kt, 256);
     a.w16 = ((int64_t)s.c_out * a.kt) % 4 == 0 ? 1 : 0;
     a.relu = 0;
+    // The 16-byte row layout where W is a multiple of 4 and it fits in LDS.
+    if (s.w % 4 == 0) {
+        const int c16 = ceil_div(a.lw + 3, 256);
+        if ((int64_t)(s.c_in * s.k + 1) * 256 * c16 + a.wregion + 64 <= kRowsLdsFloats) {
+            a.chunks16 = c16;
+            a.lwp = 256 * c16;
+        }
+    }
     a.m_kk = (65536u + (unsigned)(s.k * s.k) - 1) / (unsigned)(s.k * s.k);
     a.m_k = (65536u + (unsigned)s.k - 1) / (unsigned)s.k;
     return a;
@@ -765,6 +801,7 @@ hipError_t direct_launch(const ilpm_plan &p, const ConvShape &s, const float *x,
         const RowsVariant &d = kRows[p.variant - kFirstRows];
         RowsArgs ra = rows_args(s, d);
         ra.relu = relu ? 1 : 0;
+        ra.x16 = ra.chunks16 > 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0 ? 1 : 0;
         d.launch(dim3(p.grid), p.lds_bytes, stream, x, w, bias, out, ra);
         return hipGetLastError();
     }

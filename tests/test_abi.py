@@ -411,17 +411,22 @@ def test_low_channel_direct_variants_plan_only_short_contractions():
     for v in rows:
         # One workgroup per (output row, row segment, channel group); LDS
         # holds the C_in*K input rows the segment reads and one zero row,
-        # each padded to whole 64-word DMA chunks, then the group's weights
-        # (whole 256-word DMAs) and 64 words of biases.
+        # each padded to whole 256-word DMA chunks of 16-byte lanes (W = 224
+        # is a multiple of 4; the copy starts up to 3 columns early), then
+        # the group's weights (whole 256-word DMAs) and 64 words of biases.
         p = ilpm.plan_variant(3, 224, 224, 64, 3, 1, 1, ilpm.PATH_DIRECT, v)
         info = ilpm.variant_info(ilpm.PATH_DIRECT, v)
         segs, groups = -(-224 // info["tile_w"]), -(-64 // info["co_tile"])
-        lwp = 64 * -(-(info["tile_w"] - 1 + 3) // 64)
+        lwp = 256 * -(-(info["tile_w"] - 1 + 3 + 3) // 256)
         wregion = 256 * -(-(info["co_tile"] * 27) // 256)
         assert p.grid == 224 * segs * groups and p.block == 256 and p.workspace_bytes == 0
         assert p.lds_bytes == 4 * ((3 * 3 + 1) * lwp + wregion + 64)
         with pytest.raises(ilpm.IlpmError):
             ilpm.plan_variant(4, 224, 224, 64, 3, 1, 1, ilpm.PATH_DIRECT, v)  # 36 > 28
+        # W not a multiple of 4: rows of whole 64-word chunks of 4-byte lanes.
+        q = ilpm.plan_variant(3, 30, 222, 64, 3, 1, 1, ilpm.PATH_DIRECT, v)
+        lwp4 = 64 * -(-(info["tile_w"] - 1 + 3) // 64)
+        assert q.lds_bytes == 4 * ((3 * 3 + 1) * lwp4 + wregion + 64)
     big = [v for v in range(ilpm.num_variants(ilpm.PATH_DIRECT))
            if ilpm.variant_name(ilpm.PATH_DIRECT, v).startswith("direct_mfma_k64")]
     for v in big:

@@ -446,6 +446,41 @@ def test_fused_split_sum_matches_kernel_bitwise(ilpm):
         ilpm.set_workspace(None)
 
 
+def test_row_kernel_input_layouts(ilpm):
+    """The row-segment kernel copies input rows into LDS in 16-byte lanes
+    where W is a multiple of 4 and the input is 16-byte aligned, else in
+    4-byte lanes: an input 4 bytes off that alignment (a view one float
+    into a buffer) gives the same bits, and both match the oracle, on
+    strides 1-3, K 1-5, padding on both sides and segments ending past W."""
+    torch = torch_cuda()
+    shapes = [(3, 20, 36, 40, 3, 2, 1), (1, 9, 64, 20, 5, 1, 2), (2, 11, 44, 64, 3, 3, 1), (1, 8, 16, 17, 5, 2, 2),
+              (27, 5, 12, 33, 1, 1, 0), (3, 6, 232, 64, 3, 1, 1)]
+    names = {v: ilpm.variant_name(ilpm.PATH_DIRECT, v) for v in range(ilpm.num_variants(ilpm.PATH_DIRECT))}
+    rows = [v for v, n in names.items() if n.startswith("direct_rows")]
+    for i, (c_in, h, w_, c_out, k, s, p) in enumerate(shapes):
+        x, w, b = random_case(4700 + 7 * i, c_in, h, w_, c_out, k, bias=(i % 2 == 0))
+        ref, sab = oracle.conv2d_f64(x, w, b, s, p)
+        flat = torch.empty(x.size + 1, dtype=torch.float32, device="cuda")
+        xm = flat[1:].view(x.shape)
+        xm.copy_(torch.from_numpy(x).cuda())
+        assert xm.data_ptr() % 16 == 4
+        wd, bd = dev(w), dev(b)
+        ran = 0
+        for v in rows:
+            try:
+                plan = ilpm.plan_variant(c_in, h, w_, c_out, k, s, p, ilpm.PATH_DIRECT, v)
+            except ilpm.IlpmError:
+                continue
+            note(f"[row layouts {i}] {(c_in, h, w_, c_out, k, s, p)} {describe(plan)}")
+            got = run_conv(x, w, b, s, p, plan=plan)
+            assert_matches(got, ref, sab, c_in, k, f"rows {i} {names[v]}")
+            mis = ilpm.conv2d(xm, wd, bd, s, p, plan=plan)
+            torch.cuda.synchronize()
+            np.testing.assert_array_equal(mis.cpu().numpy(), got, err_msg=f"rows {i} {names[v]} misaligned input")
+            ran += 1
+        assert ran, f"no row variant planned {(c_in, h, w_, c_out, k, s, p)}"
+
+
 def test_low_channel_direct_ragged(ilpm):
     """The low-channel matrix-core direct kernels on ragged shapes: one output
     column or row (W_out = 1 makes the pixel division trivial), planes and
