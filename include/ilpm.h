@@ -238,11 +238,14 @@ int ilpm_variant_info(int path, int variant, int *K, int *stride, int *tile_h, i
  * ceil(C_in / ci_chunk) / stages splits.  A variant with a progressive
  * first stage (its first stage's matrix work starts once its first four
  * input channels have landed) plans only splits of at least two stages each.
+ * A 1x1 variant whose lanes take consecutive input channels (four OIHW
+ * weights per 16-byte load) plans only C_in a multiple of 4.
  * Pure host; ILPM_ERR_INVALID_ARG for an unknown variant.  Any output pointer
  * may be NULL.
  */
 #define ILPM_VARIANT_WEIGHTS_LDS 1       /* weights staged through LDS from OIHW; prepacked weights are an OIHW copy */
 #define ILPM_VARIANT_PROGRESSIVE_FIRST 2 /* progressive first stage: at least two stages per split */
+#define ILPM_VARIANT_CONSECUTIVE_CHANNELS 4 /* consecutive input channels per lane: C_in a multiple of 4 */
 int ilpm_variant_pipeline(int path, int variant, int *ci_chunk, int *stages, int *buffers, int *flags);
 
 /*

@@ -30,6 +30,7 @@ PATH_DIRECT = 0
 PATH_IGEMM = 1
 VARIANT_WEIGHTS_LDS = 1   # ilpm_variant_pipeline flags
 VARIANT_PROGRESSIVE_FIRST = 2
+VARIANT_CONSECUTIVE_CHANNELS = 4
 
 
 class IlpmError(RuntimeError):
@@ -208,7 +209,8 @@ def variant_info(path: int, variant: int):
            "ilpm_variant_pipeline")
     return dict(k=k, stride=s, tile_h=th, tile_w=tw, co_tile=co, ci_chunk=cc.value, stages=ns.value,
                 buffers=nb.value, weights_lds=bool(fl.value & VARIANT_WEIGHTS_LDS),
-                progressive_first=bool(fl.value & VARIANT_PROGRESSIVE_FIRST))
+                progressive_first=bool(fl.value & VARIANT_PROGRESSIVE_FIRST),
+                consecutive_channels=bool(fl.value & VARIANT_CONSECUTIVE_CHANNELS))
 
 
 def workspace_size(c_in, h, w, c_out, k, stride=1, pad=0) -> int:

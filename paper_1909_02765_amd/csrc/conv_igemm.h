@@ -106,6 +106,7 @@ struct Variant {
     int nbuf;    // stage buffers
     bool pf;     // progressive first stage: needs at least two stages per workgroup
     bool poolable;  // has a PoolTile instantiation (2x2 max-pool in the workgroup)
+    bool c1;        // consecutive channels per lane (Cfg::C1): plans need C_in a multiple of 4
     void (*launch)(dim3 grid, hipStream_t st, const float *, const float *, const float *, float *, float *,
                    const IgArgs &, bool packed);
 };
@@ -206,6 +207,19 @@ struct Cfg {
     static constexpr int NBM = TAIL4 ? NB - 1 : NB;  // 16x16x4 blocks
     static constexpr int NACC = TAIL4 ? NB + 3 : NB;
     static constexpr int G4 = CC / 4 / NWK;  // channel groups per wave per stage
+    // Which channel of a stage lane (g, l) of wave wk takes in its channel
+    // group c4.  In general 4*wk + g + 4*NWK*c4 (the four lane groups of a
+    // step on four neighbouring channel planes).  For 1x1 filters with a
+    // multiple of four groups per lane (C1) the lane's channels are
+    // consecutive instead, G4*(4*wk + g) + c4, so that four of its OIHW
+    // weights are one 16-byte load (with the interleaved order each is a
+    // 4-byte load, 16 output-channel rows per instruction; plans of these
+    // variants need C_in a multiple of 4, so that no such load crosses the
+    // end of the tensor).  The B reads and the prepacked layout follow the
+    // same order.
+    static constexpr bool C1 = KS == 1 && G4 % 4 == 0 && !WL_ && !PF_;
+    static constexpr int LSTEP = C1 ? G4 : 1;       // planes between lanes' channels (ci_lane = 4*wk + g)
+    static constexpr int CSTEP = C1 ? 1 : 4 * NWK;  // planes between a lane's channel groups
     // One stage buffer: the halo, a whole number of 64-word rows (one DMA
     // instruction each).
     static constexpr int XSZ = round64(CC * PL);
@@ -380,7 +394,7 @@ struct AStage<C, true> {
 // Where a lane's weights come from.  Every wave holds, per stage, the
 // weights of its 16*MA output channels for its channel groups, as
 // A.v[m][c4][t] = w[co0 + wc*16*MA + 16*m + l][ci0 + 4*wk + g + 4*NWK*c4][t]
-// for lane (g, l).  A source issues them as NA single load instructions,
+// for lane (g, l) (with Cfg::C1, channel ci0 + G4*(4*wk + g) + c4).  A source issues them as NA single load instructions,
 // load(q) being the q-th.
 struct WeightCtx {
     __amdgpu_buffer_rsrc_t rw;
@@ -399,10 +413,11 @@ struct WeightCtx {
 template <class C>
 struct OihwWeights {
     static constexpr int kPieces = C::KK / 4 + C::KK % 4;
-    static constexpr int NA = C::G4 * C::MA * kPieces;
+    // C1: load j*MA + m holds channel groups 4j..4j+3 of m-block m.
+    static constexpr int NA = C::C1 ? C::G4 / 4 * C::MA : C::G4 * C::MA * kPieces;
     static constexpr int NA_MIN = NA;  // issued by every wave
     // The last load (in issue order) of channel group c's registers.
-    static constexpr int group_last(int c) { return (c + 1) * C::MA * kPieces - 1; }
+    static constexpr int group_last(int c) { return C::C1 ? (c / 4 + 1) * C::MA - 1 : (c + 1) * C::MA * kPieces - 1; }
     __amdgpu_buffer_rsrc_t rw;
     unsigned a_base[C::G4][C::MA];
 
@@ -421,7 +436,9 @@ struct OihwWeights {
         }
 #pragma unroll
         for (int c4 = 0; c4 < C::G4; ++c4) {
-            const int ci = ci0 + k.ci_lane + 4 * C::NWK * c4;
+            // C1: a_base[j][m] (j < G4/4) for groups 4j..4j+3, all four inside
+            // the row or all past it (C_in and the first channel multiples of 4).
+            const int ci = C::C1 ? ci0 + k.ci_lane * C::G4 + 4 * c4 : ci0 + k.ci_lane + 4 * C::NWK * c4;
 #pragma unroll
             for (int m = 0; m < C::MA; ++m)
                 a_base[c4][m] =
@@ -431,6 +448,16 @@ struct OihwWeights {
 
     __device__ __forceinline__ void load(int q, AStage<C> &A) const
     {
+        if constexpr (C::C1) {
+            const int j = q / C::MA, m = q % C::MA;
+            const floatx4 v =
+                __builtin_bit_cast(floatx4, __builtin_amdgcn_raw_buffer_load_b128(rw, (int)a_base[j][m], 0, 0));
+            A.v[m][4 * j][0] = v[0];
+            A.v[m][4 * j + 1][0] = v[1];
+            A.v[m][4 * j + 2][0] = v[2];
+            A.v[m][4 * j + 3][0] = v[3];
+            return;
+        }
         const int c4 = q / (C::MA * kPieces), m = (q / kPieces) % C::MA, piece = q % kPieces;
         const unsigned base = a_base[c4][m];
         float *dst = A.v[m][c4];
@@ -737,7 +764,7 @@ __device__ __forceinline__ void read_b(const float *xl, const int (&b_base)[C::N
     const int t = st / C::G4, c4 = st % C::G4;
     const int kh = t / C::KS, kw = t % C::KS;
 #pragma unroll
-    for (int n = 0; n < C::NB; ++n) bv[n] = xl[b_base[n] + 4 * C::NWK * c4 * C::PL + kh * C::HCP + kw];
+    for (int n = 0; n < C::NB; ++n) bv[n] = xl[b_base[n] + C::CSTEP * c4 * C::PL + kh * C::HCP + kw];
 }
 
 // One stage of MFMA work for one wave: every tap, this wave's channel groups,
@@ -1268,7 +1295,7 @@ __device__ __forceinline__ void compute_stage_streamed(const float *xl, const AS
     auto read = [&](int grp, int st, float(&dst)[GB]) {
         const int t = st / C::G4, c4 = st % C::G4;
         const int kh = t / C::KS, kw = t % C::KS;
-        const int off = 4 * C::NWK * c4 * C::PL + kh * C::HCP + kw;
+        const int off = C::CSTEP * c4 * C::PL + kh * C::HCP + kw;
 #pragma unroll
         for (int j = 0; j < GB; ++j) {
             const int n = grp * GB + j;
@@ -1402,7 +1429,7 @@ __device__ __forceinline__ void compute_stage_streamed_split(const float *xl, co
     auto read = [&](int grp, int st, float(&dst)[GB]) {
         const int t = st / C::G4, c4 = st % C::G4;
         const int kh = t / C::KS, kw = t % C::KS;
-        const int off = 4 * C::NWK * c4 * C::PL + kh * C::HCP + kw;
+        const int off = C::CSTEP * c4 * C::PL + kh * C::HCP + kw;
 #pragma unroll
         for (int j = 0; j < GB; ++j) {
             const int n = grp * GB + j;
@@ -1935,7 +1962,7 @@ __global__ __launch_bounds__(C::NT) void conv_igemm(const float *__restrict__ x,
     for (int nb = 0; nb < C::NB; ++nb) {
         int p = (wp * C::NB + nb) * 16 + ((C::TAIL4 && nb == C::NB - 1) ? (l16 & 3) : l16);
         if (p >= C::NPIX) p = 0;  // padding lanes read a valid word; never stored
-        b_base[nb] = ci_lane * C::PL + (p / C::TW) * C::S * C::HCP + (p % C::TW) * C::S;
+        b_base[nb] = ci_lane * C::LSTEP * C::PL + (p / C::TW) * C::S * C::HCP + (p % C::TW) * C::S;
     }
 
     // Output side, set up before the last stage so that its stores can stream
@@ -2035,7 +2062,8 @@ template <class C>
 constexpr Variant make_variant(const char *name)
 {
     return Variant{name, C::KS, C::S, C::TH, C::TW, C::NWC, C::NWP, C::NWK, C::MA, C::CC,
-                   C::NT, C::COT, C::LDS_BYTES, C::NS, C::WL, C::NBUF, C::PF, C::POOLABLE, &launch_cfg<C>};
+                   C::NT, C::COT, C::LDS_BYTES, C::NS, C::WL, C::NBUF, C::PF, C::POOLABLE, C::C1,
+                   &launch_cfg<C>};
 }
 
 }  // namespace

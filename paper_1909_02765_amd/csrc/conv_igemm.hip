@@ -129,6 +129,7 @@ __global__ __launch_bounds__(256) void sum_splits_pool(const float *__restrict__
 // per packed float; channels past C_out or C_in become zeros.
 struct PackGeom {
     int c_in, c_out, kk, cot, cc, nwc, nwk, ma, g4, nchunks;
+    int c1;  // consecutive channels per lane (Cfg::C1)
 };
 
 __global__ __launch_bounds__(256) void pack_weights(const float *__restrict__ w, float *__restrict__ packed,
@@ -157,7 +158,8 @@ __global__ __launch_bounds__(256) void pack_weights(const float *__restrict__ w,
         const int co_t = (int)(b2 / g.nchunks);
         const int m = e / (g.g4 * g.kk), c4 = (e / g.kk) % g.g4, tap = e % g.kk;
         const int co = co_t * g.cot + wc * 16 * g.ma + 16 * m + (lane & 15);
-        const int ci = chunk * g.cc + 4 * wk + (lane >> 4) + 4 * g.nwk * c4;
+        const int ci = g.c1 ? chunk * g.cc + g.g4 * (4 * wk + (lane >> 4)) + c4
+                            : chunk * g.cc + 4 * wk + (lane >> 4) + 4 * g.nwk * c4;
         packed[idx] = (co < g.c_out && ci < g.c_in) ? w[((int64_t)co * g.c_in + ci) * g.kk + tap] : 0.f;
     }
 }
@@ -211,7 +213,8 @@ bool igemm_variant_pipeline(int v, int *ci_chunk, int *stages, int *buffers, int
     *ci_chunk = d.cc;
     *stages = d.stages;
     *buffers = d.nbuf;
-    *flags = (d.wl ? ILPM_VARIANT_WEIGHTS_LDS : 0) | (d.pf ? ILPM_VARIANT_PROGRESSIVE_FIRST : 0);
+    *flags = (d.wl ? ILPM_VARIANT_WEIGHTS_LDS : 0) | (d.pf ? ILPM_VARIANT_PROGRESSIVE_FIRST : 0) |
+             (d.c1 ? ILPM_VARIANT_CONSECUTIVE_CHANNELS : 0);
     return true;
 }
 
@@ -220,6 +223,9 @@ bool igemm_make_plan(const ConvShape &s, int variant, int splits, ilpm_plan *p)
     if (variant < 0 || variant >= num_variants()) return false;
     const Variant &d = variant_at(variant);
     if (d.ks != s.k || d.s != s.stride) return false;
+    // Consecutive channels per lane: 16-byte weight loads that stay inside
+    // the tensor only when C_in is a multiple of 4.
+    if (d.c1 && s.c_in % 4 != 0) return false;
     // Load offsets are 31-bit byte offsets.
     if ((int64_t)s.c_in * s.h * s.w * 4 >= (1LL << 31)) return false;
     if ((int64_t)s.c_out * s.c_in * s.k * s.k * 4 >= (1LL << 31)) return false;
@@ -320,6 +326,7 @@ hipError_t igemm_pack(const ilpm_plan &p, int c_in, int c_out, const float *w, f
     g.ma = d.ma;
     g.g4 = d.cc / 4 / d.nwk;
     g.nchunks = ceil_div(c_in, d.cc);
+    g.c1 = d.c1 ? 1 : 0;
     const int64_t total = igemm_packed_floats(p, c_in, c_out);
     int64_t blocks = (total + 255) / 256;
     if (blocks > 65536) blocks = 65536;

@@ -305,6 +305,8 @@ def test_prepacked_size():
                 ci = info["stages"] * info["ci_chunk"] - 3
             if info["progressive_first"]:  # at least two stages, the last partial
                 ci = max(ci, 2 * info["ci_chunk"] - 3)
+            if info["consecutive_channels"]:  # C_in a multiple of 4, the last chunk partial
+                ci = -(-ci // 4) * 4
             p = ilpm.plan_variant(ci, 16, 16, c_out, k, s, k // 2, ilpm.PATH_IGEMM, v, 0 if info["stages"] else 1)
             cot, cc = p.co_tile, p.ci_chunk
             want = -(-c_out // cot) * cot * (-(-ci // cc) * cc) * k * k * 4
@@ -483,3 +485,21 @@ def test_plan_for_layouts_and_epilogues():
     out = ilpm.ilpm_plan()
     for epi, packed in ((4, 0), (0, 2), (0, -1)):
         assert ilpm.lib.ilpm_conv2d_plan_for(*shape, epi, packed, ctypes.byref(out)) == ilpm.ERR_INVALID_ARG
+
+
+def test_consecutive_channel_variants_need_c_in_multiple_of_4():
+    """The 1x1 variants whose lanes take four consecutive input channels per
+    16-byte weight load plan only for C_in a multiple of 4 (a load then never
+    reaches past the weight tensor); the other 1x1 variant takes any C_in."""
+    names = {ilpm.variant_name(ilpm.PATH_IGEMM, v): v for v in range(ilpm.num_variants(ilpm.PATH_IGEMM))}
+    c1 = {n for n, v in names.items() if ilpm.variant_info(ilpm.PATH_IGEMM, v)["consecutive_channels"]}
+    assert c1 == {"k1s1_t7x7_co64", "k1s1_t14x14_co64", "k1s1_t4x4_co16_k4"}
+    for name in sorted(c1):
+        v = names[name]
+        for c_in in (4, 8, 36, 512):
+            ilpm.plan_variant(c_in, 7, 7, 64, 1, 1, 0, ilpm.PATH_IGEMM, v, 1)
+        for c_in in (1, 6, 37, 513):
+            with pytest.raises(ilpm.IlpmError):
+                ilpm.plan_variant(c_in, 7, 7, 64, 1, 1, 0, ilpm.PATH_IGEMM, v, 1)
+    for c_in in (1, 6, 37, 513):
+        ilpm.plan_variant(c_in, 7, 7, 64, 1, 1, 0, ilpm.PATH_IGEMM, names["k1s1_t7x7_co64_k4"], 1)

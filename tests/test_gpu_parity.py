@@ -290,6 +290,34 @@ def test_prepacked_ragged_channels(ilpm):
                 assert_matches(got.cpu().numpy(), ref, sab, c_in, k, f"prepacked ragged{seed} v{v}")
 
 
+def test_one_by_one_consecutive_channels(ilpm):
+    """1x1 variants, including those whose lanes take consecutive input
+    channels (one 16-byte weight load per four channels; planned only for
+    C_in a multiple of 4): partial channel stages, partial output-channel
+    tiles and ragged planes, split and not, on OIHW and prepacked weights
+    (the same bits) and against the oracle."""
+    torch = torch_cuda()
+    ones = [v for v in range(ilpm.num_variants(ilpm.PATH_IGEMM)) if ilpm.variant_info(ilpm.PATH_IGEMM, v)["k"] == 1]
+    assert ones
+    ran = set()
+    for seed, (c_in, h, w_, c_out) in enumerate([(4, 5, 9, 20), (12, 7, 7, 33), (36, 9, 11, 70), (68, 4, 6, 17),
+                                                 (132, 7, 7, 48)]):
+        x, w, b = random_case(7500 + 10 * seed, c_in, h, w_, c_out, 1, bias=(seed % 2 == 0))
+        ref, sab = oracle.conv2d_f64(x, w, b, 1, 0)
+        for v in ones:
+            for splits in (1, 0, 2):
+                try:
+                    plan = ilpm.plan_variant(c_in, h, w_, c_out, 1, 1, 0, ilpm.PATH_IGEMM, v, splits)
+                except ilpm.IlpmError:
+                    continue
+                note(f"[1x1] {(c_in, h, w_, c_out)} {describe(plan)}")
+                got = run_conv(x, w, b, 1, 0, plan=plan)
+                assert_matches(got, ref, sab, c_in, 1, f"1x1 {(c_in, h, w_, c_out)} {describe(plan)}")
+                _prepacked_vs_oihw(ilpm, x, w, b, 1, 0, plan, f"1x1 {(c_in, h, w_, c_out)}")
+                ran.add(v)
+    assert ran == set(ones)
+
+
 def test_wide_channels_many_splits(ilpm):
     """Channel counts that are not multiples of the stage size, split into
     uneven ranges across many workgroups (the small-layer plans).  The values
