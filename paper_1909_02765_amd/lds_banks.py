@@ -21,8 +21,9 @@ pattern measured:
 
 The implicit-GEMM kernel's B operand (the input halo) is read with
 ds_read_b32: lane (g, l) of a 16x16x4 step reads channel plane g (offset
-g*PL words) at tile pixel p = 16n + l of its block n (row p / TW, column
-p % TW, so word (p / TW)*S*HCP + (p % TW)*S within the plane); tap and
+g*PL words; g*G4*PL for the 1x1 variants whose lanes take consecutive
+channels, `lstep` = G4) at tile pixel p = 16n + l of its block n (row p / TW,
+column p % TW, so word (p / TW)*S*HCP + (p % TW)*S within the plane); tap and
 channel-group offsets shift every lane alike and do not change the cost.
 `b_read_costs` gives the cost of each block's read for a layout (row pitch
 HCP, plane pitch PL), `best_halo_layout` the smallest conflict-free layout.
@@ -58,7 +59,7 @@ def conflicts_b64(addrs):
     return tot
 
 
-def b_read_addresses(TH, TW, S, HCP, PL, NWP, wp, n):
+def b_read_addresses(TH, TW, S, HCP, PL, NWP, wp, n, lstep=1):
     """Word addresses of the B read of pixel block n of wave group wp, lanes 0..63
     (the tail block of a 16q + t pixel tile, t <= 4, reads t pixels, lanes
     16kq + 4cg + j on pixel j; lanes past the tile read pixel 0)."""
@@ -72,14 +73,15 @@ def b_read_addresses(TH, TW, S, HCP, PL, NWP, wp, n):
         p = (wp * nb + n) * 16 + ((l & 3) if (tail4 and n == nb - 1) else l)
         if p >= npix:
             p = 0
-        out.append(g * PL + (p // TW) * S * HCP + (p % TW) * S)
+        out.append(g * lstep * PL + (p // TW) * S * HCP + (p % TW) * S)
     return out
 
 
-def b_read_costs(TH, TW, S, HCP, PL, NWP=1):
+def b_read_costs(TH, TW, S, HCP, PL, NWP=1, lstep=1):
     npix = TH * TW
     nb = (npix + 16 * NWP - 1) // (16 * NWP)
-    return [conflicts_b32(b_read_addresses(TH, TW, S, HCP, PL, NWP, wp, n)) for wp in range(NWP) for n in range(nb)]
+    return [conflicts_b32(b_read_addresses(TH, TW, S, HCP, PL, NWP, wp, n, lstep))
+            for wp in range(NWP) for n in range(nb)]
 
 
 def tight_layout(TH, TW, S, K):
